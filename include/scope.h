@@ -1,0 +1,191 @@
+/*
+ * scope.h -- C ABI of the SCOPE sparse self-attention layer for video DiTs,
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The layer (one attention head at a fixed layer and denoising step; heads
+ * are independent and batched) takes post-3D-RoPE queries and keys Q, K and
+ * values V, each N x d, and computes
+ *   1. a k-means clustering of the queries in the full d-dim space   (Sec. 3.2, Eq. 2)
+ *   2. a k-means clustering of each RoPE key subspace T, H, W and the
+ *      composite code of every key                                   (Sec. 3.3, Eq. 3-4)
+ *   3. score tables P_m = Qbar^m (U^m)^T and lookup-and-sum proxy
+ *      logits for every (query cluster, key)                         (Eq. 5-6, Alg. 2)
+ *   4. hybrid Top-p / fixed Top-k counts, the online per-head Top-k
+ *      and each cluster's final key set                              (Eq. 7-10, Alg. 3)
+ *   5. exact attention of each query cluster over its key set        (Eq. 11, Alg. 1)
+ * Calls 1-5 below map one-to-one onto these stages.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Every array argument is a DEVICE pointer owned by the caller.  Scalars
+ *    and the shape/size structs are host values.  The library allocates and
+ *    frees nothing and holds no global mutable state.
+ *  - Every call is asynchronous: it validates its arguments on the host,
+ *    enqueues its kernels on `stream` (a hipStream_t; NULL = the default
+ *    stream) and returns.  No call synchronises or copies to the host.
+ *  - Layout: Q, K, V, O are [heads][n][d], d contiguous, in the dtype of the
+ *    shape (fp32 or bf16).  All other arrays are dense, row-major, with the
+ *    shapes given per argument, heads outermost.
+ *  - Workspace: calls that need scratch take `workspace` (256-byte aligned)
+ *    of at least scope_workspace_size() bytes.  One workspace serves every
+ *    call, but two calls that may run concurrently need two workspaces.
+ *  - Errors: argument checks run before any GPU work and return
+ *    SCOPE_ERR_INVALID_ARGUMENT (bad value), SCOPE_ERR_UNSUPPORTED (valid but
+ *    outside what the kernels implement) or SCOPE_ERR_WORKSPACE; nothing is
+ *    enqueued then.  A failed kernel launch returns SCOPE_ERR_HIP.  Faults
+ *    that depend on data are OR-ed into the optional device word
+ *    `dev_status` (bit 0: non-finite input; bit 1: |x| >= 2^22, outside the
+ *    fixed-point range of the k-means means; bit 2: an initial row index out
+ *    of range, replaced by the default row).  Nothing aborts or prints.
+ *  - Determinism: every output is bitwise reproducible run to run and
+ *    independent of launch geometry; calls 1-4 are bit-exact with respect to
+ *    the canonical arithmetic defined under each call.
+ */
+#ifndef SCOPE_H
+#define SCOPE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SCOPE_ABI_VERSION 1
+
+typedef enum {
+  SCOPE_OK = 0,
+  SCOPE_ERR_INVALID_ARGUMENT = 1,
+  SCOPE_ERR_UNSUPPORTED = 2,
+  SCOPE_ERR_WORKSPACE = 3,
+  SCOPE_ERR_HIP = 4
+} scope_status;
+
+typedef enum { SCOPE_F32 = 0, SCOPE_BF16 = 1 } scope_dtype;
+
+/* Problem shape.  The three RoPE channel ranges I_T, I_H, I_W (Sec. 3.3;
+ * App. A: disjoint, covering all d channels) are given as (offset, length)
+ * in T, H, W order.  Supported: 1 <= heads <= 65535, 1 <= n <= 2^24, 2 <= d <= 128
+ * for clustering/scoring/selection, d in {64, 128} for attention.         */
+typedef struct {
+  int32_t heads;
+  int32_t n;
+  int32_t d;
+  int32_t dtype; /* scope_dtype of Q, K, V and O */
+  int32_t range_off[3];
+  int32_t range_len[3];
+} scope_shape;
+
+int32_t scope_abi_version(void);
+const char *scope_status_string(int32_t status);
+
+/* Workspace bytes that suffice for every call below with these sizes.     */
+int32_t scope_workspace_size(const scope_shape *shape, int32_t c_q,
+                             const int32_t c_m[3], size_t *bytes);
+
+/* 1. Query clustering (Sec. 3.2, Eq. 2; Alg. 1 first step).
+ * Lloyd k-means of each head's n query rows into c_q clusters, `iters`
+ * iterations of (assign, update), starting from rows init_idx[h][0..c_q)
+ * (distinct rows in [0, n); NULL selects row floor((2r+1) n / (2 c_q))).
+ * Canonical arithmetic: assign = argmin_r fl(||u_r||^2 - 2<x,u_r>) with
+ * every dot product an fp32 fma chain in ascending channel order and ties
+ * to the lowest r; update = exact int64 sums of rint(x * 2^24) over the
+ * members, one fp64 division by count * 2^24, rounded to fp32; an empty
+ * cluster keeps its centroid.  The iteration ends on an update, so each
+ * returned centroid is the mean of its returned members (Eq. 2).
+ * Outputs: q_centroids [heads][c_q][d] fp32; assign g [heads][n];
+ * counts n_c [heads][c_q]; offsets [heads][c_q+1] (exclusive prefix sum of
+ * counts); perm [heads][n] = the members of each cluster in ascending token
+ * order, cluster after cluster (the query permutation of Alg. 1).
+ * Requires 1 <= c_q <= min(n, 1024), 1 <= iters.                           */
+int32_t scope_cluster_queries(const scope_shape *shape, const void *q,
+                              int32_t c_q, int32_t iters,
+                              const int32_t *init_idx, float *q_centroids,
+                              int32_t *assign, int32_t *counts,
+                              int32_t *offsets, int32_t *perm,
+                              void *workspace, size_t ws_bytes,
+                              int32_t *dev_status, void *stream);
+
+/* 2. Key subspace clustering (Sec. 3.3, Eq. 3-4; Alg. 2 k-means step).
+ * For m = T, H, W: k-means of K[:, I_m] into c_m[m] centroids with the same
+ * canonical arithmetic as call 1, from rows init_idx[h][m][0..c_m[m])
+ * (row stride init_stride >= max c_m; NULL = default rows), `iters`
+ * iterations followed by one more assignment, so every code is the exact
+ * argmin against the returned codebook (Eq. 3).
+ * Outputs: k_centroids [heads][sum_m c_m*len_m] fp32, per head U^T, U^H,
+ * U^W back to back, each [c_m][len_m]; codes [heads][n] composite code
+ * z_T | z_H << 10 | z_W << 20 (Eq. 4).  Requires 1 <= c_m <= min(n, 1024). */
+int32_t scope_cluster_key_subspaces(const scope_shape *shape, const void *k,
+                                    const int32_t c_m[3], int32_t iters,
+                                    const int32_t *init_idx,
+                                    int32_t init_stride, float *k_centroids,
+                                    uint32_t *codes, void *workspace,
+                                    size_t ws_bytes, int32_t *dev_status,
+                                    void *stream);
+
+/* 3. Score tables and proxy logits (Eq. 5-6; Alg. 2 scoring steps).
+ * tables [heads][c_q][C_T+C_H+C_W]: P_m[c][r] = <qbar_c[I_m], u_r^m> as an
+ * fp32 fma chain over the subspace channels in ascending order, columns
+ * T then H then W.  If `scores` is not NULL it receives the proxy logits
+ * [heads][c_q][n]: s_cj = fl(fl(fl(P_T[c][zT] + P_H[c][zH]) + P_W[c][zW])
+ * * fl32(1/sqrt(d))) + 0.0 (the + 0 maps -0 to +0).  scope_select computes
+ * the same logits on the fly, so `scores` is only needed for inspection.   */
+int32_t scope_proxy_scores(const scope_shape *shape, const float *q_centroids,
+                           int32_t c_q, const float *k_centroids,
+                           const int32_t c_m[3], const uint32_t *codes,
+                           float *tables, float *scores, void *stream);
+
+/* 4. Key selection (Eq. 7-10; Alg. 3).
+ * Logits come from `scores` if not NULL, else from (tables, codes) exactly
+ * as in call 3.  For each cluster c, with pi_c = keys by logit descending,
+ * ties by ascending key index:
+ *   t_c   = the shortest prefix of pi_c whose softmax mass reaches rho
+ *           (Eq. 7), rho >= 1 keeps all n; the softmax mass of key j is
+ *           E_j = fixexp(s_cj - max_j s_cj), an integer in units of 2^-32
+ *           (z = y*fl32(log2 e); 0 below z = -40; 2^frac(z) by a degree-7
+ *           Taylor polynomial in fp32), and the prefix must reach
+ *           ceil(rho * sum_j E_j) computed exactly;
+ *   b_c   = max(t_c, k_fix)                                         (Eq. 8)
+ *   k_head= ceil(sum_c n_c b_c / sum_c n_c), exact integers         (Eq. 9)
+ *   r_c   = max(b_c, k_head), S_c = the first r_c keys of pi_c      (Eq. 10)
+ * Outputs: base_counts b [heads][c_q]; topp_counts t [heads][c_q] (may be
+ * NULL); k_head [heads]; sel_counts r [heads][c_q]; sel_idx
+ * [heads][c_q][n]: S_c in ascending key order in the first r_c entries
+ * (the rest are left untouched).  counts are the n_c of call 1.
+ * Requires 0 < rho <= 1 (finite) and 1 <= k_fix <= n.                      */
+int32_t scope_select(const scope_shape *shape, int32_t c_q,
+                     const int32_t c_m[3], const float *scores,
+                     const float *tables, const uint32_t *codes,
+                     const int32_t *counts, float rho, int32_t k_fix,
+                     int32_t *base_counts, int32_t *topp_counts,
+                     int32_t *k_head, int32_t *sel_counts, int32_t *sel_idx,
+                     void *workspace, size_t ws_bytes, void *stream);
+
+/* 5. Sparse attention over the selected keys (Eq. 11; Alg. 1 last step).
+ * For every cluster c and every query i in perm[offsets[c] .. offsets[c+1]):
+ *   O[i] = softmax(q_i K[S_c]^T * scale) V[S_c],  S_c = sel_idx[c][0..r_c),
+ * with the original Q, K, V rows (scale <= 0 selects 1/sqrt(d)).  Products
+ * run on bf16 matrix cores with fp32 accumulation and an fp32 online
+ * softmax; fp32 inputs are rounded to bf16 on load; O is written in the
+ * input dtype, in original token order.  A cluster with r_c = 0 writes 0.
+ * Dense attention (Eq. 1) is the special case of one cluster holding all
+ * queries (c_q = 1, offsets = {0, n}, perm = identity) and all keys.
+ * Index arrays are clamped to their valid ranges on the device, so bad
+ * indices cannot fault; requires d in {64, 128}.                           */
+int32_t scope_sparse_attention(const scope_shape *shape, const void *q,
+                               const void *k, const void *v, int32_t c_q,
+                               const int32_t *offsets, const int32_t *perm,
+                               const int32_t *sel_counts,
+                               const int32_t *sel_idx, float scale, void *o,
+                               void *workspace, size_t ws_bytes, void *stream);
+
+/* Diagnostic: the selection's fixed-point exponential (call 4) applied to
+ * y[0..count) (y <= 0), results in out[0..count).                          */
+int32_t scope_debug_fixexp(const float *y, uint64_t *out, int64_t count,
+                           void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SCOPE_H */

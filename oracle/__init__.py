@@ -47,6 +47,8 @@ def lib():
         L.oracle_num_threads.restype = I
         L.oracle_kmeans.argtypes = [P, ctypes.c_long, I, I, I, I, P, I, P, P, P]
         L.oracle_group.argtypes = [P, I, I, P, P, P]
+        L.oracle_assign_rows.argtypes = [P, ctypes.c_long, I, I, P, I, P]
+        L.oracle_mean_rows.argtypes = [P, ctypes.c_long, I, I, P, I, P, P]
         L.oracle_cluster_queries.argtypes = [I, I, I, P, I, I, P, P, P, P, P, P]
         L.oracle_cluster_key_subspaces.argtypes = [I, I, I, P, P, P, P, I, P, I,
                                                    P, P, P]
@@ -63,7 +65,8 @@ def lib():
                                     P]
         L.oracle_attention.argtypes = [I, I, I, P, P, P, I, P, P, P, P,
                                        ctypes.c_double, P, P]
-        for name in ("oracle_kmeans", "oracle_group", "oracle_cluster_queries",
+        for name in ("oracle_kmeans", "oracle_group", "oracle_assign_rows",
+                     "oracle_mean_rows", "oracle_cluster_queries",
                      "oracle_cluster_key_subspaces", "oracle_tables",
                      "oracle_proxy_scores", "oracle_select", "oracle_attention"):
             getattr(L, name).restype = I
@@ -103,6 +106,28 @@ def kmeans(X, C, iters, init, final_assign):
                              int(final_assign), _p(U), _p(a), _p(cnt))
     _check(st, "kmeans")
     return U, a, cnt, st
+
+
+def assign_rows(X, U):
+    """One canonical assignment step: nearest centroid of every row of X."""
+    X = _c(X, np.float32)
+    U = _c(U, np.float32)
+    a = np.empty(X.shape[0], np.int32)
+    _check(lib().oracle_assign_rows(_p(X), X.shape[1], X.shape[0], X.shape[1],
+                                    _p(U), U.shape[0], _p(a)), "assign_rows")
+    return a
+
+
+def mean_rows(X, assign, U_prev):
+    """One canonical update step: fixed-point means of the members."""
+    X = _c(X, np.float32)
+    U = np.array(U_prev, dtype=np.float32, copy=True)
+    a = _c(assign, np.int32)
+    cnt = np.empty(U.shape[0], np.int32)
+    st = lib().oracle_mean_rows(_p(X), X.shape[1], X.shape[0], X.shape[1], _p(a),
+                                U.shape[0], _p(U), _p(cnt))
+    _check(st, "mean_rows")
+    return U, cnt
 
 
 def group(assign, C):

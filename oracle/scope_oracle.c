@@ -437,3 +437,21 @@ int oracle_attention(int heads, int n, int d, const float *q, const float *k,
   }
   return OR_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Single steps of the k-means above, exposed so that properties of a full-
+ * size clustering can be checked one row or one cluster at a time.         */
+int oracle_assign_rows(const float *X, long ldx, int n, int dx, const float *U,
+                       int C, int *assign) {
+  if (n < 0 || dx < 1 || C < 1) return OR_ERR_ARG;
+  km_assign(X, ldx, n, dx, U, C, assign);
+  return OR_OK;
+}
+
+int oracle_mean_rows(const float *X, long ldx, int n, int dx, const int *assign,
+                     int C, float *U, int *counts) {
+  if (n < 0 || dx < 1 || C < 1) return OR_ERR_ARG;
+  for (int i = 0; i < n; ++i)
+    if (assign[i] < 0 || assign[i] >= C) return OR_ERR_ARG;
+  return km_update(X, ldx, n, dx, assign, C, U, counts);
+}

@@ -1,0 +1,390 @@
+// C ABI of the SCOPE layer: argument validation, workspace layout and the
+// order of kernel launches for each stage.  Validation runs before any HIP
+// call, so every error path works on a host without a GPU.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "../../include/scope.h"
+#include "kernels.h"
+
+namespace {
+
+using scope::KmProblem;
+
+constexpr size_t kAlign = 256;
+constexpr int kMaxC = 1024;
+constexpr int kMaxN = 1 << 24;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Carves consecutive aligned regions out of a workspace (or just sizes them
+// when base is null).
+struct Carver {
+  char *base;
+  size_t used = 0;
+  explicit Carver(void *b) : base(static_cast<char *>(b)) {}
+  template <typename T>
+  T *take(size_t count) {
+    T *p = base ? reinterpret_cast<T *>(base + used) : nullptr;
+    used = align_up(used + count * sizeof(T));
+    return p;
+  }
+};
+
+int32_t check_shape(const scope_shape *s) {
+  if (!s) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (s->heads < 1 || s->n < 1 || s->d < 2) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (s->dtype != SCOPE_F32 && s->dtype != SCOPE_BF16) return SCOPE_ERR_UNSUPPORTED;
+  if (s->n > kMaxN || s->d > 128 || s->heads > 65535) return SCOPE_ERR_UNSUPPORTED;
+  if (static_cast<long long>(s->heads) * s->n > (1LL << 31) - 1) return SCOPE_ERR_UNSUPPORTED;
+  int total = 0;
+  for (int m = 0; m < 3; ++m) {
+    const int o = s->range_off[m], l = s->range_len[m];
+    if (l < 1 || o < 0 || o + l > s->d) return SCOPE_ERR_INVALID_ARGUMENT;
+    for (int q = 0; q < m; ++q) {
+      const int o2 = s->range_off[q], l2 = s->range_len[q];
+      if (o < o2 + l2 && o2 < o + l) return SCOPE_ERR_INVALID_ARGUMENT;  // overlap
+    }
+    total += l;
+  }
+  if (total != s->d) return SCOPE_ERR_INVALID_ARGUMENT;  // must cover all d
+  return SCOPE_OK;
+}
+
+int32_t check_cm(const scope_shape *s, const int32_t *c_m) {
+  if (!c_m) return SCOPE_ERR_INVALID_ARGUMENT;
+  for (int m = 0; m < 3; ++m) {
+    if (c_m[m] < 1 || c_m[m] > s->n) return SCOPE_ERR_INVALID_ARGUMENT;
+    if (c_m[m] > kMaxC) return SCOPE_ERR_UNSUPPORTED;
+  }
+  return SCOPE_OK;
+}
+
+int32_t check_cq(const scope_shape *s, int32_t c_q) {
+  if (c_q < 1 || c_q > s->n) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (c_q > kMaxC) return SCOPE_ERR_UNSUPPORTED;
+  return SCOPE_OK;
+}
+
+int32_t check_ws(void *ws, size_t bytes, size_t need) {
+  if (need == 0) return SCOPE_OK;
+  if (!ws || bytes < need) return SCOPE_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign) return SCOPE_ERR_WORKSPACE;
+  return SCOPE_OK;
+}
+
+bool aligned_data(const void *p, const scope_shape *s) {
+  return reinterpret_cast<uintptr_t>(p) % (s->dtype == SCOPE_BF16 ? 2 : 4) == 0;
+}
+
+// --- workspace layouts (each call's regions start at offset 0) -----------
+struct QueryWs {
+  int32_t *hist, *rel;
+  int64_t *partial;
+  int splits;
+};
+size_t query_ws(const scope_shape *s, int c_q, void *base, QueryWs *w) {
+  Carver cv(base);
+  const int nch = scope::km_nchunks(s->n);
+  const int splits = scope::km_splits(s->n, c_q, s->d);
+  QueryWs q;
+  q.hist = cv.take<int32_t>(static_cast<size_t>(s->heads) * nch * c_q);
+  q.rel = cv.take<int32_t>(static_cast<size_t>(s->heads) * nch * c_q);
+  q.partial = cv.take<int64_t>(static_cast<size_t>(s->heads) * c_q * splits * s->d);
+  q.splits = splits;
+  if (w) *w = q;
+  return cv.used;
+}
+
+struct KeyWs {
+  int32_t *assign3, *perm3;
+  int32_t *counts[3], *offsets[3], *hist[3], *rel[3];
+  int64_t *partial[3];
+  int splits[3];
+};
+size_t key_ws(const scope_shape *s, const int32_t *c_m, void *base, KeyWs *w) {
+  Carver cv(base);
+  const int nch = scope::km_nchunks(s->n);
+  const size_t H = static_cast<size_t>(s->heads);
+  KeyWs k;
+  k.assign3 = cv.take<int32_t>(H * 3 * s->n);
+  k.perm3 = cv.take<int32_t>(H * 3 * s->n);
+  for (int m = 0; m < 3; ++m) {
+    const int C = c_m[m], dx = s->range_len[m];
+    k.splits[m] = scope::km_splits(s->n, C, dx);
+    k.counts[m] = cv.take<int32_t>(H * C);
+    k.offsets[m] = cv.take<int32_t>(H * (C + 1));
+    k.hist[m] = cv.take<int32_t>(H * nch * C);
+    k.rel[m] = cv.take<int32_t>(H * nch * C);
+    k.partial[m] = cv.take<int64_t>(H * C * k.splits[m] * dx);
+  }
+  if (w) *w = k;
+  return cv.used;
+}
+
+struct SelectWs {
+  float *row_max;
+  uint32_t *row_state;
+};
+size_t select_ws(const scope_shape *s, int c_q, void *base, SelectWs *w) {
+  Carver cv(base);
+  SelectWs sw;
+  sw.row_max = cv.take<float>(static_cast<size_t>(s->heads) * c_q);
+  sw.row_state = cv.take<uint32_t>(static_cast<size_t>(s->heads) * c_q * 4);
+  if (w) *w = sw;
+  return cv.used;
+}
+
+size_t attn_ws(const scope_shape *s, int c_q, void *base, int4 **items) {
+  Carver cv(base);
+  int4 *it = cv.take<int4>(static_cast<size_t>(s->heads) * scope::attn_items_per_head(s->n, c_q));
+  if (items) *items = it;
+  return cv.used;
+}
+
+#define SCOPE_TRY(expr)                                  \
+  do {                                                   \
+    if ((expr) != hipSuccess) return SCOPE_ERR_HIP;      \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+int32_t scope_abi_version(void) { return SCOPE_ABI_VERSION; }
+
+const char *scope_status_string(int32_t status) {
+  switch (status) {
+    case SCOPE_OK: return "ok";
+    case SCOPE_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case SCOPE_ERR_UNSUPPORTED: return "unsupported argument";
+    case SCOPE_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
+    case SCOPE_ERR_HIP: return "HIP launch failure";
+    default: return "unknown status";
+  }
+}
+
+int32_t scope_workspace_size(const scope_shape *shape, int32_t c_q,
+                             const int32_t c_m[3], size_t *bytes) {
+  int32_t st = check_shape(shape);
+  if (st) return st;
+  if ((st = check_cq(shape, c_q))) return st;
+  if ((st = check_cm(shape, c_m))) return st;
+  if (!bytes) return SCOPE_ERR_INVALID_ARGUMENT;
+  size_t need = query_ws(shape, c_q, nullptr, nullptr);
+  size_t k = key_ws(shape, c_m, nullptr, nullptr);
+  size_t s = select_ws(shape, c_q, nullptr, nullptr);
+  size_t a = attn_ws(shape, c_q, nullptr, nullptr);
+  if (k > need) need = k;
+  if (s > need) need = s;
+  if (a > need) need = a;
+  *bytes = need;
+  return SCOPE_OK;
+}
+
+int32_t scope_cluster_queries(const scope_shape *shape, const void *q,
+                              int32_t c_q, int32_t iters,
+                              const int32_t *init_idx, float *q_centroids,
+                              int32_t *assign, int32_t *counts,
+                              int32_t *offsets, int32_t *perm, void *workspace,
+                              size_t ws_bytes, int32_t *dev_status,
+                              void *stream) {
+  int32_t st = check_shape(shape);
+  if (st) return st;
+  if ((st = check_cq(shape, c_q))) return st;
+  if (iters < 1) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (!q || !q_centroids || !assign || !counts || !offsets || !perm)
+    return SCOPE_ERR_INVALID_ARGUMENT;
+  if (!aligned_data(q, shape)) return SCOPE_ERR_INVALID_ARGUMENT;
+  QueryWs w;
+  const size_t need = query_ws(shape, c_q, nullptr, nullptr);
+  if ((st = check_ws(workspace, ws_bytes, need))) return st;
+  query_ws(shape, c_q, workspace, &w);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int n = shape->n, d = shape->d;
+  KmProblem p{};
+  p.x = q;
+  p.bf16 = shape->dtype == SCOPE_BF16;
+  p.x_head_stride = static_cast<size_t>(n) * d;
+  p.ld = d;
+  p.col0 = 0;
+  p.dx = d;
+  p.n = n;
+  p.C = c_q;
+  p.u = q_centroids;
+  p.u_head_stride = static_cast<size_t>(c_q) * d;
+  p.assign = assign;
+  p.a_head_stride = static_cast<size_t>(n);
+  p.counts = counts;
+  p.offsets = offsets;
+  p.perm = perm;
+  p.chunk_hist = w.hist;
+  p.chunk_rel = w.rel;
+  p.partial = w.partial;
+  p.splits = w.splits;
+  p.heads = shape->heads;
+  SCOPE_TRY(scope::km_init(p, init_idx, c_q, dev_status, s));
+  for (int it = 0; it < iters; ++it) {
+    SCOPE_TRY(scope::km_assign(p, true, s));
+    SCOPE_TRY(scope::km_group(p, s));
+    SCOPE_TRY(scope::km_update(p, dev_status, s));
+  }
+  return SCOPE_OK;
+}
+
+int32_t scope_cluster_key_subspaces(const scope_shape *shape, const void *k,
+                                    const int32_t c_m[3], int32_t iters,
+                                    const int32_t *init_idx,
+                                    int32_t init_stride, float *k_centroids,
+                                    uint32_t *codes, void *workspace,
+                                    size_t ws_bytes, int32_t *dev_status,
+                                    void *stream) {
+  int32_t st = check_shape(shape);
+  if (st) return st;
+  if ((st = check_cm(shape, c_m))) return st;
+  if (iters < 1) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (!k || !k_centroids || !codes) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (!aligned_data(k, shape)) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (init_idx) {
+    const int mx = c_m[0] > c_m[1] ? (c_m[0] > c_m[2] ? c_m[0] : c_m[2])
+                                   : (c_m[1] > c_m[2] ? c_m[1] : c_m[2]);
+    if (init_stride < mx) return SCOPE_ERR_INVALID_ARGUMENT;
+  }
+  const size_t need = key_ws(shape, c_m, nullptr, nullptr);
+  if ((st = check_ws(workspace, ws_bytes, need))) return st;
+  KeyWs w;
+  key_ws(shape, c_m, workspace, &w);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int n = shape->n, d = shape->d;
+  KmProblem p[3];
+  size_t ucol = 0;
+  size_t per_head = 0;
+  for (int m = 0; m < 3; ++m) per_head += static_cast<size_t>(c_m[m]) * shape->range_len[m];
+  for (int m = 0; m < 3; ++m) {
+    KmProblem &pm = p[m];
+    pm = KmProblem{};
+    pm.x = k;
+    pm.bf16 = shape->dtype == SCOPE_BF16;
+    pm.x_head_stride = static_cast<size_t>(n) * d;
+    pm.ld = d;
+    pm.col0 = shape->range_off[m];
+    pm.dx = shape->range_len[m];
+    pm.n = n;
+    pm.C = c_m[m];
+    pm.u = k_centroids + ucol;
+    pm.u_head_stride = per_head;
+    pm.assign = w.assign3 + static_cast<size_t>(m) * n;
+    pm.a_head_stride = static_cast<size_t>(3) * n;
+    pm.counts = w.counts[m];
+    pm.offsets = w.offsets[m];
+    pm.perm = w.perm3 + static_cast<size_t>(m) * n;
+    pm.chunk_hist = w.hist[m];
+    pm.chunk_rel = w.rel[m];
+    pm.partial = w.partial[m];
+    pm.splits = w.splits[m];
+    pm.heads = shape->heads;
+    ucol += static_cast<size_t>(c_m[m]) * pm.dx;
+    const int32_t *init = init_idx ? init_idx + static_cast<size_t>(m) * init_stride : nullptr;
+    // init rows of head h, subspace m live at init_idx[(h*3 + m)*init_stride]
+    SCOPE_TRY(scope::km_init(pm, init, 3 * init_stride, dev_status, s));
+  }
+  for (int it = 0; it < iters; ++it)
+    for (int m = 0; m < 3; ++m) {
+      SCOPE_TRY(scope::km_assign(p[m], true, s));
+      SCOPE_TRY(scope::km_group(p[m], s));
+      SCOPE_TRY(scope::km_update(p[m], dev_status, s));
+    }
+  for (int m = 0; m < 3; ++m) SCOPE_TRY(scope::km_assign(p[m], false, s));
+  SCOPE_TRY(scope::km_pack_codes(w.assign3, static_cast<size_t>(3) * n, n, n,
+                                 shape->heads, codes, s));
+  return SCOPE_OK;
+}
+
+int32_t scope_proxy_scores(const scope_shape *shape, const float *q_centroids,
+                           int32_t c_q, const float *k_centroids,
+                           const int32_t c_m[3], const uint32_t *codes,
+                           float *tables, float *scores, void *stream) {
+  int32_t st = check_shape(shape);
+  if (st) return st;
+  if ((st = check_cq(shape, c_q))) return st;
+  if ((st = check_cm(shape, c_m))) return st;
+  if (!q_centroids || !k_centroids || !tables) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (scores && !codes) return SCOPE_ERR_INVALID_ARGUMENT;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  SCOPE_TRY(scope::score_tables(shape->heads, shape->d, shape->range_off,
+                                shape->range_len, c_q, c_m, q_centroids,
+                                k_centroids, tables, s));
+  if (scores)
+    SCOPE_TRY(scope::score_logits(shape->heads, shape->n, shape->d, c_q, c_m,
+                                  tables, codes, scores, s));
+  return SCOPE_OK;
+}
+
+int32_t scope_select(const scope_shape *shape, int32_t c_q,
+                     const int32_t c_m[3], const float *scores,
+                     const float *tables, const uint32_t *codes,
+                     const int32_t *counts, float rho, int32_t k_fix,
+                     int32_t *base_counts, int32_t *topp_counts,
+                     int32_t *k_head, int32_t *sel_counts, int32_t *sel_idx,
+                     void *workspace, size_t ws_bytes, void *stream) {
+  int32_t st = check_shape(shape);
+  if (st) return st;
+  if ((st = check_cq(shape, c_q))) return st;
+  if ((st = check_cm(shape, c_m))) return st;
+  if (!scores && (!tables || !codes)) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (!counts || !base_counts || !k_head || !sel_counts || !sel_idx)
+    return SCOPE_ERR_INVALID_ARGUMENT;
+  if (!(rho > 0.0f && rho <= 1.0f)) return SCOPE_ERR_INVALID_ARGUMENT;  // rejects NaN
+  if (k_fix < 1 || k_fix > shape->n) return SCOPE_ERR_INVALID_ARGUMENT;
+  const size_t need = select_ws(shape, c_q, nullptr, nullptr);
+  if ((st = check_ws(workspace, ws_bytes, need))) return st;
+  SelectWs w;
+  select_ws(shape, c_q, workspace, &w);
+  SCOPE_TRY(scope::select_run(shape->heads, shape->n, c_q, c_m, shape->d,
+                              scores, tables, codes, counts, rho, k_fix,
+                              base_counts, topp_counts, k_head, sel_counts,
+                              sel_idx, w.row_max, w.row_state,
+                              static_cast<hipStream_t>(stream)));
+  return SCOPE_OK;
+}
+
+int32_t scope_sparse_attention(const scope_shape *shape, const void *q,
+                               const void *k, const void *v, int32_t c_q,
+                               const int32_t *offsets, const int32_t *perm,
+                               const int32_t *sel_counts,
+                               const int32_t *sel_idx, float scale, void *o,
+                               void *workspace, size_t ws_bytes,
+                               void *stream) {
+  int32_t st = check_shape(shape);
+  if (st) return st;
+  if (shape->d != 64 && shape->d != 128) return SCOPE_ERR_UNSUPPORTED;
+  if (c_q < 1 || c_q > shape->n) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (!q || !k || !v || !o || !offsets || !perm || !sel_counts || !sel_idx)
+    return SCOPE_ERR_INVALID_ARGUMENT;
+  // rows are read and written as 16-byte vectors
+  for (const void *p : {q, k, v, static_cast<const void *>(o)})
+    if (reinterpret_cast<uintptr_t>(p) % 16) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (!(scale == scale) || isinf(scale)) return SCOPE_ERR_INVALID_ARGUMENT;
+  const size_t need = attn_ws(shape, c_q, nullptr, nullptr);
+  if ((st = check_ws(workspace, ws_bytes, need))) return st;
+  int4 *items = nullptr;
+  attn_ws(shape, c_q, workspace, &items);
+  const float sc = scale > 0.0f ? scale
+                                : static_cast<float>(1.0 / sqrt(static_cast<double>(shape->d)));
+  SCOPE_TRY(scope::attention_run(shape->heads, shape->n, shape->d,
+                                 shape->dtype == SCOPE_BF16, q, k, v, o, c_q,
+                                 offsets, perm, sel_counts, sel_idx, sc, items,
+                                 static_cast<hipStream_t>(stream)));
+  return SCOPE_OK;
+}
+
+int32_t scope_debug_fixexp(const float *y, uint64_t *out, int64_t count,
+                           void *stream) {
+  if (count < 0 || (count > 0 && (!y || !out))) return SCOPE_ERR_INVALID_ARGUMENT;
+  SCOPE_TRY(scope::debug_fixexp(y, out, count, static_cast<hipStream_t>(stream)));
+  return SCOPE_OK;
+}
+
+}  // extern "C"

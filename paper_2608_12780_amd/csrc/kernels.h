@@ -1,0 +1,69 @@
+// Host-side launchers of the SCOPE kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace scope {
+
+// One batch of k-means problems, one problem per head: the rows of
+// X[h] (row stride ld elements, channels col0 .. col0+dx) clustered into C
+// centroids U[h] ([C][dx] fp32).
+struct KmProblem {
+  const void *x;          // element type given by bf16 flag
+  bool bf16;
+  size_t x_head_stride;   // elements between heads
+  int ld, col0, dx, n, C;
+  float *u;               // centroids of head 0 (this subspace)
+  size_t u_head_stride;   // floats between heads
+  int32_t *assign;        // [heads][n] (a_head_stride apart)
+  size_t a_head_stride;
+  int32_t *counts;        // [heads][C]
+  int32_t *offsets;       // [heads][C+1]
+  int32_t *perm;          // [heads][n]
+  int32_t *chunk_hist;    // [heads][nchunks][C]
+  int32_t *chunk_rel;     // [heads][nchunks][C]
+  int64_t *partial;       // [heads][C][splits][dx]
+  int splits;
+  int heads;
+};
+
+constexpr int kAssignBlock = 256;  // points per assign block == grouping chunk
+
+inline int km_nchunks(int n) { return (n + kAssignBlock - 1) / kAssignBlock; }
+int km_splits(int n, int C, int dx);
+
+hipError_t km_init(const KmProblem &p, const int32_t *init, int init_stride,
+                   int32_t *status, hipStream_t s);
+hipError_t km_assign(const KmProblem &p, bool with_hist, hipStream_t s);
+hipError_t km_group(const KmProblem &p, hipStream_t s);
+hipError_t km_update(const KmProblem &p, int32_t *status, hipStream_t s);
+hipError_t km_pack_codes(const int32_t *a3, size_t a_head_stride,
+                         size_t a_sub_stride, int n, int heads,
+                         uint32_t *codes, hipStream_t s);
+
+hipError_t score_tables(int heads, int d, const int *off, const int *len,
+                        int c_q, const int *c_m, const float *qc,
+                        const float *kc, float *tables, hipStream_t s);
+hipError_t score_logits(int heads, int n, int d, int c_q, const int *c_m,
+                        const float *tables, const uint32_t *codes,
+                        float *scores, hipStream_t s);
+
+hipError_t select_run(int heads, int n, int c_q, const int *c_m, int d,
+                      const float *scores, const float *tables,
+                      const uint32_t *codes, const int32_t *counts, float rho,
+                      int k_fix, int32_t *base, int32_t *topp, int32_t *k_head,
+                      int32_t *sel_counts, int32_t *sel_idx, float *row_max,
+                      uint32_t *row_state, hipStream_t s);
+hipError_t debug_fixexp(const float *y, uint64_t *out, int64_t count,
+                        hipStream_t s);
+
+int attn_items_per_head(int n, int c_q);
+hipError_t attention_run(int heads, int n, int d, bool bf16, const void *q,
+                         const void *k, const void *v, void *o, int c_q,
+                         const int32_t *offsets, const int32_t *perm,
+                         const int32_t *sel_counts, const int32_t *sel_idx,
+                         float scale, int4 *items, hipStream_t s);
+
+}  // namespace scope

@@ -1,0 +1,389 @@
+// K-means kernels (Sec. 3.2 Eq. 2 for queries; Sec. 3.3 Eq. 3 for the key
+// subspaces), canonical arithmetic:
+//   assign: argmin_r fl(||u_r||^2 - 2<x, u_r>), dot products as fp32 fma
+//           chains in ascending channel order, ties to the lowest r;
+//   update: exact int64 sums of rint(x * 2^24) over the members, one fp64
+//           division by count * 2^24, rounded to fp32; empty clusters keep
+//           their centroid.
+// Per iteration: assign (+ per-chunk cluster histogram) -> column scan of the
+// histograms -> stable scatter into the cluster-grouped permutation ->
+// partial fixed-point sums per (cluster, split) -> finalize.
+#include <math.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace scope {
+
+namespace {
+
+template <typename T>
+__global__ void km_init_kernel(const T *X, size_t x_hs, int ld, int col0,
+                               int dx, int n, int C, const int32_t *init,
+                               int init_stride, float *U, size_t u_hs,
+                               int32_t *status) {
+  const int r = blockIdx.x, h = blockIdx.y;
+  const int def = static_cast<int>(((2LL * r + 1) * n) / (2LL * C));
+  int row = def;
+  if (init) {
+    row = init[static_cast<size_t>(h) * init_stride + r];
+    if (row < 0 || row >= n) {
+      if (threadIdx.x == 0 && status) atomicOr(status, kStatusBadInit);
+      row = def;
+    }
+  }
+  const T *src = X + h * x_hs + static_cast<size_t>(row) * ld + col0;
+  float *dst = U + h * u_hs + static_cast<size_t>(r) * dx;
+  for (int c = threadIdx.x; c < dx; c += blockDim.x) dst[c] = load_elem(src, c);
+}
+
+// One point per thread, its channels held in registers (zero padded to DXP:
+// a trailing fma(0, 0, acc) leaves the score unchanged).  Centroids are
+// staged through LDS transposed, CB at a time, and read as wave-wide
+// broadcasts.  Scores are compared in ascending centroid order with a
+// strict '<', so ties go to the lowest index.
+template <typename T, int DXP>
+__global__ __launch_bounds__(kAssignBlock) void km_assign_kernel(
+    const T *__restrict__ X, size_t x_hs, int ld, int col0, int dx, int n,
+    const float *__restrict__ U, size_t u_hs, int C, int32_t *assign,
+    size_t a_hs, int32_t *chunk_hist, int nchunks) {
+  constexpr int CB = 64;
+  __shared__ float Ut[DXP][CB];
+  __shared__ float nu_s[CB];
+  __shared__ int hist[1024];
+  const int h = blockIdx.y, t = threadIdx.x;
+  const int i = blockIdx.x * kAssignBlock + t;
+  const bool valid = i < n;
+  const T *xrow = X + h * x_hs + static_cast<size_t>(valid ? i : 0) * ld + col0;
+  float xr[DXP];
+#pragma unroll
+  for (int c = 0; c < DXP; ++c) xr[c] = (c < dx) ? load_elem(xrow, c) : 0.0f;
+  const float *Uh = U + h * u_hs;
+  float best = INFINITY;
+  int arg = 0;
+  for (int r0 = 0; r0 < C; r0 += CB) {
+    __syncthreads();
+    for (int e = t; e < DXP * CB; e += kAssignBlock) {
+      const int rr = e % CB, c = e / CB, r = r0 + rr;
+      Ut[c][rr] = (r < C && c < dx) ? Uh[static_cast<size_t>(r) * dx + c] : 0.0f;
+    }
+    if (t < CB) {
+      const int r = r0 + t;
+      float nu = INFINITY;  // padding centroids never win
+      if (r < C) {
+        const float *u = Uh + static_cast<size_t>(r) * dx;
+        nu = 0.0f;
+        for (int c = 0; c < dx; ++c) nu = fmaf(u[c], u[c], nu);
+      }
+      nu_s[t] = nu;
+    }
+    __syncthreads();
+    const int rend = min(CB, C - r0);
+    for (int rr = 0; rr < rend; rr += 8) {
+      float acc[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) acc[k] = 0.0f;
+#pragma unroll
+      for (int c = 0; c < DXP; ++c) {
+        const float4 u0 = *reinterpret_cast<const float4 *>(&Ut[c][rr]);
+        const float4 u1 = *reinterpret_cast<const float4 *>(&Ut[c][rr + 4]);
+        acc[0] = fmaf(xr[c], u0.x, acc[0]);
+        acc[1] = fmaf(xr[c], u0.y, acc[1]);
+        acc[2] = fmaf(xr[c], u0.z, acc[2]);
+        acc[3] = fmaf(xr[c], u0.w, acc[3]);
+        acc[4] = fmaf(xr[c], u1.x, acc[4]);
+        acc[5] = fmaf(xr[c], u1.y, acc[5]);
+        acc[6] = fmaf(xr[c], u1.z, acc[6]);
+        acc[7] = fmaf(xr[c], u1.w, acc[7]);
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float s = fmaf(-2.0f, acc[k], nu_s[rr + k]);
+        if (s < best) {
+          best = s;
+          arg = r0 + rr + k;
+        }
+      }
+    }
+  }
+  if (valid) assign[h * a_hs + i] = arg;
+  if (chunk_hist) {
+    __syncthreads();
+    for (int r = t; r < C; r += kAssignBlock) hist[r] = 0;
+    __syncthreads();
+    if (valid) atomicAdd(&hist[arg], 1);
+    __syncthreads();
+    int32_t *out = chunk_hist + (static_cast<size_t>(h) * nchunks + blockIdx.x) * C;
+    for (int r = t; r < C; r += kAssignBlock) out[r] = hist[r];
+  }
+}
+
+// Column scan of the chunk histograms: counts[r] and, per chunk, the number
+// of members of r in earlier chunks.  Block = (64-column group, head); each
+// column is split into segments summed in parallel.
+__global__ __launch_bounds__(1024) void km_colscan_kernel(
+    int nchunks, int C, const int32_t *__restrict__ hist, int32_t *rel,
+    int32_t *counts) {
+  __shared__ int seg[1024];
+  const int h = blockIdx.y, t = threadIdx.x;
+  const int c0 = blockIdx.x * 64;
+  const int cols = min(64, C - c0);
+  const int nseg = 1024 / cols;
+  const int col = c0 + t % cols, g = t / cols;
+  const int seglen = (nchunks + nseg - 1) / nseg;
+  const int k0 = g * seglen, k1 = min(nchunks, k0 + seglen);
+  const int32_t *H = hist + static_cast<size_t>(h) * nchunks * C;
+  int sum = 0;
+  if (g < nseg) {
+#pragma unroll 8
+    for (int k = k0; k < k1; ++k) sum += H[static_cast<size_t>(k) * C + col];
+  }
+  seg[t] = sum;
+  __syncthreads();
+  if (t < cols) {
+    int run = 0;
+    for (int gg = 0; gg < nseg; ++gg) {
+      const int v = seg[gg * cols + t];
+      seg[gg * cols + t] = run;
+      run += v;
+    }
+    counts[static_cast<size_t>(h) * C + col] = run;
+  }
+  __syncthreads();
+  if (g < nseg) {
+    int run = seg[t];
+    int32_t *R = rel + static_cast<size_t>(h) * nchunks * C;
+#pragma unroll 8
+    for (int k = k0; k < k1; ++k) {
+      R[static_cast<size_t>(k) * C + col] = run;
+      run += H[static_cast<size_t>(k) * C + col];
+    }
+  }
+}
+
+// Exclusive prefix sum of counts[0..C) into off_s (block of 256 threads).
+__device__ void block_offsets(const int32_t *counts, int C, int *off_s) {
+  __shared__ int wtot[4];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int per = (C + 255) / 256;
+  const int b = t * per;
+  int local = 0;
+  for (int e = 0; e < per; ++e)
+    if (b + e < C) local += counts[b + e];
+  const int incl = wave_incl_scan(local);
+  if (lane == 63) wtot[w] = incl;
+  __syncthreads();
+  int base = 0;
+  for (int ww = 0; ww < w; ++ww) base += wtot[ww];
+  int run = base + incl - local;
+  for (int e = 0; e < per; ++e) {
+    if (b + e < C) {
+      off_s[b + e] = run;
+      run += counts[b + e];
+    }
+  }
+  if (t == 255) off_s[C] = base + incl;
+  __syncthreads();
+}
+
+// Stable scatter: point i of chunk k goes to
+// offsets[a] + (members of a in earlier chunks) + (earlier members in chunk).
+// The in-chunk rank uses an 11-round ballot match per wave plus per-wave
+// counts in LDS.
+__global__ __launch_bounds__(kAssignBlock) void km_scatter_kernel(
+    int n, int C, int nchunks, const int32_t *__restrict__ assign, size_t a_hs,
+    const int32_t *__restrict__ counts, const int32_t *__restrict__ rel,
+    int32_t *offsets, int32_t *perm, size_t p_hs) {
+  __shared__ int off_s[1025];
+  __shared__ int wcnt[4][1024];
+  const int h = blockIdx.y, k = blockIdx.x, t = threadIdx.x;
+  const int lane = t & 63, w = t >> 6;
+  block_offsets(counts + static_cast<size_t>(h) * C, C, off_s);
+  if (k == 0)
+    for (int r = t; r <= C; r += kAssignBlock)
+      offsets[static_cast<size_t>(h) * (C + 1) + r] = off_s[r];
+  const int i = k * kAssignBlock + t;
+  const bool valid = i < n;
+  const int a = valid ? assign[h * a_hs + i] : C;  // C: sentinel, never valid
+  uint64_t same = ~0ull;
+#pragma unroll
+  for (int b = 0; b < 11; ++b) {
+    const bool bit = (a >> b) & 1;
+    const uint64_t bal = __ballot(bit);
+    same &= bit ? bal : ~bal;
+  }
+  const int rank = __popcll(same & ((1ull << lane) - 1ull));
+  const int total = __popcll(same);
+  for (int e = t; e < 4 * C; e += kAssignBlock) wcnt[e / C][e % C] = 0;
+  __syncthreads();
+  if (valid && rank == 0) wcnt[w][a] = total;
+  __syncthreads();
+  if (valid) {
+    int pre = 0;
+    for (int ww = 0; ww < w; ++ww) pre += wcnt[ww][a];
+    const int pos = off_s[a] + rel[(static_cast<size_t>(h) * nchunks + k) * C + a] + pre + rank;
+    if (pos >= 0 && pos < n) perm[h * p_hs + pos] = i;
+  }
+}
+
+// Fixed-point partial sums of split s of cluster r: threads = (row slot,
+// channel); partial[h][r][s][c] = sum over the split's rows of
+// rint(x * 2^24).
+template <typename T>
+__global__ __launch_bounds__(256) void km_partial_kernel(
+    const T *__restrict__ X, size_t x_hs, int ld, int col0, int dx, int C,
+    int splits, const int32_t *__restrict__ offsets,
+    const int32_t *__restrict__ perm, size_t p_hs, int64_t *partial,
+    int32_t *status) {
+  __shared__ long long part[256];
+  const int s = blockIdx.x, r = blockIdx.y, h = blockIdx.z, t = threadIdx.x;
+  const int beg = offsets[static_cast<size_t>(h) * (C + 1) + r];
+  const int cnt = offsets[static_cast<size_t>(h) * (C + 1) + r + 1] - beg;
+  const int lo = beg + static_cast<int>((static_cast<long long>(cnt) * s) / splits);
+  const int hi = beg + static_cast<int>((static_cast<long long>(cnt) * (s + 1)) / splits);
+  const int slots = 256 / dx;
+  const int c = t % dx, slot = t / dx;
+  long long acc = 0;
+  int bad = 0;
+  if (slot < slots) {
+    const T *Xh = X + h * x_hs + col0 + c;
+    const int32_t *P = perm + h * p_hs;
+#pragma unroll 4
+    for (int p = lo + slot; p < hi; p += slots) {
+      const float x = load_elem(Xh, static_cast<size_t>(P[p]) * ld);
+      if (!(fabsf(x) < 4194304.0f)) bad |= isfinite(x) ? kStatusRange : (kStatusRange | kStatusNonFinite);
+      acc += static_cast<long long>(rintf(x * 16777216.0f));
+    }
+  }
+  part[t] = acc;
+  __syncthreads();
+  if (t < dx) {
+    long long tot = 0;
+    for (int g = 0; g < slots; ++g) tot += part[g * dx + t];
+    partial[((static_cast<size_t>(h) * C + r) * splits + s) * dx + t] = tot;
+  }
+  if (bad && status) atomicOr(status, bad);
+}
+
+// U[r][c] = (float)((double)sum / ((double)count * 2^24)); empty r keeps U.
+__global__ void km_finalize_kernel(int C, int dx, int splits,
+                                   const int32_t *__restrict__ offsets,
+                                   const int64_t *__restrict__ partial,
+                                   float *U, size_t u_hs) {
+  const int r = blockIdx.x, h = blockIdx.y;
+  const int cnt = offsets[static_cast<size_t>(h) * (C + 1) + r + 1] -
+                  offsets[static_cast<size_t>(h) * (C + 1) + r];
+  if (cnt <= 0) return;
+  const double den = static_cast<double>(cnt) * 16777216.0;
+  const int64_t *P = partial + (static_cast<size_t>(h) * C + r) * splits * dx;
+  for (int c = threadIdx.x; c < dx; c += blockDim.x) {
+    long long tot = 0;
+    for (int s = 0; s < splits; ++s) tot += P[static_cast<size_t>(s) * dx + c];
+    U[h * u_hs + static_cast<size_t>(r) * dx + c] =
+        static_cast<float>(static_cast<double>(tot) / den);
+  }
+}
+
+__global__ void km_pack_kernel(const int32_t *__restrict__ a3, size_t a_hs,
+                               size_t a_ss, int n, uint32_t *codes) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x, h = blockIdx.y;
+  if (j >= n) return;
+  const int32_t *A = a3 + h * a_hs;
+  codes[static_cast<size_t>(h) * n + j] =
+      static_cast<uint32_t>(A[j]) | (static_cast<uint32_t>(A[a_ss + j]) << 10) |
+      (static_cast<uint32_t>(A[2 * a_ss + j]) << 20);
+}
+
+template <typename T>
+hipError_t assign_dispatch(const KmProblem &p, bool with_hist, hipStream_t s) {
+  const dim3 grid(km_nchunks(p.n), p.heads);
+  const T *x = static_cast<const T *>(p.x);
+  int32_t *hist = with_hist ? p.chunk_hist : nullptr;
+  const int nch = km_nchunks(p.n);
+#define SCOPE_ASSIGN(DXP)                                                      \
+  hipLaunchKernelGGL((km_assign_kernel<T, DXP>), grid, dim3(kAssignBlock), 0, s, \
+                     x, p.x_head_stride, p.ld, p.col0, p.dx, p.n, p.u,          \
+                     p.u_head_stride, p.C, p.assign, p.a_head_stride, hist, nch)
+  if (p.dx <= 16) SCOPE_ASSIGN(16);
+  else if (p.dx <= 32) SCOPE_ASSIGN(32);
+  else if (p.dx <= 48) SCOPE_ASSIGN(48);
+  else if (p.dx <= 64) SCOPE_ASSIGN(64);
+  else SCOPE_ASSIGN(128);
+#undef SCOPE_ASSIGN
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int km_splits(int n, int C, int dx) {
+  const int slots = 256 / dx;
+  const long long avg = (static_cast<long long>(n) + C - 1) / C;
+  long long sp = (avg + 8LL * slots - 1) / (8LL * slots);
+  if (sp < 1) sp = 1;
+  if (sp > 16) sp = 16;
+  return static_cast<int>(sp);
+}
+
+hipError_t km_init(const KmProblem &p, const int32_t *init, int init_stride,
+                   int32_t *status, hipStream_t s) {
+  const dim3 grid(p.C, p.heads);
+  if (p.bf16)
+    hipLaunchKernelGGL(km_init_kernel<uint16_t>, grid, dim3(64), 0, s,
+                       static_cast<const uint16_t *>(p.x), p.x_head_stride,
+                       p.ld, p.col0, p.dx, p.n, p.C, init, init_stride, p.u,
+                       p.u_head_stride, status);
+  else
+    hipLaunchKernelGGL(km_init_kernel<float>, grid, dim3(64), 0, s,
+                       static_cast<const float *>(p.x), p.x_head_stride, p.ld,
+                       p.col0, p.dx, p.n, p.C, init, init_stride, p.u,
+                       p.u_head_stride, status);
+  return hipGetLastError();
+}
+
+hipError_t km_assign(const KmProblem &p, bool with_hist, hipStream_t s) {
+  return p.bf16 ? assign_dispatch<uint16_t>(p, with_hist, s)
+                : assign_dispatch<float>(p, with_hist, s);
+}
+
+hipError_t km_group(const KmProblem &p, hipStream_t s) {
+  const int nch = km_nchunks(p.n);
+  hipLaunchKernelGGL(km_colscan_kernel, dim3((p.C + 63) / 64, p.heads),
+                     dim3(1024), 0, s, nch, p.C, p.chunk_hist, p.chunk_rel,
+                     p.counts);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(km_scatter_kernel, dim3(nch, p.heads), dim3(kAssignBlock),
+                     0, s, p.n, p.C, nch, p.assign, p.a_head_stride, p.counts,
+                     p.chunk_rel, p.offsets, p.perm, p.a_head_stride);
+  return hipGetLastError();
+}
+
+hipError_t km_update(const KmProblem &p, int32_t *status, hipStream_t s) {
+  const dim3 grid(p.splits, p.C, p.heads);
+  if (p.bf16)
+    hipLaunchKernelGGL(km_partial_kernel<uint16_t>, grid, dim3(256), 0, s,
+                       static_cast<const uint16_t *>(p.x), p.x_head_stride,
+                       p.ld, p.col0, p.dx, p.C, p.splits, p.offsets, p.perm,
+                       p.a_head_stride, p.partial, status);
+  else
+    hipLaunchKernelGGL(km_partial_kernel<float>, grid, dim3(256), 0, s,
+                       static_cast<const float *>(p.x), p.x_head_stride, p.ld,
+                       p.col0, p.dx, p.C, p.splits, p.offsets, p.perm,
+                       p.a_head_stride, p.partial, status);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(km_finalize_kernel, dim3(p.C, p.heads), dim3(128), 0, s,
+                     p.C, p.dx, p.splits, p.offsets, p.partial, p.u,
+                     p.u_head_stride);
+  return hipGetLastError();
+}
+
+hipError_t km_pack_codes(const int32_t *a3, size_t a_head_stride,
+                         size_t a_sub_stride, int n, int heads,
+                         uint32_t *codes, hipStream_t s) {
+  hipLaunchKernelGGL(km_pack_kernel, dim3((n + 255) / 256, heads), dim3(256),
+                     0, s, a3, a_head_stride, a_sub_stride, n, codes);
+  return hipGetLastError();
+}
+
+}  // namespace scope

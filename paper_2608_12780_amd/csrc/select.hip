@@ -1,0 +1,382 @@
+// Key selection (Sec. 3.4, Eq. 7-10; Alg. 3) without sorting.
+//
+// Ranking pi_c = keys by proxy logit descending, ties by ascending index.
+// base kernel (one block per (cluster, head)):
+//   M = max logit; every key's softmax mass E_j = fixexp(s_j - M) in units
+//   of 2^-32; total and the exact target T = ceil(rho * total);
+//   radix selection of the logit where the descending cumulative mass first
+//   reaches T: one coarse pass over a monotone binning of M - s, then three
+//   digit passes (11/11/10 bits) over the order-preserving key bits inside
+//   the crossing bin; keys that tie at the crossing logit all carry the same
+//   mass E*, so the Top-p count is t = (#keys above) + ceil((T - mass
+//   above) / E*) (Eq. 7); b = max(t, k_fix) (Eq. 8).
+// head kernel: k_head = ceil(sum n_c b_c / sum n_c) in integers (Eq. 9),
+//   r_c = max(b_c, k_head) (Eq. 10).
+// final kernel: the rank-r_c logit by the same radix selection on counts
+//   (reused from the base kernel when r_c == t_c), then an ordered block
+//   compaction emits every key above it plus the lowest-index ties, in
+//   ascending key order.
+#include <math.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace scope {
+
+namespace {
+
+constexpr int kSelBlock = 1024;
+constexpr int kCoarseBins = 2048;
+constexpr int kMaxTable = 3072;
+
+__device__ __forceinline__ int coarse_bin(float y) {
+  // y = s - M <= 0; monotone non-increasing in s
+  return static_cast<int>(fminf(-y * 64.0f, static_cast<float>(kCoarseBins - 1)));
+}
+
+template <typename T>
+__device__ T block_excl_scan(T v, T *total) {
+  __shared__ T ws[kSelBlock / 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const T incl = wave_incl_scan(v);
+  if (lane == 63) ws[w] = incl;
+  __syncthreads();
+  T base = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < kSelBlock / 64; ++i) {
+    const T x = ws[i];
+    if (i < w) base += x;
+    tot += x;
+  }
+  __syncthreads();
+  *total = tot;
+  return base + incl - v;
+}
+
+template <typename T>
+__device__ T block_sum(T v) {
+  T tot;
+  block_excl_scan(v, &tot);
+  return tot;
+}
+
+__device__ float block_max(float v) {
+  __shared__ float ws[kSelBlock / 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  v = wave_max(v);
+  if (lane == 0) ws[w] = v;
+  __syncthreads();
+  float m = ws[0];
+#pragma unroll
+  for (int i = 1; i < kSelBlock / 64; ++i) m = fmaxf(m, ws[i]);
+  __syncthreads();
+  return m;
+}
+
+struct Crossing {
+  int bin;
+  uint32_t cnt_before;
+  uint64_t mass_before;
+};
+
+// Smallest bin b with base + sum_{b' <= b} w[b'] >= target, where w is the
+// mass histogram (BY_MASS) or the count histogram.  Two bins per thread.
+template <bool BY_MASS>
+__device__ Crossing find_crossing(const uint32_t *hc, const uint64_t *hm,
+                                  int nbins, uint64_t base, uint64_t target) {
+  __shared__ Crossing res;
+  const int t = threadIdx.x;
+  const int b0 = 2 * t, b1 = 2 * t + 1;
+  const uint32_t c0 = b0 < nbins ? hc[b0] : 0u, c1 = b1 < nbins ? hc[b1] : 0u;
+  uint64_t w0, w1;
+  if (BY_MASS) {
+    w0 = b0 < nbins ? hm[b0] : 0ull;
+    w1 = b1 < nbins ? hm[b1] : 0ull;
+  } else {
+    w0 = c0;
+    w1 = c1;
+  }
+  uint64_t wt;
+  uint32_t ct;
+  const uint64_t wex = block_excl_scan<uint64_t>(w0 + w1, &wt);
+  const uint32_t cex = block_excl_scan<uint32_t>(c0 + c1, &ct);
+  const uint64_t a0 = base + wex, a1 = a0 + w0, a2 = a1 + w1;
+  if (a0 < target && target <= a1) res = Crossing{b0, cex, wex};
+  if (a1 < target && target <= a2) res = Crossing{b1, cex + c0, wex + w0};
+  __syncthreads();
+  const Crossing out = res;
+  __syncthreads();
+  return out;
+}
+
+template <bool FUSED>
+struct LogitSource {
+  const float *P;        // LDS table row (fused) or global score row
+  const uint32_t *codes; // [n] of this head
+  int cT, cTH, cs;
+  float sigma;
+  __device__ __forceinline__ float operator()(int j) const {
+    if (FUSED) return proxy_logit(P, cT, cTH, cs, codes[j], sigma);
+    return P[j];
+  }
+};
+
+template <bool FUSED>
+__device__ LogitSource<FUSED> make_source(float *lut, int h, int c, int n,
+                                          int c_q, const int *cm, float sigma,
+                                          const float *scores,
+                                          const float *tables,
+                                          const uint32_t *codes) {
+  LogitSource<FUSED> src;
+  src.cT = cm[0];
+  src.cTH = cm[0] + cm[1];
+  src.cs = cm[0] + cm[1] + cm[2];
+  src.sigma = sigma;
+  src.codes = codes + static_cast<size_t>(h) * n;
+  if (FUSED) {
+    const int cs = cm[0] + cm[1] + cm[2];
+    const float *row = tables + (static_cast<size_t>(h) * c_q + c) * cs;
+    for (int e = threadIdx.x; e < cs; e += kSelBlock) lut[e] = row[e];
+    __syncthreads();
+    src.P = lut;
+  } else {
+    src.P = scores + (static_cast<size_t>(h) * c_q + c) * n;
+  }
+  return src;
+}
+
+struct Cm3 {
+  int v[3];
+};
+
+// Radix refinement inside coarse bin `cbin`: three digit passes over the
+// order-preserving key.  BY_MASS selects the mass target (Top-p) or the
+// count target (rank).  Returns the exact crossing key and what lies above.
+template <bool FUSED, bool BY_MASS>
+__device__ void refine(const LogitSource<FUSED> &src, int n, float M, int cbin,
+                       uint64_t target, uint32_t *hc, uint64_t *hm,
+                       uint32_t *key_out, uint32_t *cnt_above,
+                       uint64_t *mass_above) {
+  const int shifts[3] = {21, 10, 0};
+  const int widths[3] = {11, 11, 10};
+  uint32_t prefix = 0, pmask = 0;
+  for (int round = 0; round < 3; ++round) {
+    const int sh = shifts[round], nb = 1 << widths[round];
+    for (int b = threadIdx.x; b < nb; b += kSelBlock) {
+      hc[b] = 0;
+      if (BY_MASS) hm[b] = 0;
+    }
+    __syncthreads();
+    for (int j = threadIdx.x; j < n; j += kSelBlock) {
+      const float s = src(j);
+      const float y = s - M;
+      if (coarse_bin(y) != cbin) continue;
+      const uint32_t key = desc_key(s);
+      if ((key & pmask) != prefix) continue;
+      const int dig = (key >> sh) & (nb - 1);
+      atomicAdd(&hc[dig], 1u);
+      if (BY_MASS) {
+        const uint64_t e = fixexp(y);
+        if (e) atomicAdd(reinterpret_cast<unsigned long long *>(&hm[dig]),
+                         static_cast<unsigned long long>(e));
+      }
+    }
+    __syncthreads();
+    const uint64_t base = BY_MASS ? *mass_above : static_cast<uint64_t>(*cnt_above);
+    const Crossing x = find_crossing<BY_MASS>(hc, hm, nb, base, target);
+    *cnt_above += x.cnt_before;
+    if (BY_MASS) *mass_above += x.mass_before;
+    prefix |= static_cast<uint32_t>(x.bin) << sh;
+    pmask |= static_cast<uint32_t>(nb - 1) << sh;
+  }
+  *key_out = prefix;
+}
+
+template <bool FUSED>
+__global__ __launch_bounds__(kSelBlock) void select_base_kernel(
+    int n, int c_q, Cm3 cm, float sigma, const float *__restrict__ scores,
+    const float *__restrict__ tables, const uint32_t *__restrict__ codes,
+    float rho, int k_fix, int32_t *base_counts, int32_t *topp_counts,
+    float *row_max, uint32_t *row_state) {
+  __shared__ float lut[kMaxTable];
+  __shared__ uint32_t hc[kCoarseBins];
+  __shared__ uint64_t hm[kCoarseBins];
+  const int c = blockIdx.x, h = blockIdx.y;
+  const size_t row = static_cast<size_t>(h) * c_q + c;
+  const LogitSource<FUSED> src =
+      make_source<FUSED>(lut, h, c, n, c_q, cm.v, sigma, scores, tables, codes);
+  float mloc = -INFINITY;
+  for (int j = threadIdx.x; j < n; j += kSelBlock) mloc = fmaxf(mloc, src(j));
+  const float M = block_max(mloc);
+  int t_p = n;
+  uint32_t key_star = 0, above_star = 0;
+  if (rho < 1.0f) {
+    for (int b = threadIdx.x; b < kCoarseBins; b += kSelBlock) {
+      hc[b] = 0;
+      hm[b] = 0;
+    }
+    __syncthreads();
+    uint64_t tloc = 0;
+    for (int j = threadIdx.x; j < n; j += kSelBlock) {
+      const float y = src(j) - M;
+      const int bin = coarse_bin(y);
+      const uint64_t e = fixexp(y);
+      atomicAdd(&hc[bin], 1u);
+      if (e) atomicAdd(reinterpret_cast<unsigned long long *>(&hm[bin]),
+                       static_cast<unsigned long long>(e));
+      tloc += e;
+    }
+    const uint64_t tot = block_sum<uint64_t>(tloc);
+    __syncthreads();
+    const uint64_t T = mass_target(rho, tot);
+    const Crossing x = find_crossing<true>(hc, hm, kCoarseBins, 0, T);
+    uint32_t cnt_above = x.cnt_before;
+    uint64_t mass_above = x.mass_before;
+    refine<FUSED, true>(src, n, M, x.bin, T, hc, hm, &key_star, &cnt_above,
+                        &mass_above);
+    const float s_star = desc_key_value(key_star);
+    const uint64_t e_star = fixexp(s_star - M);
+    const uint64_t need = (T - mass_above + e_star - 1) / e_star;
+    t_p = static_cast<int>(cnt_above + need);
+    above_star = cnt_above;
+  }
+  if (threadIdx.x == 0) {
+    const int b = t_p > k_fix ? t_p : k_fix;
+    base_counts[row] = b;
+    if (topp_counts) topp_counts[row] = t_p;
+    row_max[row] = M;
+    row_state[4 * row + 0] = static_cast<uint32_t>(t_p);
+    row_state[4 * row + 1] = key_star;
+    row_state[4 * row + 2] = above_star;
+  }
+}
+
+__global__ __launch_bounds__(kSelBlock) void select_head_kernel(
+    int c_q, const int32_t *__restrict__ counts, const int32_t *__restrict__ base,
+    int32_t *k_head, int32_t *sel_counts) {
+  const int h = blockIdx.x;
+  uint64_t num = 0, den = 0;
+  for (int c = threadIdx.x; c < c_q; c += kSelBlock) {
+    const uint64_t nc = static_cast<uint64_t>(max(counts[static_cast<size_t>(h) * c_q + c], 0));
+    num += nc * static_cast<uint64_t>(base[static_cast<size_t>(h) * c_q + c]);
+    den += nc;
+  }
+  num = block_sum<uint64_t>(num);
+  den = block_sum<uint64_t>(den);
+  const int kh = den ? static_cast<int>((num + den - 1) / den) : 0;
+  if (threadIdx.x == 0) k_head[h] = kh;
+  for (int c = threadIdx.x; c < c_q; c += kSelBlock) {
+    const int b = base[static_cast<size_t>(h) * c_q + c];
+    sel_counts[static_cast<size_t>(h) * c_q + c] = b > kh ? b : kh;
+  }
+}
+
+template <bool FUSED>
+__global__ __launch_bounds__(kSelBlock) void select_final_kernel(
+    int n, int c_q, Cm3 cm, float sigma, const float *__restrict__ scores,
+    const float *__restrict__ tables, const uint32_t *__restrict__ codes,
+    const int32_t *__restrict__ sel_counts, const float *__restrict__ row_max,
+    const uint32_t *__restrict__ row_state, int32_t *sel_idx) {
+  __shared__ float lut[kMaxTable];
+  __shared__ uint32_t hc[kCoarseBins];
+  const int c = blockIdx.x, h = blockIdx.y;
+  const size_t row = static_cast<size_t>(h) * c_q + c;
+  int32_t *out = sel_idx + row * n;
+  const int r = min(sel_counts[row], n);
+  if (r >= n) {
+    for (int j = threadIdx.x; j < n; j += kSelBlock) out[j] = j;
+    return;
+  }
+  if (r <= 0) return;
+  const LogitSource<FUSED> src =
+      make_source<FUSED>(lut, h, c, n, c_q, cm.v, sigma, scores, tables, codes);
+  const float M = row_max[row];
+  uint32_t key_r, above;
+  if (static_cast<uint32_t>(r) == row_state[4 * row + 0]) {
+    key_r = row_state[4 * row + 1];
+    above = row_state[4 * row + 2];
+  } else {
+    for (int b = threadIdx.x; b < kCoarseBins; b += kSelBlock) hc[b] = 0;
+    __syncthreads();
+    for (int j = threadIdx.x; j < n; j += kSelBlock)
+      atomicAdd(&hc[coarse_bin(src(j) - M)], 1u);
+    __syncthreads();
+    const Crossing x = find_crossing<false>(hc, nullptr, kCoarseBins, 0,
+                                            static_cast<uint64_t>(r));
+    above = x.cnt_before;
+    uint64_t unused = 0;
+    refine<FUSED, false>(src, n, M, x.bin, static_cast<uint64_t>(r), hc,
+                         nullptr, &key_r, &above, &unused);
+  }
+  const uint32_t need = static_cast<uint32_t>(r) - above;
+  uint32_t out_run = 0, ties_run = 0;
+  for (int j0 = 0; j0 < n; j0 += kSelBlock) {
+    const int j = j0 + threadIdx.x;
+    uint32_t a = 0, tie = 0;
+    if (j < n) {
+      const uint32_t key = desc_key(src(j));
+      a = key < key_r;
+      tie = key == key_r;
+    }
+    uint32_t tot;
+    const uint32_t ex = block_excl_scan<uint32_t>((tie << 16) | a, &tot);
+    const uint32_t a_pre = ex & 0xFFFFu, t_pre = ex >> 16;
+    const uint32_t remaining = need > ties_run ? need - ties_run : 0u;
+    if (a || (tie && t_pre < remaining))
+      out[out_run + a_pre + min(t_pre, remaining)] = j;
+    out_run += (tot & 0xFFFFu) + min(tot >> 16, remaining);
+    ties_run += tot >> 16;
+  }
+}
+
+__global__ void fixexp_kernel(const float *y, uint64_t *out, int64_t count) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < count) out[i] = fixexp(y[i]);
+}
+
+}  // namespace
+
+hipError_t select_run(int heads, int n, int c_q, const int *c_m, int d,
+                      const float *scores, const float *tables,
+                      const uint32_t *codes, const int32_t *counts, float rho,
+                      int k_fix, int32_t *base, int32_t *topp, int32_t *k_head,
+                      int32_t *sel_counts, int32_t *sel_idx, float *row_max,
+                      uint32_t *row_state, hipStream_t s) {
+  Cm3 cm{{c_m[0], c_m[1], c_m[2]}};
+  const float sigma = static_cast<float>(1.0 / sqrt(static_cast<double>(d)));
+  const dim3 grid(c_q, heads), block(kSelBlock);
+  if (scores)
+    hipLaunchKernelGGL(select_base_kernel<false>, grid, block, 0, s, n, c_q, cm,
+                       sigma, scores, tables, codes, rho, k_fix, base, topp,
+                       row_max, row_state);
+  else
+    hipLaunchKernelGGL(select_base_kernel<true>, grid, block, 0, s, n, c_q, cm,
+                       sigma, scores, tables, codes, rho, k_fix, base, topp,
+                       row_max, row_state);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(select_head_kernel, dim3(heads), block, 0, s, c_q, counts,
+                     base, k_head, sel_counts);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (scores)
+    hipLaunchKernelGGL(select_final_kernel<false>, grid, block, 0, s, n, c_q, cm,
+                       sigma, scores, tables, codes, sel_counts, row_max,
+                       row_state, sel_idx);
+  else
+    hipLaunchKernelGGL(select_final_kernel<true>, grid, block, 0, s, n, c_q, cm,
+                       sigma, scores, tables, codes, sel_counts, row_max,
+                       row_state, sel_idx);
+  return hipGetLastError();
+}
+
+hipError_t debug_fixexp(const float *y, uint64_t *out, int64_t count,
+                        hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  const int64_t blocks = (count + 255) / 256;
+  hipLaunchKernelGGL(fixexp_kernel, dim3(static_cast<unsigned>(blocks)),
+                     dim3(256), 0, s, y, out, count);
+  return hipGetLastError();
+}
+
+}  // namespace scope

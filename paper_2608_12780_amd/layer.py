@@ -1,0 +1,123 @@
+"""The SCOPE layer as five library calls on buffers allocated once.
+
+ScopeLayer owns every output and the workspace for one problem size and runs
+Alg. 1 end to end through the C ABI: query clustering, key-subspace
+clustering, score tables, selection and sparse attention.  Nothing here
+computes; it allocates device memory and sequences the calls.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import binding as B
+
+
+class ScopeLayer:
+    def __init__(self, heads, n, d, ranges, c_q, c_m, iters, rho, k_fix,
+                 dtype="bf16", device="cuda", materialize_scores=False):
+        self.heads, self.n, self.d = int(heads), int(n), int(d)
+        self.ranges = (tuple(map(int, ranges[0])), tuple(map(int, ranges[1])))
+        self.c_q = int(c_q)
+        self.c_m = tuple(int(c) for c in c_m)
+        self.iters, self.rho, self.k_fix = int(iters), float(rho), int(k_fix)
+        self.dtype = B.BF16 if dtype == "bf16" else B.F32
+        self.tdtype = torch.bfloat16 if self.dtype == B.BF16 else torch.float32
+        self.shape = B.make_shape(heads, n, d, self.dtype, self.ranges)
+        H, N, D, C = self.heads, self.n, self.d, self.c_q
+        cs = sum(self.c_m)
+        per_head = sum(self.c_m[m] * self.ranges[1][m] for m in range(3))
+        i32 = dict(dtype=torch.int32, device=device)
+        f32 = dict(dtype=torch.float32, device=device)
+        self.q_centroids = torch.empty(H, C, D, **f32)
+        self.assign = torch.empty(H, N, **i32)
+        self.counts = torch.empty(H, C, **i32)
+        self.offsets = torch.empty(H, C + 1, **i32)
+        self.perm = torch.empty(H, N, **i32)
+        self.k_centroids = torch.empty(H, per_head, **f32)
+        self.codes = torch.empty(H, N, **i32)
+        self.tables = torch.empty(H, C, cs, **f32)
+        self.scores = torch.empty(H, C, N, **f32) if materialize_scores else None
+        self.base_counts = torch.empty(H, C, **i32)
+        self.topp_counts = torch.empty(H, C, **i32)
+        self.k_head = torch.empty(H, **i32)
+        self.sel_counts = torch.empty(H, C, **i32)
+        self.sel_idx = torch.empty(H, C, N, **i32)
+        self.out = torch.empty(H, N, D, dtype=self.tdtype, device=device)
+        self.workspace = B.alloc_workspace(self.shape, C, self.c_m, device)
+        self.status = torch.zeros(1, **i32)
+
+    # the five stages -------------------------------------------------------
+    def cluster_queries(self, q, init_q=None, stream=None):
+        B.scope_cluster_queries(self.shape, q, self.c_q, self.iters, init_q,
+                                self.q_centroids, self.assign, self.counts,
+                                self.offsets, self.perm, self.workspace,
+                                self.status, stream)
+
+    def cluster_keys(self, k, init_k=None, stream=None):
+        stride = init_k.shape[-1] if init_k is not None else 0
+        B.scope_cluster_key_subspaces(self.shape, k, self.c_m, self.iters,
+                                      init_k, stride, self.k_centroids,
+                                      self.codes, self.workspace, self.status,
+                                      stream)
+
+    def proxy_scores(self, stream=None):
+        B.scope_proxy_scores(self.shape, self.q_centroids, self.c_q,
+                             self.k_centroids, self.c_m, self.codes,
+                             self.tables, self.scores, stream)
+
+    def select(self, stream=None, use_scores=False):
+        B.scope_select(self.shape, self.c_q, self.c_m,
+                       self.scores if use_scores else None, self.tables,
+                       self.codes, self.counts, self.rho, self.k_fix,
+                       self.base_counts, self.topp_counts, self.k_head,
+                       self.sel_counts, self.sel_idx, self.workspace, stream)
+
+    def attend(self, q, k, v, scale=0.0, stream=None):
+        B.scope_sparse_attention(self.shape, q, k, v, self.c_q, self.offsets,
+                                 self.perm, self.sel_counts, self.sel_idx,
+                                 scale, self.out, self.workspace, stream)
+
+    def forward(self, q, k, v, init_q=None, init_k=None, stream=None,
+                marks=None):
+        """Runs the layer; `marks(i)` (if given) is called before stage i and
+        after the last one, e.g. to record timing events."""
+        steps = (lambda: self.cluster_queries(q, init_q, stream),
+                 lambda: self.cluster_keys(k, init_k, stream),
+                 lambda: self.proxy_scores(stream),
+                 lambda: self.select(stream),
+                 lambda: self.attend(q, k, v, 0.0, stream))
+        for i, f in enumerate(steps):
+            if marks:
+                marks(i)
+            f()
+        if marks:
+            marks(len(steps))
+        return self.out
+
+
+class DenseAttention:
+    """Dense attention (Eq. 1) through the same attention call: one cluster
+    holding every query, whose key set is every key."""
+
+    def __init__(self, heads, n, d, dtype="bf16", device="cuda"):
+        self.heads, self.n, self.d = int(heads), int(n), int(d)
+        self.dtype = B.BF16 if dtype == "bf16" else B.F32
+        tdt = torch.bfloat16 if self.dtype == B.BF16 else torch.float32
+        split = (d // 3 // 2 * 2, d // 3 // 2 * 2)
+        ln = (split[0], split[1], d - split[0] - split[1])
+        self.shape = B.make_shape(heads, n, d, self.dtype,
+                                  ((0, ln[0], ln[0] + ln[1]), ln))
+        i32 = dict(dtype=torch.int32, device=device)
+        H, N = self.heads, self.n
+        self.offsets = torch.tensor([0, N], **i32).repeat(H, 1).contiguous()
+        self.perm = torch.arange(N, **i32).repeat(H, 1).contiguous()
+        self.sel_counts = torch.full((H, 1), N, **i32)
+        self.sel_idx = torch.arange(N, **i32).repeat(H, 1).reshape(H, 1, N).contiguous()
+        self.out = torch.empty(H, N, d, dtype=tdt, device=device)
+        self.workspace = B.alloc_workspace(self.shape, 1, (1, 1, 1), device)
+
+    def forward(self, q, k, v, scale=0.0, stream=None):
+        B.scope_sparse_attention(self.shape, q, k, v, 1, self.offsets,
+                                 self.perm, self.sel_counts, self.sel_idx,
+                                 scale, self.out, self.workspace, stream)
+        return self.out

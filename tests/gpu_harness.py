@@ -1,0 +1,94 @@
+"""Shared helpers of the GPU tests: run the library on generated inputs and
+compare with the oracle.  Imported only by tests marked `gpu`."""
+from __future__ import annotations
+
+import math
+import sys
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2608_12780_amd import inputs
+from paper_2608_12780_amd.layer import DenseAttention, ScopeLayer
+
+# Attention tolerance (bf16 matrix products, fp32 softmax): max |o - ref| and
+# sum |o - ref| / sum |ref| over the compared elements.
+MAX_ABS = 2e-2
+MEAN_REL = 1e-2
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_device(x: inputs.LayerInputs, device="cuda"):
+    """Q, K, V on the GPU in the workload's storage dtype."""
+    if x.cfg.dtype == "bf16":
+        conv = lambda b: torch.from_numpy(b.view(np.int16)).to(device).view(torch.bfloat16)
+        return conv(x.q_bits), conv(x.k_bits), conv(x.v_bits)
+    return (torch.from_numpy(x.q).to(device), torch.from_numpy(x.k).to(device),
+            torch.from_numpy(x.v).to(device))
+
+
+def bf16_round(a: np.ndarray) -> np.ndarray:
+    return inputs.bf16_widen(inputs.bf16_bits(a))
+
+
+def make_layer(cfg: inputs.LayerConfig, heads=None, materialize=True, **over):
+    a = dict(heads=cfg.heads if heads is None else heads, n=cfg.n, d=cfg.d,
+             ranges=cfg.ranges, c_q=cfg.c_q, c_m=(cfg.c_m,) * 3, iters=cfg.iters,
+             rho=cfg.rho, k_fix=cfg.k_fix, dtype=cfg.dtype,
+             materialize_scores=materialize)
+    a.update(over)
+    return ScopeLayer(**a)
+
+
+def run_gpu(layer: ScopeLayer, x: inputs.LayerInputs, use_scores=False):
+    q, k, v = to_device(x)
+    iq = torch.from_numpy(x.init_q).cuda()
+    ik = torch.from_numpy(x.init_k).cuda()
+    layer.cluster_queries(q, iq)
+    layer.cluster_keys(k, ik)
+    layer.proxy_scores()
+    layer.select(use_scores=use_scores)
+    layer.attend(q, k, v)
+    torch.cuda.synchronize()
+    g = lambda t: None if t is None else t.cpu().numpy()
+    return dict(centroids=g(layer.q_centroids), assign=g(layer.assign),
+                counts=g(layer.counts), offsets=g(layer.offsets),
+                perm=g(layer.perm), k_centroids=g(layer.k_centroids),
+                codes=g(layer.codes).view(np.uint32), tables=g(layer.tables),
+                scores=g(layer.scores), base=g(layer.base_counts),
+                topp=g(layer.topp_counts), k_head=g(layer.k_head),
+                sel_counts=g(layer.sel_counts), sel_idx=g(layer.sel_idx),
+                out=layer.out.float().cpu().numpy(), status=int(layer.status.item()))
+
+
+def oracle_all(x: inputs.LayerInputs, c_q, c_m, iters, rho, k_fix):
+    return oracle.layer(x.q, x.k, x.v, x.cfg.ranges, c_q, c_m, iters, x.init_q,
+                        x.init_k, rho, k_fix)
+
+
+def assert_same_selection(gpu, ref_sel):
+    assert np.array_equal(gpu["base"], ref_sel["base_counts"])
+    assert np.array_equal(gpu["topp"], ref_sel["topp"])
+    assert np.array_equal(gpu["k_head"], ref_sel["k_head"])
+    assert np.array_equal(gpu["sel_counts"], ref_sel["sel_counts"])
+    H, C, _ = ref_sel["sel_idx"].shape
+    for h in range(H):
+        for c in range(C):
+            r = int(ref_sel["sel_counts"][h, c])
+            assert np.array_equal(gpu["sel_idx"][h, c, :r], ref_sel["sel_idx"][h, c, :r]), (h, c)
+
+
+def attention_error(out, ref):
+    diff = np.abs(out.astype(np.float64) - ref.astype(np.float64))
+    return float(diff.max()), float(diff.sum() / max(np.abs(ref).sum(), 1e-30))
+
+
+def assert_attention_close(out, ref):
+    mx, mr = attention_error(out, ref)
+    assert mx <= MAX_ABS and mr <= MEAN_REL, (mx, mr)
+    return mx, mr

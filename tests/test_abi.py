@@ -1,0 +1,154 @@
+"""The C ABI on a host without a GPU: the library loads, exports every entry
+point include/scope.h declares, and rejects bad arguments before touching
+the GPU (fake device pointers are never dereferenced on these paths)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_12780_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+OK, INVALID, UNSUPPORTED, WORKSPACE = 0, 1, 2, 3
+FAKE = ctypes.c_void_p(1 << 20)     # never dereferenced by validation
+
+
+def declared_entry_points():
+    hdr = open(os.path.join(ROOT, "include", "scope.h")).read()
+    return re.findall(r"^\w[\w\s\*]*?\b(scope_\w+)\s*\(", hdr, re.M)
+
+
+def hy_shape(**kw):
+    a = dict(heads=24, n=118800, d=128, dtype=B.BF16,
+             ranges=((0, 16, 72), (16, 56, 56)))
+    a.update(kw)
+    return B.make_shape(a["heads"], a["n"], a["d"], a["dtype"], a["ranges"])
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_entry_points()
+    assert set(names) == set(B.ENTRY_POINTS)
+    L = B.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert L.scope_abi_version() == 1
+
+
+def test_status_strings():
+    for s in (OK, INVALID, UNSUPPORTED, WORKSPACE, 4, 99):
+        assert isinstance(B.status_string(s), str) and B.status_string(s)
+
+
+def ws_size(shape, c_q=256, c_m=(128, 128, 128)):
+    out = ctypes.c_size_t(0)
+    st = B.lib().scope_workspace_size(ctypes.byref(shape), c_q,
+                                      (ctypes.c_int32 * 3)(*c_m), ctypes.byref(out))
+    return st, out.value
+
+
+def test_workspace_size_and_shape_validation():
+    st, size = ws_size(hy_shape())
+    assert st == OK and 10 ** 7 < size < 10 ** 9 and size % 256 == 0
+    bad = [
+        (hy_shape(heads=0), INVALID),
+        (hy_shape(n=0), INVALID),
+        (hy_shape(d=256, ranges=((0, 16, 72), (16, 56, 184))), UNSUPPORTED),
+        (hy_shape(dtype=7), UNSUPPORTED),
+        (hy_shape(ranges=((0, 16, 72), (16, 56, 50))), INVALID),     # not covering d
+        (hy_shape(ranges=((0, 10, 72), (16, 56, 56))), INVALID),     # overlap
+        (hy_shape(ranges=((0, 16, 72), (16, 0, 56))), INVALID),      # empty range
+        (hy_shape(ranges=((0, 16, 100), (16, 56, 56))), INVALID),    # out of d
+    ]
+    for shape, want in bad:
+        assert ws_size(shape)[0] == want
+    assert ws_size(hy_shape(), c_q=0)[0] == INVALID
+    assert ws_size(hy_shape(), c_q=2048)[0] == UNSUPPORTED
+    assert ws_size(hy_shape(), c_m=(128, 0, 128))[0] == INVALID
+    assert ws_size(hy_shape(), c_m=(128, 2000, 128))[0] == UNSUPPORTED
+    assert ws_size(hy_shape(n=100), c_q=101)[0] == INVALID          # C > n
+
+
+def call_queries(shape, c_q=256, iters=10, ws=FAKE, ws_bytes=1 << 40, q=FAKE):
+    return B.lib().scope_cluster_queries(
+        ctypes.byref(shape), q, c_q, iters, None, FAKE, FAKE, FAKE, FAKE, FAKE,
+        ws, ws_bytes, None, None)
+
+
+def test_cluster_queries_validation():
+    sh = hy_shape()
+    assert call_queries(sh, iters=0) == INVALID
+    assert call_queries(sh, c_q=0) == INVALID
+    assert call_queries(sh, q=None) == INVALID
+    assert call_queries(sh, ws=None) == WORKSPACE
+    assert call_queries(sh, ws_bytes=16) == WORKSPACE
+    assert call_queries(sh, ws=ctypes.c_void_p((1 << 20) + 8)) == WORKSPACE
+    assert call_queries(sh, q=ctypes.c_void_p((1 << 20) + 1)) == INVALID
+
+
+def test_cluster_keys_validation():
+    L = B.lib()
+    sh = hy_shape()
+    cm = (ctypes.c_int32 * 3)(128, 128, 128)
+
+    def call(c_m=cm, iters=10, init=None, stride=0, ws_bytes=1 << 40):
+        return L.scope_cluster_key_subspaces(ctypes.byref(sh), FAKE, c_m, iters,
+                                             init, stride, FAKE, FAKE, FAKE,
+                                             ws_bytes, None, None)
+    assert call(iters=0) == INVALID
+    assert call(c_m=(ctypes.c_int32 * 3)(128, 0, 128)) == INVALID
+    assert call(init=FAKE, stride=64) == INVALID          # stride < max c_m
+    assert call(ws_bytes=100) == WORKSPACE
+
+
+def test_select_validation():
+    L = B.lib()
+    sh = hy_shape()
+    cm = (ctypes.c_int32 * 3)(128, 128, 128)
+
+    def call(rho=0.9, k_fix=11880, scores=None, tables=FAKE, codes=FAKE):
+        return L.scope_select(ctypes.byref(sh), 256, cm, scores, tables, codes,
+                              FAKE, ctypes.c_float(rho), k_fix, FAKE, None, FAKE,
+                              FAKE, FAKE, FAKE, 1 << 40, None)
+    for rho in (0.0, -0.5, 1.5, float("nan"), float("inf")):
+        assert call(rho=rho) == INVALID
+    assert call(k_fix=0) == INVALID
+    assert call(k_fix=118801) == INVALID
+    assert call(tables=None) == INVALID            # neither scores nor tables
+    assert call(codes=None) == INVALID
+
+
+def test_attention_validation():
+    L = B.lib()
+
+    def call(shape, scale=0.0, q=FAKE, c_q=256):
+        return L.scope_sparse_attention(ctypes.byref(shape), q, FAKE, FAKE, c_q,
+                                        FAKE, FAKE, FAKE, FAKE,
+                                        ctypes.c_float(scale), FAKE, FAKE, 1 << 40,
+                                        None)
+    assert call(hy_shape(d=96, ranges=((0, 32, 64), (32, 32, 32)))) == UNSUPPORTED
+    assert call(hy_shape(), scale=float("nan")) == INVALID
+    assert call(hy_shape(), q=None) == INVALID
+    assert call(hy_shape(), q=ctypes.c_void_p((1 << 20) + 8)) == INVALID   # 16B rows
+    assert call(hy_shape(), c_q=0) == INVALID
+
+
+def test_proxy_scores_and_fixexp_validation():
+    L = B.lib()
+    sh = hy_shape()
+    cm = (ctypes.c_int32 * 3)(128, 128, 128)
+    assert L.scope_proxy_scores(ctypes.byref(sh), None, 256, FAKE, cm, FAKE, FAKE,
+                                None, None) == INVALID
+    assert L.scope_proxy_scores(ctypes.byref(sh), FAKE, 256, FAKE, cm, None, FAKE,
+                                FAKE, None) == INVALID   # scores need codes
+    assert L.scope_debug_fixexp(None, FAKE, 5, None) == INVALID
+    assert L.scope_debug_fixexp(FAKE, FAKE, -1, None) == INVALID
+    assert L.scope_debug_fixexp(None, None, 0, None) == OK   # empty: no launch
+
+
+def test_binding_rejects_host_tensors():
+    torch = pytest.importorskip("torch")
+    sh = hy_shape(heads=1, n=64, d=64, ranges=((0, 16, 40), (16, 24, 24)))
+    q = torch.zeros(64, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        B.scope_cluster_queries(sh, q, 8, 2, None, q, q, q, q, q, q)

@@ -1,0 +1,186 @@
+"""GPU parity: the HIP library through the C ABI against the CPU oracle.
+
+Integer results (assignments, counts, permutation, codes, selected sets) and
+the canonical fp32 results (centroids, tables, proxy logits) must match bit
+for bit; attention output must be within max-abs 2e-2 and mean-rel 1e-2 of
+the oracle's fp64 attention on the same bf16-rounded Q/K/V and key sets.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+import oracle  # noqa: E402
+from paper_2608_12780_amd import binding as B  # noqa: E402
+from paper_2608_12780_amd import inputs  # noqa: E402
+from paper_2608_12780_amd.layer import DenseAttention  # noqa: E402
+
+import gpu_harness as G  # noqa: E402
+
+MID_HY = inputs.LayerConfig("mid_hy", 2, (5, 19, 23), 128, (16, 56, 56), 32, 16,
+                            4, 0.9, inputs.ceil_tenth(5 * 19 * 23), "bf16", 8, 7)
+MID_WAN = inputs.LayerConfig("mid_wan", 1, (4, 10, 13), 128, (44, 42, 42), 16, 8,
+                             3, 0.9, inputs.ceil_tenth(520), "bf16", 8, 8)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()
+    oracle.lib()
+
+
+def check_layer(cfg, use_scores=False):
+    G.say(f"[parity] {cfg.name}: heads={cfg.heads} n={cfg.n} d={cfg.d} "
+          f"split={cfg.split} c_q={cfg.c_q} c_m={cfg.c_m} iters={cfg.iters}")
+    x = inputs.generate(cfg)
+    layer = G.make_layer(cfg)
+    gpu = G.run_gpu(layer, x, use_scores=use_scores)
+    ref = G.oracle_all(x, cfg.c_q, (cfg.c_m,) * 3, cfg.iters, cfg.rho, cfg.k_fix)
+    assert gpu["status"] == 0
+    # query clustering (Eq. 2)
+    assert np.array_equal(gpu["assign"], ref["q"]["assign"])
+    assert np.array_equal(gpu["counts"], ref["q"]["counts"])
+    assert np.array_equal(gpu["offsets"], ref["q"]["offsets"])
+    assert np.array_equal(gpu["perm"], ref["q"]["perm"])
+    assert np.array_equal(gpu["centroids"].view(np.uint32),
+                          ref["q"]["centroids"].view(np.uint32))
+    # key subspaces (Eq. 3-4)
+    assert np.array_equal(gpu["codes"], ref["k"]["codes"])
+    assert np.array_equal(gpu["k_centroids"].view(np.uint32),
+                          ref["k"]["centroids"].view(np.uint32))
+    # tables and proxy logits (Eq. 5-6)
+    assert np.array_equal(gpu["tables"].view(np.uint32), ref["tables"].view(np.uint32))
+    assert np.array_equal(gpu["scores"].view(np.uint32), ref["scores"].view(np.uint32))
+    # selection (Eq. 7-10)
+    G.assert_same_selection(gpu, ref["sel"])
+    # attention (Eq. 11) against fp64 on the same bf16 operands
+    qr, kr, vr = (G.bf16_round(a) for a in (x.q, x.k, x.v))
+    att = oracle.attention(qr, kr, vr, ref["q"]["offsets"], ref["q"]["perm"],
+                           ref["sel"]["sel_counts"], ref["sel"]["sel_idx"])
+    mx, mr = G.assert_attention_close(gpu["out"], att)
+    G.say(f"[parity] {cfg.name}: attention max-abs {mx:.3e} mean-rel {mr:.3e}; "
+          f"k_head {gpu['k_head'].tolist()}")
+    return gpu, ref
+
+
+def test_fixexp_matches_oracle_exhaustively():
+    """Every fp32 y in [-28, 0] (and a band below): GPU == oracle, bit for bit."""
+    lo = 0x80000000
+    hi = int(np.float32(-30.0).view(np.uint32))
+    step = 1 << 26
+    for start in range(lo, hi + 1, step):
+        bits = np.arange(start, min(start + step, hi + 1), dtype=np.uint32)
+        y = bits.view(np.float32)
+        yd = torch.from_numpy(y).cuda()
+        out = torch.empty(y.size, dtype=torch.int64, device="cuda")
+        B.scope_debug_fixexp(yd, out)
+        got = out.cpu().numpy().view(np.uint64)
+        want = oracle.fixexp(y)
+        bad = np.flatnonzero(got != want)
+        assert bad.size == 0, (y[bad[:5]], got[bad[:5]], want[bad[:5]])
+    G.say("[parity] fixexp: all fp32 in [-30, 0] identical")
+
+
+def test_tiny_layer():
+    check_layer(inputs.CONFIGS["tiny"])
+
+
+def test_mid_layer_hunyuan_split_ragged():
+    check_layer(MID_HY)
+
+
+def test_mid_layer_wan_split():
+    check_layer(MID_WAN)
+
+
+def test_selection_from_materialised_scores_is_identical():
+    cfg = MID_HY
+    x = inputs.generate(cfg)
+    a = G.run_gpu(G.make_layer(cfg), x, use_scores=False)
+    b = G.run_gpu(G.make_layer(cfg), x, use_scores=True)
+    for key in ("base", "topp", "k_head", "sel_counts", "sel_idx", "out"):
+        assert np.array_equal(a[key], b[key]), key
+
+
+def test_layer_is_deterministic():
+    cfg = MID_HY
+    x = inputs.generate(cfg)
+    layer = G.make_layer(cfg)
+    a = G.run_gpu(layer, x)
+    b = G.run_gpu(layer, x)
+    for key, va in a.items():
+        if isinstance(va, np.ndarray):
+            assert np.array_equal(va.view(np.uint8), b[key].view(np.uint8)), key
+
+
+def test_rho_one_keeps_every_key_and_equals_dense_mode():
+    cfg = MID_HY.with_(rho=1.0, heads=1)
+    x = inputs.generate(cfg)
+    gpu = G.run_gpu(G.make_layer(cfg), x)
+    assert (gpu["sel_counts"] == cfg.n).all()
+    assert (gpu["sel_idx"] == np.arange(cfg.n)).all()
+    q, k, v = G.to_device(x)
+    dense = DenseAttention(1, cfg.n, cfg.d, "bf16").forward(q, k, v)
+    torch.cuda.synchronize()
+    # identical key tiles in identical order: bit-identical to dense mode
+    assert np.array_equal(gpu["out"], dense.float().cpu().numpy())
+    ref = oracle.dense_attention(x.q, x.k, x.v)
+    G.assert_attention_close(gpu["out"], ref)
+
+
+def test_single_selected_key_returns_its_value():
+    cfg = MID_HY.with_(rho=1e-7, k_fix=1, heads=1)
+    x = inputs.generate(cfg)
+    gpu = G.run_gpu(G.make_layer(cfg), x)
+    assert (gpu["sel_counts"] == 1).all() and (gpu["k_head"] == 1).all()
+    perm, off = gpu["perm"][0], gpu["offsets"][0]
+    for c in range(cfg.c_q):
+        j = gpu["sel_idx"][0, c, 0]
+        rows = perm[off[c]:off[c + 1]]
+        assert np.array_equal(gpu["out"][0, rows], np.repeat(x.v[0, j][None], len(rows), 0))
+
+
+def test_empty_clusters():
+    # many duplicate query rows: equal starting centroids tie and the higher
+    # index never wins, so some clusters stay empty (n_c = 0)
+    cfg = MID_WAN.with_(name="dups", c_q=24)
+    x = inputs.generate(cfg)
+    rng = np.random.default_rng(3)
+    proto = x.q[0, rng.choice(cfg.n, 6, replace=False)]
+    x.q[0] = proto[rng.integers(0, 6, cfg.n)]
+    x.q_bits[0] = inputs.bf16_bits(x.q[0])
+    gpu, ref = check_layer_inputs(cfg, x)
+    assert (gpu["counts"] == 0).any()
+
+
+def check_layer_inputs(cfg, x):
+    layer = G.make_layer(cfg)
+    gpu = G.run_gpu(layer, x)
+    ref = G.oracle_all(x, cfg.c_q, (cfg.c_m,) * 3, cfg.iters, cfg.rho, cfg.k_fix)
+    assert np.array_equal(gpu["assign"], ref["q"]["assign"])
+    assert np.array_equal(gpu["perm"], ref["q"]["perm"])
+    assert np.array_equal(gpu["centroids"].view(np.uint32),
+                          ref["q"]["centroids"].view(np.uint32))
+    assert np.array_equal(gpu["codes"], ref["k"]["codes"])
+    G.assert_same_selection(gpu, ref["sel"])
+    qr, kr, vr = (G.bf16_round(a) for a in (x.q, x.k, x.v))
+    att = oracle.attention(qr, kr, vr, ref["q"]["offsets"], ref["q"]["perm"],
+                           ref["sel"]["sel_counts"], ref["sel"]["sel_idx"])
+    G.assert_attention_close(gpu["out"], att)
+    return gpu, ref
+
+
+@pytest.mark.parametrize("d,n", [(64, 700), (128, 1000)])
+def test_dense_mode_matches_oracle(d, n):
+    rng = np.random.default_rng(d + n)
+    qkv = [G.bf16_round(rng.standard_normal((2, n, d)).astype(np.float32) * s)
+           for s in (1.5, 1.5, 1.0)]
+    dev = [torch.from_numpy(a).cuda().to(torch.bfloat16) for a in qkv]
+    out = DenseAttention(2, n, d, "bf16").forward(*dev).float().cpu().numpy()
+    ref = oracle.dense_attention(*qkv)
+    mx, mr = G.assert_attention_close(out, ref)
+    G.say(f"[parity] dense d={d} n={n}: max-abs {mx:.3e} mean-rel {mr:.3e}")
