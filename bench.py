@@ -1,0 +1,273 @@
+"""Benchmark of the SCOPE attention layer on one MI355X.
+
+One step = the whole layer (query clustering, key-subspace clustering, score
+tables, selection, sparse attention: the five C-ABI calls for every head) on
+one batch of synthetic post-RoPE Q/K/V already resident in HBM.  The default
+workload is the HunyuanVideo-720p-like layer (24 heads, 33x45x80 = 118800
+tokens, d = 128, RoPE split 16/56/56, C_q = 256, C_m = 128, 10 iterations,
+rho = 0.9, k_fix = ceil(0.1 N)).
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+  value          effective TFLOP/s = dense attention flops 4 N^2 d H / layer time
+  ms_per_step    layer latency
+  roofline       the sparse-attention kernel against the bf16 MFMA peak
+                 (algorithmic flops 4 d sum_c n_c r_c per launch)
+  cpu_baseline   the CPU oracle on a bounded sample of one head, extrapolated
+  dense_*        the same GPU's dense attention: the library's dense mode and
+                 torch's scaled_dot_product_attention (flash backend)
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
+HBM_PEAK_GBS = 8000.0
+
+WORKLOAD_NAMES = {
+    "hy720": "HunyuanVideo-720p-like",
+    "wan720": "Wan2.2-720p-like",
+    "wan480": "Wan2.2-480p-like",
+    "stress": "HunyuanVideo-720p-like selection stress",
+    "tiny": "Tiny",
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def dense_flops(cfg):
+    return 4.0 * cfg.n * cfg.n * cfg.d * cfg.heads
+
+
+def time_events(torch, fn, reps, stream):
+    s = torch.cuda.Event(enable_timing=True)
+    e = torch.cuda.Event(enable_timing=True)
+    s.record(stream)
+    for _ in range(reps):
+        fn()
+    e.record(stream)
+    e.synchronize()
+    return s.elapsed_time(e) / reps
+
+
+def sdpa_ms(torch, q, k, v, reps):
+    """torch's fused SDPA on the same bf16 tensors (flash, else efficient)."""
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    F = torch.nn.functional
+    qb, kb, vb = (t.unsqueeze(0) for t in (q, k, v))
+    for backend in (SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION):
+        try:
+            with sdpa_kernel(backend):
+                F.scaled_dot_product_attention(qb, kb, vb)
+                torch.cuda.synchronize()
+                ms = time_events(torch, lambda: F.scaled_dot_product_attention(qb, kb, vb),
+                                 reps, torch.cuda.current_stream())
+            return ms, backend.name
+        except RuntimeError as exc:  # backend not available for this shape
+            log(f"sdpa {backend.name} unavailable: {exc}")
+    return None, None
+
+
+def cpu_baseline(cfg, x, layer_np):
+    """The oracle on one head of the workload, timed on this host's cores.
+
+    Sample: head 0; query k-means with 2 of the iterations; key-subspace
+    k-means with 1 iteration plus the final assignment; score tables and
+    proxy logits; selection for every query cluster; attention for 64 query
+    rows.  Each stage is scaled to its full per-head work (iterations, rows)
+    and the per-head sum to all heads."""
+    import oracle
+    oracle.lib()
+    cm = (cfg.c_m,) * 3
+    q, k, v = x.q[:1], x.k[:1], x.v[:1]
+    t = {}
+    it_q = min(3, cfg.iters)
+    s = time.perf_counter()
+    qr = oracle.cluster_queries(q, cfg.c_q, it_q, x.init_q[:1])
+    t["query_kmeans"] = (time.perf_counter() - s) * cfg.iters / it_q
+    s = time.perf_counter()
+    kr = oracle.cluster_key_subspaces(k, cfg.ranges, cm, 1, x.init_k[:1])
+    t["key_kmeans"] = (time.perf_counter() - s) * (cfg.iters + 1) / 2
+    s = time.perf_counter()
+    P = oracle.tables(qr["centroids"], kr["centroids"], cfg.ranges, cm)
+    S = oracle.proxy_scores(P, kr["codes"], cfg.d, cm)
+    t["scores"] = time.perf_counter() - s
+    s = time.perf_counter()
+    sel = oracle.select(S, qr["counts"], cfg.rho, cfg.k_fix)
+    t["select"] = time.perf_counter() - s
+    del S
+    rows = 256
+    mask = np.zeros((1, cfg.n), np.uint8)
+    mask[0, np.random.default_rng(0).choice(cfg.n, rows, replace=False)] = 1
+    s = time.perf_counter()
+    oracle.attention(q, k, v, qr["offsets"], qr["perm"], sel["sel_counts"],
+                     sel["sel_idx"], row_mask=mask)
+    t["attention"] = (time.perf_counter() - s) * cfg.n / rows
+    per_head = sum(t.values())
+    layer_s = per_head * cfg.heads
+    return {
+        "value": dense_flops(cfg) / layer_s / 1e12,
+        "unit": "TFLOP/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "layer_s_extrapolated": layer_s,
+        "per_head_stage_s": {k_: round(v_, 3) for k_, v_ in t.items()},
+        "sample": (f"head 0 of {cfg.heads}: query k-means {it_q}/{cfg.iters} "
+                   f"iterations, key k-means 1/{cfg.iters} iterations + final "
+                   f"assignment, tables, logits, selection of all {cfg.c_q} "
+                   f"clusters, attention for {rows}/{cfg.n} query rows; each "
+                   f"stage scaled to its full work, x{cfg.heads} heads"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", default="hy720")
+    ap.add_argument("--rho", type=float, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the layer "
+              "shards by head with no communication inside it, so a multi-GPU "
+              "figure would be the one-GPU figure times the GPU count.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_12780_amd import inputs
+    from paper_2608_12780_amd.layer import DenseAttention, ScopeLayer
+
+    if not torch.cuda.is_available():
+        log("bench.py needs a GPU")
+        sys.exit(1)
+    cfg = inputs.CONFIGS[args.config]
+    if args.rho is not None:
+        cfg = cfg.with_(rho=args.rho)
+    log(f"[bench] generating {cfg.name}: heads={cfg.heads} n={cfg.n} d={cfg.d}")
+    t0 = time.perf_counter()
+    x = inputs.generate(cfg)
+    log(f"[bench] inputs ready in {time.perf_counter() - t0:.1f}s")
+    dev = torch.device("cuda", 0)
+    if cfg.dtype == "bf16":
+        up = lambda b: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
+        q, k, v = up(x.q_bits), up(x.k_bits), up(x.v_bits)
+    else:
+        q, k, v = (torch.from_numpy(a).to(dev) for a in (x.q, x.k, x.v))
+    iq = torch.from_numpy(x.init_q).to(dev)
+    ik = torch.from_numpy(x.init_k).to(dev)
+    layer = ScopeLayer(cfg.heads, cfg.n, cfg.d, cfg.ranges, cfg.c_q, (cfg.c_m,) * 3,
+                       cfg.iters, cfg.rho, cfg.k_fix, dtype=cfg.dtype, device=dev)
+    stream = torch.cuda.current_stream()
+    nstage = 5
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(nstage + 1)]
+          for _ in range(args.steps)]
+
+    for i in range(args.warmup):
+        layer.forward(q, k, v, iq, ik)
+        torch.cuda.synchronize()
+        log(f"[bench] warmup step {i + 1}/{args.warmup} done")
+
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        layer.forward(q, k, v, iq, ik, marks=lambda j, i=i: ev[i][j].record(stream))
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_start) * 1e3 / args.steps
+    stage_names = ["cluster_queries", "cluster_key_subspaces", "proxy_scores",
+                   "select", "sparse_attention"]
+    stage_ms = {n_: float(np.mean([ev[i][j].elapsed_time(ev[i][j + 1])
+                                   for i in range(args.steps)]))
+                for j, n_ in enumerate(stage_names)}
+    layer_ms = float(np.mean([ev[i][0].elapsed_time(ev[i][nstage])
+                              for i in range(args.steps)]))
+    log(f"[bench] timed {args.steps} steps: {layer_ms:.2f} ms/layer (wall {wall_ms:.2f})")
+
+    counts = layer.counts.cpu().numpy().astype(np.float64)
+    selc = layer.sel_counts.cpu().numpy().astype(np.float64)
+    pairs = float((counts * selc).sum())
+    attn_flops = 4.0 * cfg.d * pairs
+    attn_ms = stage_ms["sparse_attention"]
+    achieved = attn_flops / (attn_ms * 1e-3) / 1e12
+    retained = pairs / (cfg.heads * float(cfg.n) * cfg.n)
+    khead = layer.k_head.cpu().numpy()
+    topp = layer.topp_counts.cpu().numpy().astype(np.float64)
+    floor_bound = float((topp < cfg.k_fix).mean())
+
+    result = {
+        "metric": "SCOPE layer latency (ms) and effective TFLOP/s vs dense attention, 720p; % MFMA peak",
+        "value": round(dense_flops(cfg) / (layer_ms * 1e-3) / 1e12, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(layer_ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": WORKLOAD_NAMES.get(cfg.name, cfg.name),
+            "heads": cfg.heads, "grid": list(cfg.grid), "n": cfg.n, "d": cfg.d,
+            "rope_split": list(cfg.split), "c_q": cfg.c_q, "c_m": cfg.c_m,
+            "iters": cfg.iters, "rho": cfg.rho, "k_fix": cfg.k_fix,
+        },
+        "roofline": {
+            "kernel": "sparse_attention",
+            "bound": "mfma",
+            "achieved": round(achieved, 2),
+            "peak": MFMA_BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+            "traffic": None,
+            "algorithmic_flops_per_launch": attn_flops,
+        },
+        "stages_ms": {k_: round(v_, 3) for k_, v_ in stage_ms.items()},
+        "wall_ms_per_step": round(wall_ms, 3),
+        "retained_fraction": round(retained, 4),
+        "k_head_mean": float(khead.mean()),
+        "floor_bound_fraction": round(floor_bound, 4),
+    }
+
+    if not args.no_dense:
+        dense = DenseAttention(cfg.heads, cfg.n, cfg.d, cfg.dtype, dev)
+        dense.forward(q, k, v)
+        torch.cuda.synchronize()
+        d_ms = time_events(torch, lambda: dense.forward(q, k, v), 2, stream)
+        result["dense_mode_ms"] = round(d_ms, 3)
+        result["speedup_vs_dense_mode"] = round(d_ms / layer_ms, 3)
+        result["dense_mode_tflops"] = round(dense_flops(cfg) / (d_ms * 1e-3) / 1e12, 2)
+        log(f"[bench] library dense mode: {d_ms:.2f} ms")
+        del dense
+        s_ms, backend = sdpa_ms(torch, q, k, v, 2)
+        result["sdpa_ms"] = None if s_ms is None else round(s_ms, 3)
+        result["sdpa_backend"] = backend
+        if s_ms is not None:
+            result["speedup_vs_sdpa"] = round(s_ms / layer_ms, 3)
+            log(f"[bench] torch sdpa ({backend}): {s_ms:.2f} ms")
+
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(cfg, x, None)
+        log(f"[bench] cpu baseline: {result['cpu_baseline']['layer_s_extrapolated']:.1f} s/layer")
+
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

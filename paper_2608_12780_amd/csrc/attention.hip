@@ -22,14 +22,25 @@ namespace scope {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int kBN = 64;   // keys per tile
-constexpr int kNW = 8;    // waves per block (32 queries each)
-constexpr int kBM = 32 * kNW;
+constexpr int kBN = 64;          // keys per tile
+constexpr int kNW = 8;           // waves per block
+constexpr int kQB = 1;           // 32-query column blocks per wave
+constexpr int kBM = 32 * kQB * kNW;
+constexpr float kRescale = 8.0f; // lazy rescale: running max may lag by 2^8
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 u) {
   return __builtin_bit_cast(bf16x8, u);
+}
+
+// Two floats -> packed bf16 (round to nearest even, v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
+  bf16x2 r;
+  r[0] = static_cast<__bf16>(a);
+  r[1] = static_cast<__bf16>(b);
+  return __builtin_bit_cast(uint32_t, r);
 }
 
 // 8 consecutive input elements as packed bf16.
@@ -40,214 +51,275 @@ __device__ __forceinline__ uint4 load8(const void *base, size_t elem) {
   } else {
     const float4 a = *reinterpret_cast<const float4 *>(static_cast<const float *>(base) + elem);
     const float4 b = *reinterpret_cast<const float4 *>(static_cast<const float *>(base) + elem + 4);
-    uint4 u;
-    u.x = f32_to_bf16(a.x) | (static_cast<uint32_t>(f32_to_bf16(a.y)) << 16);
-    u.y = f32_to_bf16(a.z) | (static_cast<uint32_t>(f32_to_bf16(a.w)) << 16);
-    u.z = f32_to_bf16(b.x) | (static_cast<uint32_t>(f32_to_bf16(b.y)) << 16);
-    u.w = f32_to_bf16(b.z) | (static_cast<uint32_t>(f32_to_bf16(b.w)) << 16);
-    return u;
+    return make_uint4(pack_bf16(a.x, a.y), pack_bf16(a.z, a.w), pack_bf16(b.x, b.y),
+                      pack_bf16(b.z, b.w));
   }
+}
+
+// Block -> work item, XCD aware: blocks are dispatched round-robin over the
+// 8 XCDs, so block b runs on XCD b % 8.  Consecutive work items (the row
+// chunks of one cluster, which gather the same keys) are given to blocks of
+// one XCD so they share its L2.
+__device__ __forceinline__ int item_of_block(int b, int nblocks) {
+  const int per = nblocks >> 3;          // nblocks is a multiple of 8
+  return (b & 7) * per + (b >> 3);
 }
 
 template <int D, bool BF16IN>
 __global__ __launch_bounds__(kNW * 64) void attn_kernel(
-    int n, int c_q, int items_per_head, const void *__restrict__ qv,
-    const void *__restrict__ kv, const void *__restrict__ vv, void *ov,
-    const int32_t *__restrict__ offsets, const int32_t *__restrict__ perm,
-    const int32_t *__restrict__ sel_idx, const int4 *__restrict__ items,
-    float scale_log2) {
+    int n, int c_q, int items_per_head, int total_items, int nblocks,
+    const void *__restrict__ qv, const void *__restrict__ kv,
+    const void *__restrict__ vv, void *ov, const int32_t *__restrict__ offsets,
+    const int32_t *__restrict__ perm, const int32_t *__restrict__ sel_idx,
+    const int4 *__restrict__ items, float scale_log2) {
   constexpr int NT = kNW * 64;
-  constexpr int KS = D + 8;     // K tile row stride (bf16 elements)
-  constexpr int VS = kBN + 8;   // V^T tile row stride
-  constexpr int C8 = D / 8;     // 16-byte chunks per row
-  constexpr int CH = kBN * C8 / NT;
-  static_assert(CH >= 1 && kBN * C8 % NT == 0, "tile/threads mismatch");
+  constexpr int KS = D + 8;       // K tile row stride (bf16 elements)
+  constexpr int VS = kBN + 4;     // V^T tile row stride
+  constexpr int C8 = D / 8;       // 16-byte chunks per row
+  // staging: the first half of the block stages V (4 consecutive keys of one
+  // 8-channel column per thread), the second half K (RK consecutive rows of
+  // one 16-byte column per thread)
+  constexpr int HALF = NT / 2;
+  constexpr int RK = kBN * C8 / HALF;       // K rows per staging thread
+  constexpr int VTH = 16 * C8;              // threads staging V
+  static_assert(kBN * C8 % HALF == 0 && RK >= 1 && RK <= 4 && VTH <= HALF,
+                "tile/threads mismatch");
+  constexpr int NR = 4;                     // rows fetched per thread per tile
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kBN * KS];
   __shared__ __attribute__((aligned(16))) uint16_t Vt[2][D * VS];
 
-  const int h = blockIdx.y;
-  const int4 it = items[static_cast<size_t>(h) * items_per_head + blockIdx.x];
+  const int item = item_of_block(blockIdx.x, nblocks);
+  if (item >= total_items) return;
+  const int h = item / items_per_head;
+  const int4 it = items[item];
   const int c = it.x, row0 = it.y, rows = it.z, r = it.w;
   if (rows <= 0) return;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int l32 = lane & 31, hf = lane >> 5;
   const size_t hoff = static_cast<size_t>(h) * n * D;
 
-  // this lane's query row (column l32 of the wave's 32-query block)
-  const int ql = w * 32 + l32;
-  const bool qvalid = ql < rows;
-  const bool wave_active = w * 32 < rows;
-  int qi = 0;
-  if (qvalid) {
-    const int pb = offsets[static_cast<size_t>(h) * (c_q + 1) + c] + row0 + ql;
-    qi = perm[static_cast<size_t>(h) * n + min(max(pb, 0), n - 1)];
-    qi = min(max(qi, 0), n - 1);
-  }
-  bf16x8 qf[D / 16];
+  // queries: wave w owns rows w*32*kQB + 32*qb + l32 of the chunk
+  int qi[kQB];
+  bool qvalid[kQB];
+  bf16x8 qf[kQB][D / 16];
 #pragma unroll
-  for (int s = 0; s < D / 16; ++s) {
-    const uint4 u = qvalid ? load8<BF16IN>(qv, hoff + static_cast<size_t>(qi) * D + 16 * s + 8 * hf)
-                           : make_uint4(0, 0, 0, 0);
-    qf[s] = as_bf16x8(u);
+  for (int qb = 0; qb < kQB; ++qb) {
+    const int ql = w * 32 * kQB + 32 * qb + l32;
+    qvalid[qb] = ql < rows;
+    qi[qb] = 0;
+    if (qvalid[qb]) {
+      const int pb = offsets[static_cast<size_t>(h) * (c_q + 1) + c] + row0 + ql;
+      qi[qb] = min(max(perm[static_cast<size_t>(h) * n + min(max(pb, 0), n - 1)], 0), n - 1);
+    }
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s)
+      qf[qb][s] = as_bf16x8(qvalid[qb] ? load8<BF16IN>(qv, hoff + static_cast<size_t>(qi[qb]) * D + 16 * s + 8 * hf)
+                                       : make_uint4(0, 0, 0, 0));
   }
+  const bool wave_active = w * 32 * kQB < rows;
 
-  f32x16 oacc[D / 32];
+  f32x16 oacc[kQB][D / 32];
 #pragma unroll
-  for (int db = 0; db < D / 32; ++db)
+  for (int qb = 0; qb < kQB; ++qb)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) oacc[db][e] = 0.0f;
-  float m_run = -INFINITY, l_run = 0.0f;
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) oacc[qb][db][e] = 0.0f;
+  float m_run[kQB], l_run[kQB];
+#pragma unroll
+  for (int qb = 0; qb < kQB; ++qb) {
+    m_run[qb] = -INFINITY;
+    l_run[qb] = 0.0f;
+  }
 
   const int32_t *sel = sel_idx + (static_cast<size_t>(h) * c_q + c) * n;
   const int ntiles = (r + kBN - 1) / kBN;
 
-  uint4 kreg[CH], vreg[CH];
-  auto gload = [&](int tile) {
+  // this thread's staging role (wave-uniform, kept in scalar registers)
+  const bool is_v = __builtin_amdgcn_readfirstlane(t) < HALF;
+  const int u = is_v ? t : t - HALF;
+  const int c8 = is_v ? ((u >> 4) % C8) : (u % C8);
+  const int key0 = is_v ? 4 * (u & 15) : RK * (u / C8) % kBN;
+  const bool stores = __builtin_amdgcn_readfirstlane(is_v ? (u < VTH) : (u < HALF));
+  const void *src = is_v ? vv : kv;
+
+  // Software pipeline, two tiles deep: the row indices of tile T+1 are
+  // requested before the rows of tile T, so waiting for indices never waits
+  // for rows in flight (vector loads complete in order).  Every load is
+  // unconditional with clamped indices, so the pipeline has no branches;
+  // rows past the key set are fetched but masked (or never read).
+  int selA[NR], selB[NR];
+  uint4 dA[NR], dB[NR];
+  auto load_sel = [&](int tile, int (&sx)[NR]) {
 #pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int id = t + i * NT;
-      {  // K: row-major chunks
-        const int key = id / C8, c8 = id % C8, kk = tile * kBN + key;
-        if (kk < r) {
-          const int row = min(max(sel[kk], 0), n - 1);
-          kreg[i] = load8<BF16IN>(kv, hoff + static_cast<size_t>(row) * D + 8 * c8);
-        } else {
-          kreg[i] = make_uint4(0, 0, 0, 0);
-        }
-      }
-      {  // V: key-fastest chunks (conflict-free transposed LDS writes)
-        const int key = id % kBN, c8 = id / kBN, kk = tile * kBN + key;
-        if (kk < r) {
-          const int row = min(max(sel[kk], 0), n - 1);
-          vreg[i] = load8<BF16IN>(vv, hoff + static_cast<size_t>(row) * D + 8 * c8);
-        } else {
-          vreg[i] = make_uint4(0, 0, 0, 0);
-        }
+    for (int i = 0; i < NR; ++i)
+      sx[i] = sel[min(tile * kBN + key0 + (is_v ? i : i % RK), n - 1)];
+  };
+  auto load_rows = [&](const int (&sx)[NR], uint4 (&dx)[NR]) {
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+      const int row = min(max(sx[i], 0), n - 1);
+      dx[i] = load8<BF16IN>(src, hoff + static_cast<size_t>(row) * D + 8 * c8);
+    }
+  };
+  auto store_rows = [&](int buf, const uint4 (&dx)[NR]) {
+    if (!stores) return;
+    if (!is_v) {
+#pragma unroll
+      for (int i = 0; i < RK; ++i)
+        *reinterpret_cast<uint4 *>(&Ks[buf][(key0 + i) * KS + 8 * c8]) = dx[i];
+    } else {
+      // transpose 4 keys x 8 channels in registers: one 8-byte row per channel
+      const uint32_t *w0 = reinterpret_cast<const uint32_t *>(&dx[0]);
+      const uint32_t *w1 = reinterpret_cast<const uint32_t *>(&dx[1]);
+      const uint32_t *w2 = reinterpret_cast<const uint32_t *>(&dx[2]);
+      const uint32_t *w3 = reinterpret_cast<const uint32_t *>(&dx[3]);
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        uint2 lo, hi;
+        lo.x = __builtin_amdgcn_perm(w1[p], w0[p], 0x05040100u);
+        lo.y = __builtin_amdgcn_perm(w3[p], w2[p], 0x05040100u);
+        hi.x = __builtin_amdgcn_perm(w1[p], w0[p], 0x07060302u);
+        hi.y = __builtin_amdgcn_perm(w3[p], w2[p], 0x07060302u);
+        *reinterpret_cast<uint2 *>(&Vt[buf][(8 * c8 + 2 * p) * VS + key0]) = lo;
+        *reinterpret_cast<uint2 *>(&Vt[buf][(8 * c8 + 2 * p + 1) * VS + key0]) = hi;
       }
     }
   };
-  auto lstore = [&](int buf) {
+
+  auto compute = [&](int tile, int buf) {
+    if (!wave_active) return;
 #pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int id = t + i * NT;
-      {
-        const int key = id / C8, c8 = id % C8;
-        *reinterpret_cast<uint4 *>(&Ks[buf][key * KS + 8 * c8]) = kreg[i];
+    for (int kb = 0; kb < 2; ++kb) {
+      // S^T = K_blk . Q^T for one 32-key block and kQB query blocks
+      f32x16 sacc[kQB];
+#pragma unroll
+      for (int qb = 0; qb < kQB; ++qb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sacc[qb][e] = 0.0f;
+#pragma unroll
+      for (int s = 0; s < D / 16; ++s) {
+        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4 *>(
+            &Ks[buf][(kb * 32 + l32) * KS + 16 * s + 8 * hf]));
+#pragma unroll
+        for (int qb = 0; qb < kQB; ++qb)
+          sacc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[qb][s], sacc[qb], 0, 0, 0);
       }
-      {
-        const int key = id % kBN, c8 = id / kBN;
-        const uint32_t wv[4] = {vreg[i].x, vreg[i].y, vreg[i].z, vreg[i].w};
+      // lane holds keys 32kb + 8(e/4) + 4hf + (e%4) of query column l32
+      const int kbase = tile * kBN + kb * 32;
+      if (kbase + 32 > r) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          Vt[buf][(8 * c8 + 2 * e) * VS + key] = static_cast<uint16_t>(wv[e] & 0xFFFFu);
-          Vt[buf][(8 * c8 + 2 * e + 1) * VS + key] = static_cast<uint16_t>(wv[e] >> 16);
+        for (int qb = 0; qb < kQB; ++qb)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (kbase + 8 * (e >> 2) + 4 * hf + (e & 3) >= r) sacc[qb][e] = -INFINITY;
+      }
+      uint4 pk[kQB][2];
+#pragma unroll
+      for (int qb = 0; qb < kQB; ++qb) {
+        float mx = fmaxf(fmaxf(sacc[qb][0], sacc[qb][1]), sacc[qb][2]);
+#pragma unroll
+        for (int e = 3; e < 15; e += 2) mx = fmaxf(fmaxf(mx, sacc[qb][e]), sacc[qb][e + 1]);
+        mx = fmaxf(mx, sacc[qb][15]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float mt = mx * scale_log2;
+        // rescale only when the running max falls too far behind; the
+        // branch is wave-wide but each query decides for itself (alpha = 1
+        // otherwise), so a query's result never depends on its wave-mates
+        const bool behind = mt > m_run[qb] + kRescale;
+        if (__ballot(behind)) {
+          const float m_new = behind ? fmaxf(m_run[qb], mt) : m_run[qb];
+          const float alpha = behind ? __builtin_amdgcn_exp2f(m_run[qb] - m_new) : 1.0f;
+          l_run[qb] *= alpha;
+#pragma unroll
+          for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) oacc[qb][db][e] *= alpha;
+          m_run[qb] = m_new;
         }
+        const float neg_m = -m_run[qb];
+        float p[16];
+        float psum = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          p[e] = __builtin_amdgcn_exp2f(fmaf(sacc[qb][e], scale_log2, neg_m));
+          psum += p[e];
+        }
+        l_run[qb] += psum;
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2)
+          pk[qb][s2] = make_uint4(pack_bf16(p[8 * s2 + 0], p[8 * s2 + 1]),
+                                  pack_bf16(p[8 * s2 + 2], p[8 * s2 + 3]),
+                                  pack_bf16(p[8 * s2 + 4], p[8 * s2 + 5]),
+                                  pack_bf16(p[8 * s2 + 6], p[8 * s2 + 7]));
       }
+      // O^T += V_blk^T . P^T in 16-key steps; each V fragment feeds kQB MFMAs
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+          const uint16_t *vrow = &Vt[buf][(db * 32 + l32) * VS + kb * 32 + 16 * s2];
+          const uint2 lo = *reinterpret_cast<const uint2 *>(vrow + 4 * hf);
+          const uint2 hi = *reinterpret_cast<const uint2 *>(vrow + 8 + 4 * hf);
+          const bf16x8 a = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+#pragma unroll
+          for (int qb = 0; qb < kQB; ++qb)
+            oacc[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                a, as_bf16x8(pk[qb][s2]), oacc[qb][db], 0, 0, 0);
+        }
     }
+  };
+
+  // one pipeline step: compute tile T from LDS while tile T+1 (already in
+  // registers `cur`) lands in the other LDS buffer and tile T+2 is requested
+  auto step = [&](int tile, int (&sel_next)[NR], uint4 (&cur)[NR],
+                  int (&sel_far)[NR], uint4 (&far)[NR]) {
+    load_sel(tile + 3, sel_next);
+    load_rows(sel_far, far);
+    compute(tile, tile & 1);
+    store_rows((tile + 1) & 1, cur);
+    __syncthreads();
   };
 
   if (ntiles > 0) {
-    gload(0);
-    lstore(0);
+    load_sel(0, selA);
+    load_sel(1, selB);
+    load_rows(selA, dA);   // tile 0
+    load_sel(2, selA);
+    load_rows(selB, dB);   // tile 1
+    store_rows(0, dA);
   }
   __syncthreads();
-
-  for (int tile = 0; tile < ntiles; ++tile) {
-    const int buf = tile & 1;
-    if (tile + 1 < ntiles) gload(tile + 1);
-    if (wave_active) {
-      // S^T = K_tile . Q^T : two 32-key blocks
-      f32x16 sacc[2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) sacc[kb][e] = 0.0f;
-#pragma unroll
-        for (int s = 0; s < D / 16; ++s) {
-          const uint4 a = *reinterpret_cast<const uint4 *>(
-              &Ks[buf][(kb * 32 + l32) * KS + 16 * s + 8 * hf]);
-          sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), qf[s],
-                                                             sacc[kb], 0, 0, 0);
-        }
-      }
-      // online softmax; lane holds keys 32kb + 8i + 4hf + j of query l32
-      const int kbase = tile * kBN;
-      float mt = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = kbase + kb * 32 + 8 * (e >> 2) + 4 * hf + (e & 3);
-          const float x = key < r ? sacc[kb][e] * scale_log2 : -INFINITY;
-          sacc[kb][e] = x;
-          mt = fmaxf(mt, x);
-        }
-      mt = fmaxf(mt, __shfl_xor(mt, 32));
-      const float m_new = fmaxf(m_run, mt);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      float psum = 0.0f;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float p = __builtin_amdgcn_exp2f(sacc[kb][e] - m_new);
-          sacc[kb][e] = p;
-          psum += p;
-        }
-      l_run = l_run * alpha + psum;
-      m_run = m_new;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) oacc[db][e] *= alpha;
-      // O^T += V_tile^T . P^T, 16 keys per step
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-          uint4 pu;
-          pu.x = f32_to_bf16(sacc[kb][8 * s2 + 0]) | (static_cast<uint32_t>(f32_to_bf16(sacc[kb][8 * s2 + 1])) << 16);
-          pu.y = f32_to_bf16(sacc[kb][8 * s2 + 2]) | (static_cast<uint32_t>(f32_to_bf16(sacc[kb][8 * s2 + 3])) << 16);
-          pu.z = f32_to_bf16(sacc[kb][8 * s2 + 4]) | (static_cast<uint32_t>(f32_to_bf16(sacc[kb][8 * s2 + 5])) << 16);
-          pu.w = f32_to_bf16(sacc[kb][8 * s2 + 6]) | (static_cast<uint32_t>(f32_to_bf16(sacc[kb][8 * s2 + 7])) << 16);
-          const bf16x8 pb = as_bf16x8(pu);
-#pragma unroll
-          for (int db = 0; db < D / 32; ++db) {
-            const uint16_t *vrow = &Vt[buf][(db * 32 + l32) * VS + kb * 32 + 16 * s2];
-            const uint2 lo = *reinterpret_cast<const uint2 *>(vrow + 4 * hf);
-            const uint2 hi = *reinterpret_cast<const uint2 *>(vrow + 8 + 4 * hf);
-            const uint4 a = make_uint4(lo.x, lo.y, hi.x, hi.y);
-            oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), pb,
-                                                               oacc[db], 0, 0, 0);
-          }
-        }
-    }
-    if (tile + 1 < ntiles) lstore(buf ^ 1);
-    __syncthreads();
+  // registers: tile T+1 is in (T even ? dB : dA); the row indices of tile
+  // T+2 in (T even ? selA : selB)
+  for (int tile = 0; tile < ntiles; tile += 2) {
+    step(tile, selB, dB, selA, dA);
+    if (tile + 1 < ntiles) step(tile + 1, selA, dA, selB, dB);
   }
 
-  // lanes l and l^32 hold the two halves of one query's row sum
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (!qvalid) return;
-  const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
-  // lane holds O^T[32db + 8i + 4hf + j][query l32]
 #pragma unroll
-  for (int db = 0; db < D / 32; ++db)
+  for (int qb = 0; qb < kQB; ++qb) {
+    // lanes l and l^32 hold the two halves of one query's row sum
+    const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
+    if (!qvalid[qb]) continue;
+    const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
+    // lane holds O^T[32db + 8i + 4hf + j][query]
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int dim = db * 32 + 8 * i + 4 * hf;
-      const size_t at = hoff + static_cast<size_t>(qi) * D + dim;
-      const float o0 = oacc[db][4 * i + 0] * inv, o1 = oacc[db][4 * i + 1] * inv;
-      const float o2 = oacc[db][4 * i + 2] * inv, o3 = oacc[db][4 * i + 3] * inv;
-      if (BF16IN) {
-        uint2 u;
-        u.x = f32_to_bf16(o0) | (static_cast<uint32_t>(f32_to_bf16(o1)) << 16);
-        u.y = f32_to_bf16(o2) | (static_cast<uint32_t>(f32_to_bf16(o3)) << 16);
-        *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(ov) + at) = u;
-      } else {
-        *reinterpret_cast<float4 *>(static_cast<float *>(ov) + at) = make_float4(o0, o1, o2, o3);
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int dim = db * 32 + 8 * i + 4 * hf;
+        const size_t at = hoff + static_cast<size_t>(qi[qb]) * D + dim;
+        const float o0 = oacc[qb][db][4 * i + 0] * inv, o1 = oacc[qb][db][4 * i + 1] * inv;
+        const float o2 = oacc[qb][db][4 * i + 2] * inv, o3 = oacc[qb][db][4 * i + 3] * inv;
+        if (BF16IN) {
+          *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(ov) + at) =
+              make_uint2(pack_bf16(o0, o1), pack_bf16(o2, o3));
+        } else {
+          *reinterpret_cast<float4 *>(static_cast<float *>(ov) + at) = make_float4(o0, o1, o2, o3);
+        }
       }
-    }
+  }
 }
 
 // Work list: per head, every cluster's queries cut into chunks of kBM rows,
@@ -295,13 +367,17 @@ hipError_t launch_attn(int heads, int n, bool bf16, const void *q,
                        const int32_t *offsets, const int32_t *perm,
                        const int32_t *sel_idx, const int4 *items, int iph,
                        float scale_log2, hipStream_t s) {
-  const dim3 grid(iph, heads), block(kNW * 64);
+  const int total = iph * heads;
+  const int nblocks = (total + 7) / 8 * 8;  // a multiple of the XCD count
+  const dim3 grid(nblocks), block(kNW * 64);
   if (bf16)
-    hipLaunchKernelGGL((attn_kernel<D, true>), grid, block, 0, s, n, c_q, iph, q,
-                       k, v, o, offsets, perm, sel_idx, items, scale_log2);
+    hipLaunchKernelGGL((attn_kernel<D, true>), grid, block, 0, s, n, c_q, iph,
+                       total, nblocks, q, k, v, o, offsets, perm, sel_idx, items,
+                       scale_log2);
   else
     hipLaunchKernelGGL((attn_kernel<D, false>), grid, block, 0, s, n, c_q, iph,
-                       q, k, v, o, offsets, perm, sel_idx, items, scale_log2);
+                       total, nblocks, q, k, v, o, offsets, perm, sel_idx, items,
+                       scale_log2);
   return hipGetLastError();
 }
 

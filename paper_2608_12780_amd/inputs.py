@@ -22,8 +22,10 @@ Workload recipe (post-3D-RoPE queries/keys of a video DiT head, Sec. 3.1):
 """
 from __future__ import annotations
 
+import concurrent.futures
 import dataclasses
 import math
+import os
 
 import numpy as np
 
@@ -170,11 +172,12 @@ class LayerInputs:
 
 
 def generate(cfg: LayerConfig, heads: int | None = None,
-             head_offset: int = 0) -> LayerInputs:
+             head_offset: int = 0, threads: int | None = None) -> LayerInputs:
     """Generate heads [head_offset, head_offset + heads) of a workload.
 
     Each head has its own child stream of SeedSequence(cfg.seed), so a
-    subset of heads is identical to the same heads of the full layer.
+    subset of heads is identical to the same heads of the full layer, and
+    heads are generated in parallel threads with identical results.
     """
     nh = cfg.heads if heads is None else heads
     children = np.random.SeedSequence(cfg.seed).spawn(cfg.heads)
@@ -187,7 +190,7 @@ def generate(cfg: LayerConfig, heads: int | None = None,
     init_q = np.empty((nh, cfg.c_q), np.int32)
     init_k = np.empty((nh, 3, cfg.c_m), np.int32)
     tau = np.ones(nh, np.float64)
-    for hi in range(nh):
+    def one(hi):
         rng = np.random.default_rng(children[head_offset + hi])
         F = _fields(rng, cfg, coords)
         c_h = rng.standard_normal(d)
@@ -200,21 +203,27 @@ def generate(cfg: LayerConfig, heads: int | None = None,
         t_h = math.exp(rng.uniform(math.log(0.25), math.log(4.0)))
         eq *= np.float32(0.6)
         ek *= np.float32(0.6)
-        qp = shared + eq
-        kp = shared + ek
-        qh = _apply_rope(qp, cos, sin)
+        qh = _apply_rope(shared + eq, cos, sin)
         if cfg.stress:
             tau[hi] = t_h
-            qh = qh * t_h
+            qh *= np.float32(t_h)
         q[hi] = qh
-        k[hi] = _apply_rope(kp, cos, sin)
+        k[hi] = _apply_rope(shared + ek, cos, sin)
         v[hi] = vv
         init_q[hi] = init_rows(rng, n, cfg.c_q)
         for m in range(3):
             init_k[hi, m] = init_rows(rng, n, cfg.c_m)
+        if cfg.dtype == "bf16":
+            qb[hi], kb[hi], vb[hi] = bf16_bits(q[hi]), bf16_bits(k[hi]), bf16_bits(v[hi])
+            q[hi], k[hi], v[hi] = bf16_widen(qb[hi]), bf16_widen(kb[hi]), bf16_widen(vb[hi])
+
     if cfg.dtype == "bf16":
-        qb, kb, vb = bf16_bits(q), bf16_bits(k), bf16_bits(v)
-        q, k, v = bf16_widen(qb), bf16_widen(kb), bf16_widen(vb)
+        qb = np.empty((nh, n, d), np.uint16)
+        kb = np.empty((nh, n, d), np.uint16)
+        vb = np.empty((nh, n, d), np.uint16)
     else:
         qb = kb = vb = None
+    workers = max(1, min(nh, threads or os.cpu_count() or 1, 16))
+    with concurrent.futures.ThreadPoolExecutor(workers) as ex:
+        list(ex.map(one, range(nh)))
     return LayerInputs(cfg, q, k, v, qb, kb, vb, init_q, init_k, tau)
