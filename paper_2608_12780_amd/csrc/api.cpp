@@ -84,6 +84,8 @@ struct QueryWs {
   int32_t *hist, *rel;
   int64_t *partial;
   int splits;
+  uint16_t *ubf;
+  float *nu, *bnd;
 };
 size_t query_ws(const scope_shape *s, int c_q, void *base, QueryWs *w) {
   Carver cv(base);
@@ -94,6 +96,10 @@ size_t query_ws(const scope_shape *s, int c_q, void *base, QueryWs *w) {
   q.rel = cv.take<int32_t>(static_cast<size_t>(s->heads) * nch * c_q);
   q.partial = cv.take<int64_t>(static_cast<size_t>(s->heads) * c_q * splits * s->d);
   q.splits = splits;
+  const int cpad = scope::km_cpad(c_q);
+  q.ubf = cv.take<uint16_t>(static_cast<size_t>(s->heads) * cpad * scope::km_dxp(s->d));
+  q.nu = cv.take<float>(static_cast<size_t>(s->heads) * cpad);
+  q.bnd = cv.take<float>(static_cast<size_t>(s->heads) * 4);
   if (w) *w = q;
   return cv.used;
 }
@@ -103,6 +109,8 @@ struct KeyWs {
   int32_t *counts[3], *offsets[3], *hist[3], *rel[3];
   int64_t *partial[3];
   int splits[3];
+  uint16_t *ubf[3];
+  float *nu[3], *bnd[3];
 };
 size_t key_ws(const scope_shape *s, const int32_t *c_m, void *base, KeyWs *w) {
   Carver cv(base);
@@ -119,6 +127,10 @@ size_t key_ws(const scope_shape *s, const int32_t *c_m, void *base, KeyWs *w) {
     k.hist[m] = cv.take<int32_t>(H * nch * C);
     k.rel[m] = cv.take<int32_t>(H * nch * C);
     k.partial[m] = cv.take<int64_t>(H * C * k.splits[m] * dx);
+    const int cpad = scope::km_cpad(C);
+    k.ubf[m] = cv.take<uint16_t>(H * cpad * scope::km_dxp(dx));
+    k.nu[m] = cv.take<float>(H * cpad);
+    k.bnd[m] = cv.take<float>(H * 4);
   }
   if (w) *w = k;
   return cv.used;
@@ -225,6 +237,12 @@ int32_t scope_cluster_queries(const scope_shape *shape, const void *q,
   p.partial = w.partial;
   p.splits = w.splits;
   p.heads = shape->heads;
+  p.mfma = scope::km_mfma_ok(p.bf16, p.ld, p.col0, p.dx, p.C);
+  p.cpad = scope::km_cpad(p.C);
+  p.dxp = scope::km_dxp(p.dx);
+  p.ubf = w.ubf;
+  p.nu = w.nu;
+  p.bnd = w.bnd;
   SCOPE_TRY(scope::km_init(p, init_idx, c_q, dev_status, s));
   for (int it = 0; it < iters; ++it) {
     SCOPE_TRY(scope::km_assign(p, true, s));
@@ -285,6 +303,12 @@ int32_t scope_cluster_key_subspaces(const scope_shape *shape, const void *k,
     pm.partial = w.partial[m];
     pm.splits = w.splits[m];
     pm.heads = shape->heads;
+    pm.mfma = scope::km_mfma_ok(pm.bf16, pm.ld, pm.col0, pm.dx, pm.C);
+    pm.cpad = scope::km_cpad(pm.C);
+    pm.dxp = scope::km_dxp(pm.dx);
+    pm.ubf = w.ubf[m];
+    pm.nu = w.nu[m];
+    pm.bnd = w.bnd[m];
     ucol += static_cast<size_t>(c_m[m]) * pm.dx;
     const int32_t *init = init_idx ? init_idx + static_cast<size_t>(m) * init_stride : nullptr;
     // init rows of head h, subspace m live at init_idx[(h*3 + m)*init_stride]

@@ -56,18 +56,14 @@ __device__ __forceinline__ uint4 load8(const void *base, size_t elem) {
   }
 }
 
-// Block -> work item, XCD aware: blocks are dispatched round-robin over the
-// 8 XCDs, so block b runs on XCD b % 8.  Consecutive work items (the row
-// chunks of one cluster, which gather the same keys) are given to blocks of
-// one XCD so they share its L2.
-__device__ __forceinline__ int item_of_block(int b, int nblocks) {
-  const int per = nblocks >> 3;          // nblocks is a multiple of 8
-  return (b & 7) * per + (b >> 3);
-}
+// Work items run in list order: heads one after the other and, within a
+// head, clusters in order with their row chunks adjacent.  All XCDs work on
+// the same head at a time, so one head's K/V (60 MB at 118800 x 128 bf16) is
+// what the 256 MB memory-side cache has to hold.
 
 template <int D, bool BF16IN>
 __global__ __launch_bounds__(kNW * 64) void attn_kernel(
-    int n, int c_q, int items_per_head, int total_items, int nblocks,
+    int n, int c_q, int items_per_head, int total_items,
     const void *__restrict__ qv, const void *__restrict__ kv,
     const void *__restrict__ vv, void *ov, const int32_t *__restrict__ offsets,
     const int32_t *__restrict__ perm, const int32_t *__restrict__ sel_idx,
@@ -88,7 +84,7 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel(
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kBN * KS];
   __shared__ __attribute__((aligned(16))) uint16_t Vt[2][D * VS];
 
-  const int item = item_of_block(blockIdx.x, nblocks);
+  const int item = blockIdx.x;
   if (item >= total_items) return;
   const int h = item / items_per_head;
   const int4 it = items[item];
@@ -322,7 +318,7 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel(
   }
 }
 
-// Work list: per head, every cluster's queries cut into chunks of kBM rows,
+// Work list of one head: every cluster's queries cut into chunks of kBM rows,
 // clusters in order; unused slots get rows = 0.
 __global__ __launch_bounds__(1024) void attn_items_kernel(
     int n, int c_q, int items_per_head, const int32_t *__restrict__ offsets,
@@ -368,21 +364,21 @@ hipError_t launch_attn(int heads, int n, bool bf16, const void *q,
                        const int32_t *sel_idx, const int4 *items, int iph,
                        float scale_log2, hipStream_t s) {
   const int total = iph * heads;
-  const int nblocks = (total + 7) / 8 * 8;  // a multiple of the XCD count
-  const dim3 grid(nblocks), block(kNW * 64);
+  const dim3 grid(total), block(kNW * 64);
   if (bf16)
     hipLaunchKernelGGL((attn_kernel<D, true>), grid, block, 0, s, n, c_q, iph,
-                       total, nblocks, q, k, v, o, offsets, perm, sel_idx, items,
+                       total, q, k, v, o, offsets, perm, sel_idx, items,
                        scale_log2);
   else
     hipLaunchKernelGGL((attn_kernel<D, false>), grid, block, 0, s, n, c_q, iph,
-                       total, nblocks, q, k, v, o, offsets, perm, sel_idx, items,
+                       total, q, k, v, o, offsets, perm, sel_idx, items,
                        scale_log2);
   return hipGetLastError();
 }
 
 }  // namespace
 
+// Slots of one head: sum_c ceil(n_c / kBM) <= ceil(n / kBM) + c_q.
 int attn_items_per_head(int n, int c_q) { return (n + kBM - 1) / kBM + c_q; }
 
 hipError_t attention_run(int heads, int n, int d, bool bf16, const void *q,

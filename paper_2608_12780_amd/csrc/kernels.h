@@ -27,7 +27,20 @@ struct KmProblem {
   int64_t *partial;       // [heads][C][splits][dx]
   int splits;
   int heads;
+  // matrix-core assignment (bf16 inputs): bf16 copy of the centroids,
+  // their squared norms and the error-bound constants, refreshed per pass
+  bool mfma;
+  int cpad, dxp;          // centroids padded to 32, channels padded to 16
+  uint16_t *ubf;          // [heads][cpad][dxp]
+  float *nu;              // [heads][cpad]
+  float *bnd;             // [heads][4]
 };
+
+// Whether the matrix-core assignment applies: bf16 rows at even offsets and
+// a bf16 codebook that fits the kernel's LDS.
+bool km_mfma_ok(bool bf16, int ld, int col0, int dx, int C);
+int km_cpad(int C);
+int km_dxp(int dx);
 
 constexpr int kAssignBlock = 256;  // points per assign block == grouping chunk
 

@@ -340,7 +340,10 @@ hipError_t km_init(const KmProblem &p, const int32_t *init, int init_stride,
   return hipGetLastError();
 }
 
+hipError_t km_assign_mfma(const KmProblem &p, bool with_hist, hipStream_t s);
+
 hipError_t km_assign(const KmProblem &p, bool with_hist, hipStream_t s) {
+  if (p.mfma) return km_assign_mfma(p, with_hist, s);
   return p.bf16 ? assign_dispatch<uint16_t>(p, with_hist, s)
                 : assign_dispatch<float>(p, with_hist, s);
 }
