@@ -97,7 +97,7 @@ size_t query_ws(const scope_shape *s, int c_q, void *base, QueryWs *w) {
   q.partial = cv.take<int64_t>(static_cast<size_t>(s->heads) * c_q * splits * s->d);
   q.splits = splits;
   const int cpad = scope::km_cpad(c_q);
-  q.ubf = cv.take<uint16_t>(static_cast<size_t>(s->heads) * cpad * scope::km_dxp(s->d));
+  q.ubf = cv.take<uint16_t>(static_cast<size_t>(s->heads) * cpad * 2 * scope::km_dxp(s->d));
   q.nu = cv.take<float>(static_cast<size_t>(s->heads) * cpad);
   q.bnd = cv.take<float>(static_cast<size_t>(s->heads) * 4);
   if (w) *w = q;
@@ -128,7 +128,7 @@ size_t key_ws(const scope_shape *s, const int32_t *c_m, void *base, KeyWs *w) {
     k.rel[m] = cv.take<int32_t>(H * nch * C);
     k.partial[m] = cv.take<int64_t>(H * C * k.splits[m] * dx);
     const int cpad = scope::km_cpad(C);
-    k.ubf[m] = cv.take<uint16_t>(H * cpad * scope::km_dxp(dx));
+    k.ubf[m] = cv.take<uint16_t>(H * cpad * 2 * scope::km_dxp(dx));
     k.nu[m] = cv.take<float>(H * cpad);
     k.bnd[m] = cv.take<float>(H * 4);
   }

@@ -31,7 +31,7 @@ struct KmProblem {
   // their squared norms and the error-bound constants, refreshed per pass
   bool mfma;
   int cpad, dxp;          // centroids padded to 32, channels padded to 16
-  uint16_t *ubf;          // [heads][cpad][dxp]
+  uint16_t *ubf;          // [heads][cpad][2 * dxp]: bf16 hi then lo terms
   float *nu;              // [heads][cpad]
   float *bnd;             // [heads][4]
 };
