@@ -10,7 +10,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libscope.so")
-SOURCES = ["api.cpp", "kmeans.hip", "kmeans_mfma.hip", "score.hip", "select.hip",
+SOURCES = ["api.cpp", "kmeans.hip", "kmeans_mfma.hip", "kmeans_update.hip", "score.hip",
+           "select.hip",
            "attention.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -80,22 +80,36 @@ bool aligned_data(const void *p, const scope_shape *s) {
 }
 
 // --- workspace layouts (each call's regions start at offset 0) -----------
+// Update plans; shapes were validated, so planning cannot fail for them.
+scope::AccPlan query_plan(const scope_shape *s, int c_q) {
+  scope::AccPlan p;
+  const int col0 = 0, dx = s->d;
+  scope::km_accum_plan(1, &col0, &dx, &c_q, s->heads, s->n, &p);
+  return p;
+}
+scope::AccPlan key_plan(const scope_shape *s, const int32_t *c_m) {
+  scope::AccPlan p;
+  const int C[3] = {c_m[0], c_m[1], c_m[2]};
+  scope::km_accum_plan(3, s->range_off, s->range_len, C, s->heads, s->n, &p);
+  return p;
+}
+
 struct QueryWs {
   int32_t *hist, *rel;
-  int64_t *partial;
-  int splits;
+  long long *slab;
+  int32_t *cslab;
   uint16_t *ubf;
   float *nu, *bnd;
 };
 size_t query_ws(const scope_shape *s, int c_q, void *base, QueryWs *w) {
   Carver cv(base);
   const int nch = scope::km_nchunks(s->n);
-  const int splits = scope::km_splits(s->n, c_q, s->d);
+  const scope::AccPlan plan = query_plan(s, c_q);
   QueryWs q;
   q.hist = cv.take<int32_t>(static_cast<size_t>(s->heads) * nch * c_q);
   q.rel = cv.take<int32_t>(static_cast<size_t>(s->heads) * nch * c_q);
-  q.partial = cv.take<int64_t>(static_cast<size_t>(s->heads) * c_q * splits * s->d);
-  q.splits = splits;
+  q.slab = cv.take<long long>(scope::km_accum_slab_bytes(plan, s->heads) / sizeof(long long));
+  q.cslab = cv.take<int32_t>(scope::km_accum_cslab_bytes(plan, s->heads) / sizeof(int32_t));
   const int cpad = scope::km_cpad(c_q);
   q.ubf = cv.take<uint16_t>(static_cast<size_t>(s->heads) * cpad * 2 * scope::km_dxp(s->d));
   q.nu = cv.take<float>(static_cast<size_t>(s->heads) * cpad);
@@ -105,28 +119,22 @@ size_t query_ws(const scope_shape *s, int c_q, void *base, QueryWs *w) {
 }
 
 struct KeyWs {
-  int32_t *assign3, *perm3;
-  int32_t *counts[3], *offsets[3], *hist[3], *rel[3];
-  int64_t *partial[3];
-  int splits[3];
+  int32_t *assign3;
+  long long *slab;
+  int32_t *cslab;
   uint16_t *ubf[3];
   float *nu[3], *bnd[3];
 };
 size_t key_ws(const scope_shape *s, const int32_t *c_m, void *base, KeyWs *w) {
   Carver cv(base);
-  const int nch = scope::km_nchunks(s->n);
   const size_t H = static_cast<size_t>(s->heads);
+  const scope::AccPlan plan = key_plan(s, c_m);
   KeyWs k;
   k.assign3 = cv.take<int32_t>(H * 3 * s->n);
-  k.perm3 = cv.take<int32_t>(H * 3 * s->n);
+  k.slab = cv.take<long long>(scope::km_accum_slab_bytes(plan, s->heads) / sizeof(long long));
+  k.cslab = cv.take<int32_t>(scope::km_accum_cslab_bytes(plan, s->heads) / sizeof(int32_t));
   for (int m = 0; m < 3; ++m) {
     const int C = c_m[m], dx = s->range_len[m];
-    k.splits[m] = scope::km_splits(s->n, C, dx);
-    k.counts[m] = cv.take<int32_t>(H * C);
-    k.offsets[m] = cv.take<int32_t>(H * (C + 1));
-    k.hist[m] = cv.take<int32_t>(H * nch * C);
-    k.rel[m] = cv.take<int32_t>(H * nch * C);
-    k.partial[m] = cv.take<int64_t>(H * C * k.splits[m] * dx);
     const int cpad = scope::km_cpad(C);
     k.ubf[m] = cv.take<uint16_t>(H * cpad * 2 * scope::km_dxp(dx));
     k.nu[m] = cv.take<float>(H * cpad);
@@ -185,6 +193,8 @@ int32_t scope_workspace_size(const scope_shape *shape, int32_t c_q,
   if ((st = check_cq(shape, c_q))) return st;
   if ((st = check_cm(shape, c_m))) return st;
   if (!bytes) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (query_plan(shape, c_q).nwin == 0 || key_plan(shape, c_m).nwin == 0)
+    return SCOPE_ERR_UNSUPPORTED;
   size_t need = query_ws(shape, c_q, nullptr, nullptr);
   size_t k = key_ws(shape, c_m, nullptr, nullptr);
   size_t s = select_ws(shape, c_q, nullptr, nullptr);
@@ -210,6 +220,7 @@ int32_t scope_cluster_queries(const scope_shape *shape, const void *q,
   if (!q || !q_centroids || !assign || !counts || !offsets || !perm)
     return SCOPE_ERR_INVALID_ARGUMENT;
   if (!aligned_data(q, shape)) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (query_plan(shape, c_q).nwin == 0) return SCOPE_ERR_UNSUPPORTED;
   QueryWs w;
   const size_t need = query_ws(shape, c_q, nullptr, nullptr);
   if ((st = check_ws(workspace, ws_bytes, need))) return st;
@@ -234,8 +245,6 @@ int32_t scope_cluster_queries(const scope_shape *shape, const void *q,
   p.perm = perm;
   p.chunk_hist = w.hist;
   p.chunk_rel = w.rel;
-  p.partial = w.partial;
-  p.splits = w.splits;
   p.heads = shape->heads;
   p.mfma = scope::km_mfma_ok(p.bf16, p.ld, p.col0, p.dx, p.C);
   p.cpad = scope::km_cpad(p.C);
@@ -243,11 +252,18 @@ int32_t scope_cluster_queries(const scope_shape *shape, const void *q,
   p.ubf = w.ubf;
   p.nu = w.nu;
   p.bnd = w.bnd;
+  const scope::AccPlan plan = query_plan(shape, c_q);
   SCOPE_TRY(scope::km_init(p, init_idx, c_q, dev_status, s));
+  // the returned grouping is that of the last assignment, taken before the
+  // last update
   for (int it = 0; it < iters; ++it) {
-    SCOPE_TRY(scope::km_assign(p, true, s));
-    SCOPE_TRY(scope::km_group(p, s));
-    SCOPE_TRY(scope::km_update(p, dev_status, s));
+    const bool last = it + 1 == iters;
+    SCOPE_TRY(scope::km_assign(p, last, s));
+    if (last) SCOPE_TRY(scope::km_group(p, s));
+    SCOPE_TRY(scope::km_accum(plan, q, p.bf16, p.x_head_stride, d, n, shape->heads,
+                              assign, p.a_head_stride, 0, w.slab, w.cslab,
+                              q_centroids, p.u_head_stride, it == 0 ? dev_status : nullptr,
+                              s));
   }
   return SCOPE_OK;
 }
@@ -270,6 +286,7 @@ int32_t scope_cluster_key_subspaces(const scope_shape *shape, const void *k,
                                    : (c_m[1] > c_m[2] ? c_m[1] : c_m[2]);
     if (init_stride < mx) return SCOPE_ERR_INVALID_ARGUMENT;
   }
+  if (key_plan(shape, c_m).nwin == 0) return SCOPE_ERR_UNSUPPORTED;
   const size_t need = key_ws(shape, c_m, nullptr, nullptr);
   if ((st = check_ws(workspace, ws_bytes, need))) return st;
   KeyWs w;
@@ -295,13 +312,6 @@ int32_t scope_cluster_key_subspaces(const scope_shape *shape, const void *k,
     pm.u_head_stride = per_head;
     pm.assign = w.assign3 + static_cast<size_t>(m) * n;
     pm.a_head_stride = static_cast<size_t>(3) * n;
-    pm.counts = w.counts[m];
-    pm.offsets = w.offsets[m];
-    pm.perm = w.perm3 + static_cast<size_t>(m) * n;
-    pm.chunk_hist = w.hist[m];
-    pm.chunk_rel = w.rel[m];
-    pm.partial = w.partial[m];
-    pm.splits = w.splits[m];
     pm.heads = shape->heads;
     pm.mfma = scope::km_mfma_ok(pm.bf16, pm.ld, pm.col0, pm.dx, pm.C);
     pm.cpad = scope::km_cpad(pm.C);
@@ -314,12 +324,13 @@ int32_t scope_cluster_key_subspaces(const scope_shape *shape, const void *k,
     // init rows of head h, subspace m live at init_idx[(h*3 + m)*init_stride]
     SCOPE_TRY(scope::km_init(pm, init, 3 * init_stride, dev_status, s));
   }
-  for (int it = 0; it < iters; ++it)
-    for (int m = 0; m < 3; ++m) {
-      SCOPE_TRY(scope::km_assign(p[m], true, s));
-      SCOPE_TRY(scope::km_group(p[m], s));
-      SCOPE_TRY(scope::km_update(p[m], dev_status, s));
-    }
+  const scope::AccPlan plan = key_plan(shape, c_m);
+  for (int it = 0; it < iters; ++it) {
+    for (int m = 0; m < 3; ++m) SCOPE_TRY(scope::km_assign(p[m], false, s));
+    SCOPE_TRY(scope::km_accum(plan, k, p[0].bf16, p[0].x_head_stride, d, n, shape->heads,
+                              w.assign3, static_cast<size_t>(3) * n, n, w.slab, w.cslab,
+                              k_centroids, per_head, it == 0 ? dev_status : nullptr, s));
+  }
   for (int m = 0; m < 3; ++m) SCOPE_TRY(scope::km_assign(p[m], false, s));
   SCOPE_TRY(scope::km_pack_codes(w.assign3, static_cast<size_t>(3) * n, n, n,
                                  shape->heads, codes, s));

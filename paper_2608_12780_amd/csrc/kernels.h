@@ -24,8 +24,6 @@ struct KmProblem {
   int32_t *perm;          // [heads][n]
   int32_t *chunk_hist;    // [heads][nchunks][C]
   int32_t *chunk_rel;     // [heads][nchunks][C]
-  int64_t *partial;       // [heads][C][splits][dx]
-  int splits;
   int heads;
   // matrix-core assignment (bf16 inputs): bf16 copy of the centroids,
   // their squared norms and the error-bound constants, refreshed per pass
@@ -45,13 +43,49 @@ int km_dxp(int dx);
 constexpr int kAssignBlock = 256;  // points per assign block == grouping chunk
 
 inline int km_nchunks(int n) { return (n + kAssignBlock - 1) / kAssignBlock; }
-int km_splits(int n, int C, int dx);
 
 hipError_t km_init(const KmProblem &p, const int32_t *init, int init_stride,
                    int32_t *status, hipStream_t s);
 hipError_t km_assign(const KmProblem &p, bool with_hist, hipStream_t s);
 hipError_t km_group(const KmProblem &p, hipStream_t s);
-hipError_t km_update(const KmProblem &p, int32_t *status, hipStream_t s);
+
+// Centroid update by one streaming pass over the rows.  Up to three
+// subspaces of the same rows (channels col0[m] .. col0[m]+dx[m], C[m]
+// clusters, centroids [C[m]][dx[m]] at float offset ucol[m] of a head) are
+// updated together; their channels are cut into windows whose int64 sums
+// fit one block's LDS.
+constexpr int kAccLds = 16384;           // int64 sums per block
+constexpr int kAccCnt = 3072;            // int32 cluster counts per block
+constexpr int kAccMaxPieces = 4;
+constexpr int kAccMaxWindows = 16;
+constexpr int kAccTargetBlocks = 256;    // blocks per launch, about one per CU
+struct AccPiece {
+  int m, sub0, width;   // channels sub0 .. sub0+width of subspace m
+  int lds;              // first int64 LDS sum of the piece ([C][width])
+  int cnt;              // first LDS count of subspace m, or -1 if not counted here
+};
+struct AccWindow {
+  int npieces, lanes, elems, cnt_elems;
+  AccPiece piece[kAccMaxPieces];
+};
+struct AccPlan {
+  int nsub;
+  int C[3], dx[3], col0[3], ucol[3], ccol[3];
+  int S, SC;            // centroid elements and clusters of one head
+  int nwin, blocks;     // windows; blocks per (head, window)
+  AccWindow win[kAccMaxWindows];
+};
+bool km_accum_plan(int nsub, const int *col0, const int *dx, const int *C,
+                   int heads, int n, AccPlan *plan);
+size_t km_accum_slab_bytes(const AccPlan &p, int heads);
+size_t km_accum_cslab_bytes(const AccPlan &p, int heads);
+// assign of subspace m, head h at assign[h * a_hs + m * a_ss]; with a
+// status word, the visited inputs are also checked for |x| >= 2^22 and
+// non-finite values.
+hipError_t km_accum(const AccPlan &plan, const void *x, bool bf16, size_t x_hs,
+                    int ld, int n, int heads, const int32_t *assign,
+                    size_t a_hs, size_t a_ss, long long *slab, int32_t *cslab,
+                    float *U, size_t u_hs, int32_t *status, hipStream_t s);
 hipError_t km_pack_codes(const int32_t *a3, size_t a_head_stride,
                          size_t a_sub_stride, int n, int heads,
                          uint32_t *codes, hipStream_t s);

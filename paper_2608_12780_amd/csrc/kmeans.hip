@@ -5,9 +5,9 @@
 //   update: exact int64 sums of rint(x * 2^24) over the members, one fp64
 //           division by count * 2^24, rounded to fp32; empty clusters keep
 //           their centroid.
-// Per iteration: assign (+ per-chunk cluster histogram) -> column scan of the
-// histograms -> stable scatter into the cluster-grouped permutation ->
-// partial fixed-point sums per (cluster, split) -> finalize.
+// This file: initialisation, the VALU assignment, and the grouping of the
+// final query assignment (per-chunk cluster histograms -> column scan ->
+// stable scatter into the cluster-grouped permutation).
 #include <math.h>
 
 #include "common.h"
@@ -226,64 +226,7 @@ __global__ __launch_bounds__(kAssignBlock) void km_scatter_kernel(
   }
 }
 
-// Fixed-point partial sums of split s of cluster r: threads = (row slot,
-// channel); partial[h][r][s][c] = sum over the split's rows of
-// rint(x * 2^24).
-template <typename T>
-__global__ __launch_bounds__(256) void km_partial_kernel(
-    const T *__restrict__ X, size_t x_hs, int ld, int col0, int dx, int C,
-    int splits, const int32_t *__restrict__ offsets,
-    const int32_t *__restrict__ perm, size_t p_hs, int64_t *partial,
-    int32_t *status) {
-  __shared__ long long part[256];
-  const int s = blockIdx.x, r = blockIdx.y, h = blockIdx.z, t = threadIdx.x;
-  const int beg = offsets[static_cast<size_t>(h) * (C + 1) + r];
-  const int cnt = offsets[static_cast<size_t>(h) * (C + 1) + r + 1] - beg;
-  const int lo = beg + static_cast<int>((static_cast<long long>(cnt) * s) / splits);
-  const int hi = beg + static_cast<int>((static_cast<long long>(cnt) * (s + 1)) / splits);
-  const int slots = 256 / dx;
-  const int c = t % dx, slot = t / dx;
-  long long acc = 0;
-  int bad = 0;
-  if (slot < slots) {
-    const T *Xh = X + h * x_hs + col0 + c;
-    const int32_t *P = perm + h * p_hs;
-#pragma unroll 4
-    for (int p = lo + slot; p < hi; p += slots) {
-      const float x = load_elem(Xh, static_cast<size_t>(P[p]) * ld);
-      if (!(fabsf(x) < 4194304.0f)) bad |= isfinite(x) ? kStatusRange : (kStatusRange | kStatusNonFinite);
-      acc += static_cast<long long>(rintf(x * 16777216.0f));
-    }
-  }
-  part[t] = acc;
-  __syncthreads();
-  if (t < dx) {
-    long long tot = 0;
-    for (int g = 0; g < slots; ++g) tot += part[g * dx + t];
-    partial[((static_cast<size_t>(h) * C + r) * splits + s) * dx + t] = tot;
-  }
-  if (bad && status) atomicOr(status, bad);
-}
-
-// U[r][c] = (float)((double)sum / ((double)count * 2^24)); empty r keeps U.
-__global__ void km_finalize_kernel(int C, int dx, int splits,
-                                   const int32_t *__restrict__ offsets,
-                                   const int64_t *__restrict__ partial,
-                                   float *U, size_t u_hs) {
-  const int r = blockIdx.x, h = blockIdx.y;
-  const int cnt = offsets[static_cast<size_t>(h) * (C + 1) + r + 1] -
-                  offsets[static_cast<size_t>(h) * (C + 1) + r];
-  if (cnt <= 0) return;
-  const double den = static_cast<double>(cnt) * 16777216.0;
-  const int64_t *P = partial + (static_cast<size_t>(h) * C + r) * splits * dx;
-  for (int c = threadIdx.x; c < dx; c += blockDim.x) {
-    long long tot = 0;
-    for (int s = 0; s < splits; ++s) tot += P[static_cast<size_t>(s) * dx + c];
-    U[h * u_hs + static_cast<size_t>(r) * dx + c] =
-        static_cast<float>(static_cast<double>(tot) / den);
-  }
-}
-
+// Composite key codes zT | zH << 10 | zW << 20 (Sec. 3.3).
 __global__ void km_pack_kernel(const int32_t *__restrict__ a3, size_t a_hs,
                                size_t a_ss, int n, uint32_t *codes) {
   const int j = blockIdx.x * blockDim.x + threadIdx.x, h = blockIdx.y;
@@ -314,15 +257,6 @@ hipError_t assign_dispatch(const KmProblem &p, bool with_hist, hipStream_t s) {
 }
 
 }  // namespace
-
-int km_splits(int n, int C, int dx) {
-  const int slots = 256 / dx;
-  const long long avg = (static_cast<long long>(n) + C - 1) / C;
-  long long sp = (avg + 8LL * slots - 1) / (8LL * slots);
-  if (sp < 1) sp = 1;
-  if (sp > 16) sp = 16;
-  return static_cast<int>(sp);
-}
 
 hipError_t km_init(const KmProblem &p, const int32_t *init, int init_stride,
                    int32_t *status, hipStream_t s) {
@@ -358,26 +292,6 @@ hipError_t km_group(const KmProblem &p, hipStream_t s) {
   hipLaunchKernelGGL(km_scatter_kernel, dim3(nch, p.heads), dim3(kAssignBlock),
                      0, s, p.n, p.C, nch, p.assign, p.a_head_stride, p.counts,
                      p.chunk_rel, p.offsets, p.perm, p.a_head_stride);
-  return hipGetLastError();
-}
-
-hipError_t km_update(const KmProblem &p, int32_t *status, hipStream_t s) {
-  const dim3 grid(p.splits, p.C, p.heads);
-  if (p.bf16)
-    hipLaunchKernelGGL(km_partial_kernel<uint16_t>, grid, dim3(256), 0, s,
-                       static_cast<const uint16_t *>(p.x), p.x_head_stride,
-                       p.ld, p.col0, p.dx, p.C, p.splits, p.offsets, p.perm,
-                       p.a_head_stride, p.partial, status);
-  else
-    hipLaunchKernelGGL(km_partial_kernel<float>, grid, dim3(256), 0, s,
-                       static_cast<const float *>(p.x), p.x_head_stride, p.ld,
-                       p.col0, p.dx, p.C, p.splits, p.offsets, p.perm,
-                       p.a_head_stride, p.partial, status);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(km_finalize_kernel, dim3(p.C, p.heads), dim3(128), 0, s,
-                     p.C, p.dx, p.splits, p.offsets, p.partial, p.u,
-                     p.u_head_stride);
   return hipGetLastError();
 }
 
