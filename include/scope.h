@@ -170,8 +170,11 @@ int32_t scope_select(const scope_shape *shape, int32_t c_q,
  * input dtype, in original token order.  A cluster with r_c = 0 writes 0.
  * Dense attention (Eq. 1) is the special case of one cluster holding all
  * queries (c_q = 1, offsets = {0, n}, perm = identity) and all keys.
- * Index arrays are clamped to their valid ranges on the device, so bad
- * indices cannot fault; requires d in {64, 128}.                           */
+ * Bad indices cannot fault: index arrays are clamped to their valid
+ * ranges on the device, or read through range-checked loads that return
+ * 0 (the selected-key gather of bf16 inputs).  Requires d in {64, 128},
+ * 16-byte aligned q, k, v, o, and for bf16 inputs n * d * 2 < 2^32
+ * (n < 2^24 at d = 128), else SCOPE_ERR_UNSUPPORTED.                     */
 int32_t scope_sparse_attention(const scope_shape *shape, const void *q,
                                const void *k, const void *v, int32_t c_q,
                                const int32_t *offsets, const int32_t *perm,

@@ -395,6 +395,10 @@ int32_t scope_sparse_attention(const scope_shape *shape, const void *q,
   int32_t st = check_shape(shape);
   if (st) return st;
   if (shape->d != 64 && shape->d != 128) return SCOPE_ERR_UNSUPPORTED;
+  // the bf16 gather addresses one head's K or V with 32-bit byte offsets
+  if (shape->dtype == SCOPE_BF16 &&
+      static_cast<uint64_t>(shape->n) * shape->d * 2 >= (1ull << 32))
+    return SCOPE_ERR_UNSUPPORTED;
   if (c_q < 1 || c_q > shape->n) return SCOPE_ERR_INVALID_ARGUMENT;
   if (!q || !k || !v || !o || !offsets || !perm || !sel_counts || !sel_idx)
     return SCOPE_ERR_INVALID_ARGUMENT;

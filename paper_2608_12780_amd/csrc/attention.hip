@@ -2,16 +2,20 @@
 // dense attention (Eq. 1) as the one-cluster special case.
 //
 // Work item = (head, query cluster c, chunk of up to 32*NW of its queries).
-// The block gathers the cluster's selected keys 64 at a time: K rows into LDS
-// row-major, V rows transposed (dim-major) so both products read operands
-// straight from LDS.  Each wave owns 32 queries and runs
-//   S^T (64 keys x 32 queries) = K_tile . Q^T       bf16 MFMA 32x32x16
-//   online softmax in fp32 (exp2 domain), one query per lane column
+// The block gathers the cluster's selected keys 64 at a time, K and V rows
+// both into LDS row-major.  Each wave owns 32 queries and runs
+//   S^T (64 keys x 32 queries) = K_tile . Q^T       bf16 MFMA 32x32x16,
+//                                 two 32-key chains interleaved
+//   online softmax in fp32 (exp2 domain), one query per lane column, one
+//                                 max / rescale decision per 64-key tile
 //   O^T (d x 32 queries)      += V_tile^T . P^T      bf16 MFMA 32x32x16
 // The S^T accumulator layout is reused directly as the B operand of the
-// second product: the MFMA k-index order is matched by reading V^T with the
-// same key permutation, so P never leaves registers.  K/V tiles are double
-// buffered: the next tile's global loads are in flight during the MFMAs.
+// second product, so P never leaves registers; the matching V^T operand
+// comes from the row-major V tile through transposing LDS reads
+// (ds_read_b64_tr_b16).  K/V tiles are double buffered: the next tiles'
+// gathers are in flight during the MFMAs.  bf16 gathers go through buffer
+// resources, whose range checks turn every out-of-range index into a zero
+// read instead of a fault.
 #include <math.h>
 
 #include "common.h"
@@ -24,6 +28,8 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kBN = 64;          // keys per tile
 constexpr int kNW = 8;           // waves per block
@@ -69,20 +75,17 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel(
     const int32_t *__restrict__ perm, const int32_t *__restrict__ sel_idx,
     const int4 *__restrict__ items, float scale_log2) {
   constexpr int NT = kNW * 64;
-  constexpr int KS = D + 8;       // K tile row stride (bf16 elements)
-  constexpr int VS = kBN + 4;     // V^T tile row stride
+  constexpr int KS = D + 8;       // K and V tile row stride (bf16 elements)
   constexpr int C8 = D / 8;       // 16-byte chunks per row
   // staging: the first half of the block stages V (4 consecutive keys of one
   // 8-channel column per thread), the second half K (RK consecutive rows of
   // one 16-byte column per thread)
   constexpr int HALF = NT / 2;
-  constexpr int RK = kBN * C8 / HALF;       // K rows per staging thread
-  constexpr int VTH = 16 * C8;              // threads staging V
-  static_assert(kBN * C8 % HALF == 0 && RK >= 1 && RK <= 4 && VTH <= HALF,
-                "tile/threads mismatch");
+  constexpr int RK = kBN * C8 / HALF;       // rows per staging thread
+  static_assert(kBN * C8 % HALF == 0 && RK >= 1 && RK <= 4, "tile/threads mismatch");
   constexpr int NR = 4;                     // rows fetched per thread per tile
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kBN * KS];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][D * VS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][kBN * KS];
 
   const int item = blockIdx.x;
   if (item >= total_items) return;
@@ -131,13 +134,27 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel(
   const int32_t *sel = sel_idx + (static_cast<size_t>(h) * c_q + c) * n;
   const int ntiles = (r + kBN - 1) / kBN;
 
-  // this thread's staging role (wave-uniform, kept in scalar registers)
+  // this thread's staging role (wave-uniform, kept in scalar registers):
+  // the first half of the block stages V rows, the second K rows, both
+  // row-major, RK consecutive rows of one 16-byte column per thread
   const bool is_v = __builtin_amdgcn_readfirstlane(t) < HALF;
   const int u = is_v ? t : t - HALF;
-  const int c8 = is_v ? ((u >> 4) % C8) : (u % C8);
-  const int key0 = is_v ? 4 * (u & 15) : RK * (u / C8) % kBN;
-  const bool stores = __builtin_amdgcn_readfirstlane(is_v ? (u < VTH) : (u < HALF));
+  const int c8 = u % C8;
+  const int key0 = RK * (u / C8) % kBN;
+  const bool stores = true;
+  // transposing reads of V (ds_read_b64_tr_b16): source lane s supplies
+  // row 4*(s/32) + (s%16)/4 and channels 16*((s/16)%2) + 4*(s%4) .. +3 of a
+  // 16-key step; lane L then holds 4 consecutive keys of channel L%32
+  const int tr_off = (4 * (lane >> 5) + ((lane & 15) >> 2)) * KS + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
   const void *src = is_v ? vv : kv;
+  // bf16 inputs are gathered through buffer resources: out-of-range offsets
+  // (index slots past the key set, any bad row) read as zero in hardware,
+  // so no index needs clamping; the host guarantees n * D * 2 < 2^32
+  const __amdgpu_buffer_rsrc_t rsel = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int32_t *>(sel), static_cast<short>(0), r * 4, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t *>(static_cast<const uint16_t *>(src) + hoff), static_cast<short>(0),
+      static_cast<int>(static_cast<uint32_t>(n) * (D * 2)), 0x00020000);
 
   // Software pipeline, two tiles deep: the row indices of tile T+1 are
   // requested before the rows of tile T, so waiting for indices never waits
@@ -148,122 +165,131 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel(
   uint4 dA[NR], dB[NR];
   auto load_sel = [&](int tile, int (&sx)[NR]) {
 #pragma unroll
-    for (int i = 0; i < NR; ++i)
-      sx[i] = sel[min(tile * kBN + key0 + (is_v ? i : i % RK), n - 1)];
+    for (int i = 0; i < NR; ++i) {
+      if constexpr (BF16IN)
+        sx[i] = __builtin_amdgcn_raw_buffer_load_b32(rsel, (tile * kBN + key0 + i % RK) * 4, 0, 0);
+      else
+        sx[i] = sel[min(tile * kBN + key0 + i % RK, n - 1)];
+    }
   };
   auto load_rows = [&](const int (&sx)[NR], uint4 (&dx)[NR]) {
 #pragma unroll
     for (int i = 0; i < NR; ++i) {
-      const int row = min(max(sx[i], 0), n - 1);
-      dx[i] = load8<BF16IN>(src, hoff + static_cast<size_t>(row) * D + 8 * c8);
+      if constexpr (BF16IN) {
+        const auto v4 = __builtin_amdgcn_raw_buffer_load_b128(rsrc, sx[i] * (D * 2) + 16 * c8, 0, 0);
+        dx[i] = make_uint4(v4[0], v4[1], v4[2], v4[3]);
+      } else {
+        const int row = min(max(sx[i], 0), n - 1);
+        dx[i] = load8<BF16IN>(src, hoff + static_cast<size_t>(row) * D + 8 * c8);
+      }
     }
   };
   auto store_rows = [&](int buf, const uint4 (&dx)[NR]) {
     if (!stores) return;
-    if (!is_v) {
+    uint16_t *dst = is_v ? Vs[buf] : Ks[buf];
 #pragma unroll
-      for (int i = 0; i < RK; ++i)
-        *reinterpret_cast<uint4 *>(&Ks[buf][(key0 + i) * KS + 8 * c8]) = dx[i];
-    } else {
-      // transpose 4 keys x 8 channels in registers: one 8-byte row per channel
-      const uint32_t *w0 = reinterpret_cast<const uint32_t *>(&dx[0]);
-      const uint32_t *w1 = reinterpret_cast<const uint32_t *>(&dx[1]);
-      const uint32_t *w2 = reinterpret_cast<const uint32_t *>(&dx[2]);
-      const uint32_t *w3 = reinterpret_cast<const uint32_t *>(&dx[3]);
-#pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        uint2 lo, hi;
-        lo.x = __builtin_amdgcn_perm(w1[p], w0[p], 0x05040100u);
-        lo.y = __builtin_amdgcn_perm(w3[p], w2[p], 0x05040100u);
-        hi.x = __builtin_amdgcn_perm(w1[p], w0[p], 0x07060302u);
-        hi.y = __builtin_amdgcn_perm(w3[p], w2[p], 0x07060302u);
-        *reinterpret_cast<uint2 *>(&Vt[buf][(8 * c8 + 2 * p) * VS + key0]) = lo;
-        *reinterpret_cast<uint2 *>(&Vt[buf][(8 * c8 + 2 * p + 1) * VS + key0]) = hi;
-      }
-    }
+    for (int i = 0; i < RK; ++i)
+      *reinterpret_cast<uint4 *>(&dst[(key0 + i) * KS + 8 * c8]) = dx[i];
   };
 
   auto compute = [&](int tile, int buf) {
     if (!wave_active) return;
+    // S^T for both 32-key blocks of the tile: two independent MFMA chains,
+    // interleaved so the matrix pipe never waits on one accumulator
+    f32x16 sacc[2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      // S^T = K_blk . Q^T for one 32-key block and kQB query blocks
-      f32x16 sacc[kQB];
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int qb = 0; qb < kQB; ++qb)
+      for (int e = 0; e < 16; ++e) sacc[kb][e] = 0.0f;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) sacc[qb][e] = 0.0f;
+    for (int s = 0; s < D / 16; ++s)
 #pragma unroll
-      for (int s = 0; s < D / 16; ++s) {
+      for (int kb = 0; kb < 2; ++kb) {
         const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4 *>(
             &Ks[buf][(kb * 32 + l32) * KS + 16 * s + 8 * hf]));
-#pragma unroll
-        for (int qb = 0; qb < kQB; ++qb)
-          sacc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[qb][s], sacc[qb], 0, 0, 0);
+        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[0][s], sacc[kb], 0, 0, 0);
       }
-      // lane holds keys 32kb + 8(e/4) + 4hf + (e%4) of query column l32
-      const int kbase = tile * kBN + kb * 32;
-      if (kbase + 32 > r) {
+    // lane holds keys 32kb + 8(e/4) + 4hf + (e%4) of query column l32
+    const int kbase = tile * kBN;
+    if (kbase + kBN > r) {
 #pragma unroll
-        for (int qb = 0; qb < kQB; ++qb)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int e = 0; e < 16; ++e)
-            if (kbase + 8 * (e >> 2) + 4 * hf + (e & 3) >= r) sacc[qb][e] = -INFINITY;
-      }
-      uint4 pk[kQB][2];
+        for (int e = 0; e < 16; ++e)
+          if (kbase + 32 * kb + 8 * (e >> 2) + 4 * hf + (e & 3) >= r) sacc[kb][e] = -INFINITY;
+    }
+    float mx0 = fmaxf(sacc[0][0], sacc[0][1]), mx1 = fmaxf(sacc[1][0], sacc[1][1]);
 #pragma unroll
-      for (int qb = 0; qb < kQB; ++qb) {
-        float mx = fmaxf(fmaxf(sacc[qb][0], sacc[qb][1]), sacc[qb][2]);
+    for (int e = 2; e < 16; e += 2) {
+      mx0 = fmaxf(fmaxf(mx0, sacc[0][e]), sacc[0][e + 1]);
+      mx1 = fmaxf(fmaxf(mx1, sacc[1][e]), sacc[1][e + 1]);
+    }
+    float mx = fmaxf(mx0, mx1);
+    {
+      // the other half-wave holds the query's other keys
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+    }
+    const float mt = mx * scale_log2;
+    // rescale only when the running max falls too far behind; the branch is
+    // wave-wide but each query decides for itself (alpha = 1 otherwise), so
+    // a query's result never depends on its wave-mates
+    const bool behind = mt > m_run[0] + kRescale;
+    if (__ballot(behind)) {
+      const float m_new = behind ? fmaxf(m_run[0], mt) : m_run[0];
+      const float alpha = behind ? __builtin_amdgcn_exp2f(m_run[0] - m_new) : 1.0f;
+      l_run[0] *= alpha;
 #pragma unroll
-        for (int e = 3; e < 15; e += 2) mx = fmaxf(fmaxf(mx, sacc[qb][e]), sacc[qb][e + 1]);
-        mx = fmaxf(mx, sacc[qb][15]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float mt = mx * scale_log2;
-        // rescale only when the running max falls too far behind; the
-        // branch is wave-wide but each query decides for itself (alpha = 1
-        // otherwise), so a query's result never depends on its wave-mates
-        const bool behind = mt > m_run[qb] + kRescale;
-        if (__ballot(behind)) {
-          const float m_new = behind ? fmaxf(m_run[qb], mt) : m_run[qb];
-          const float alpha = behind ? __builtin_amdgcn_exp2f(m_run[qb] - m_new) : 1.0f;
-          l_run[qb] *= alpha;
+      for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-          for (int db = 0; db < D / 32; ++db)
+        for (int e = 0; e < 16; ++e) oacc[0][db][e] *= alpha;
+      m_run[0] = m_new;
+    }
+    const float neg_m = -m_run[0];
+    uint4 pk[2][2];
 #pragma unroll
-            for (int e = 0; e < 16; ++e) oacc[qb][db][e] *= alpha;
-          m_run[qb] = m_new;
+    for (int kb = 0; kb < 2; ++kb) {
+      float p[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) p[e] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][e], scale_log2, neg_m));
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2)
+        pk[kb][s2] = make_uint4(pack_bf16(p[8 * s2 + 0], p[8 * s2 + 1]),
+                                pack_bf16(p[8 * s2 + 2], p[8 * s2 + 3]),
+                                pack_bf16(p[8 * s2 + 4], p[8 * s2 + 5]),
+                                pack_bf16(p[8 * s2 + 6], p[8 * s2 + 7]));
+    }
+    // the row sum of the bf16 weights the PV product uses, two per dot2
+    {
+      const bf16x2 one = __builtin_bit_cast(bf16x2, 0x3F803F80u);
+      float ps[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+          const uint4 w4 = pk[kb][s2];
+          ps[0] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4.x), one, ps[0], false);
+          ps[1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4.y), one, ps[1], false);
+          ps[2] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4.z), one, ps[2], false);
+          ps[3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4.w), one, ps[3], false);
         }
-        const float neg_m = -m_run[qb];
-        float p[16];
-        float psum = 0.0f;
+      l_run[0] += (ps[0] + ps[1]) + (ps[2] + ps[3]);
+    }
+    // O^T += V_tile^T . P^T in 16-key steps, four independent accumulators
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          p[e] = __builtin_amdgcn_exp2f(fmaf(sacc[qb][e], scale_log2, neg_m));
-          psum += p[e];
-        }
-        l_run[qb] += psum;
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2)
-          pk[qb][s2] = make_uint4(pack_bf16(p[8 * s2 + 0], p[8 * s2 + 1]),
-                                  pack_bf16(p[8 * s2 + 2], p[8 * s2 + 3]),
-                                  pack_bf16(p[8 * s2 + 4], p[8 * s2 + 5]),
-                                  pack_bf16(p[8 * s2 + 6], p[8 * s2 + 7]));
-      }
-      // O^T += V_blk^T . P^T in 16-key steps; each V fragment feeds kQB MFMAs
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
-          const uint16_t *vrow = &Vt[buf][(db * 32 + l32) * VS + kb * 32 + 16 * s2];
-          const uint2 lo = *reinterpret_cast<const uint2 *>(vrow + 4 * hf);
-          const uint2 hi = *reinterpret_cast<const uint2 *>(vrow + 8 + 4 * hf);
-          const bf16x8 a = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
-#pragma unroll
-          for (int qb = 0; qb < kQB; ++qb)
-            oacc[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                a, as_bf16x8(pk[qb][s2]), oacc[qb][db], 0, 0, 0);
+          const uint16_t *vt = &Vs[buf][(kb * 32 + 16 * s2) * KS + db * 32 + tr_off];
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(vt));
+          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(vt + 8 * KS));
+          const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+          const bf16x8 a = as_bf16x8(make_uint4(l2.x, l2.y, h2.x, h2.y));
+          oacc[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              a, as_bf16x8(pk[kb][s2]), oacc[0][db], 0, 0, 0);
         }
-    }
   };
 
   // one pipeline step: compute tile T from LDS while tile T+1 (already in

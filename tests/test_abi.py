@@ -131,6 +131,8 @@ def test_attention_validation():
     assert call(hy_shape(), q=None) == INVALID
     assert call(hy_shape(), q=ctypes.c_void_p((1 << 20) + 8)) == INVALID   # 16B rows
     assert call(hy_shape(), c_q=0) == INVALID
+    # bf16 gathers use 32-bit byte offsets within one head: n * d * 2 < 2^32
+    assert call(hy_shape(n=1 << 24)) == UNSUPPORTED
 
 
 def test_proxy_scores_and_fixexp_validation():
