@@ -147,12 +147,14 @@ size_t key_ws(const scope_shape *s, const int32_t *c_m, void *base, KeyWs *w) {
 struct SelectWs {
   float *row_max;
   uint32_t *row_state;
+  uint32_t *coarse_hist;
 };
 size_t select_ws(const scope_shape *s, int c_q, void *base, SelectWs *w) {
   Carver cv(base);
   SelectWs sw;
   sw.row_max = cv.take<float>(static_cast<size_t>(s->heads) * c_q);
   sw.row_state = cv.take<uint32_t>(static_cast<size_t>(s->heads) * c_q * 4);
+  sw.coarse_hist = cv.take<uint32_t>(static_cast<size_t>(s->heads) * c_q * scope::kSelCoarseBins);
   if (w) *w = sw;
   return cv.used;
 }
@@ -380,7 +382,7 @@ int32_t scope_select(const scope_shape *shape, int32_t c_q,
   SCOPE_TRY(scope::select_run(shape->heads, shape->n, c_q, c_m, shape->d,
                               scores, tables, codes, counts, rho, k_fix,
                               base_counts, topp_counts, k_head, sel_counts,
-                              sel_idx, w.row_max, w.row_state,
+                              sel_idx, w.row_max, w.row_state, w.coarse_hist,
                               static_cast<hipStream_t>(stream)));
   return SCOPE_OK;
 }

@@ -5,17 +5,21 @@
 //   M = max logit; every key's softmax mass E_j = fixexp(s_j - M) in units
 //   of 2^-32; total and the exact target T = ceil(rho * total);
 //   radix selection of the logit where the descending cumulative mass first
-//   reaches T: one coarse pass over a monotone binning of M - s, then three
-//   digit passes (11/11/10 bits) over the order-preserving key bits inside
-//   the crossing bin; keys that tie at the crossing logit all carry the same
-//   mass E*, so the Top-p count is t = (#keys above) + ceil((T - mass
-//   above) / E*) (Eq. 7); b = max(t, k_fix) (Eq. 8).
+//   reaches T: one coarse pass over a monotone binning of M - s, one pass
+//   that gathers the logits of the crossing bin into LDS, then three digit
+//   rounds (11/11/10 bits) of the order-preserving key bits over that list
+//   (over all keys again if the bin overflows the list); keys that tie at
+//   the crossing logit all carry the same mass E*, so the Top-p count is
+//   t = (#keys above) + ceil((T - mass above) / E*) (Eq. 7);
+//   b = max(t, k_fix) (Eq. 8).  The coarse count histogram is kept for the
+//   final kernel.
 // head kernel: k_head = ceil(sum n_c b_c / sum n_c) in integers (Eq. 9),
 //   r_c = max(b_c, k_head) (Eq. 10).
 // final kernel: the rank-r_c logit by the same radix selection on counts
-//   (reused from the base kernel when r_c == t_c), then an ordered block
-//   compaction emits every key above it plus the lowest-index ties, in
-//   ascending key order.
+//   (reused from the base kernel when r_c == t_c; otherwise from the kept
+//   coarse histogram, one gathering pass and the digit rounds), then an
+//   ordered block compaction, four keys per thread, emits every key above
+//   it plus the lowest-index ties, in ascending key order.
 #include <math.h>
 
 #include "common.h"
@@ -26,8 +30,9 @@ namespace scope {
 namespace {
 
 constexpr int kSelBlock = 1024;
-constexpr int kCoarseBins = 2048;
+constexpr int kCoarseBins = kSelCoarseBins;
 constexpr int kMaxTable = 3072;
+constexpr int kCand = 8192;      // logits of the crossing coarse bin held in LDS
 
 __device__ __forceinline__ int coarse_bin(float y) {
   // y = s - M <= 0; monotone non-increasing in s
@@ -149,13 +154,13 @@ struct Cm3 {
   int v[3];
 };
 
-// Radix refinement inside coarse bin `cbin`: three digit passes over the
-// order-preserving key.  BY_MASS selects the mass target (Top-p) or the
-// count target (rank).  Returns the exact crossing key and what lies above.
-template <bool FUSED, bool BY_MASS>
-__device__ void refine(const LogitSource<FUSED> &src, int n, float M, int cbin,
-                       uint64_t target, uint32_t *hc, uint64_t *hm,
-                       uint32_t *key_out, uint32_t *cnt_above,
+// Radix refinement inside one coarse bin: three digit passes over the
+// order-preserving key of every logit the source visits (all keys of the
+// bin).  BY_MASS selects the mass target (Top-p) or the count target
+// (rank).  Returns the exact crossing key and what lies above it.
+template <bool BY_MASS, typename Visit>
+__device__ void refine(Visit visit, float M, uint64_t target, uint32_t *hc,
+                       uint64_t *hm, uint32_t *key_out, uint32_t *cnt_above,
                        uint64_t *mass_above) {
   const int shifts[3] = {21, 10, 0};
   const int widths[3] = {11, 11, 10};
@@ -167,20 +172,17 @@ __device__ void refine(const LogitSource<FUSED> &src, int n, float M, int cbin,
       if (BY_MASS) hm[b] = 0;
     }
     __syncthreads();
-    for (int j = threadIdx.x; j < n; j += kSelBlock) {
-      const float s = src(j);
-      const float y = s - M;
-      if (coarse_bin(y) != cbin) continue;
+    visit([&](float s) {
       const uint32_t key = desc_key(s);
-      if ((key & pmask) != prefix) continue;
+      if ((key & pmask) != prefix) return;
       const int dig = (key >> sh) & (nb - 1);
       atomicAdd(&hc[dig], 1u);
       if (BY_MASS) {
-        const uint64_t e = fixexp(y);
+        const uint64_t e = fixexp(s - M);
         if (e) atomicAdd(reinterpret_cast<unsigned long long *>(&hm[dig]),
                          static_cast<unsigned long long>(e));
       }
-    }
+    });
     __syncthreads();
     const uint64_t base = BY_MASS ? *mass_above : static_cast<uint64_t>(*cnt_above);
     const Crossing x = find_crossing<BY_MASS>(hc, hm, nb, base, target);
@@ -192,15 +194,73 @@ __device__ void refine(const LogitSource<FUSED> &src, int n, float M, int cbin,
   *key_out = prefix;
 }
 
+// Gathers the logits of coarse bin `cbin` into cand (one LDS slot per key,
+// reserved per wave); returns how many there are (more than kCand: the
+// list is incomplete and the caller visits all keys instead).
+template <bool FUSED>
+__device__ int gather_bin(const LogitSource<FUSED> &src, int n, float M, int cbin,
+                          float *cand, int *ncand) {
+  if (threadIdx.x == 0) *ncand = 0;
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  for (int j0 = 0; j0 < n; j0 += kSelBlock) {
+    const int j = j0 + threadIdx.x;
+    float s = 0.0f;
+    bool in = false;
+    if (j < n) {
+      s = src(j);
+      in = coarse_bin(s - M) == cbin;
+    }
+    const uint64_t mask = __ballot(in);
+    if (mask) {
+      int first = 0;
+      if (lane == static_cast<int>(__ffsll(static_cast<long long>(mask))) - 1)
+        first = atomicAdd(ncand, __popcll(mask));
+      first = __shfl(first, __ffsll(static_cast<long long>(mask)) - 1);
+      const int slot = first + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+          static_cast<uint32_t>(mask >> 32), __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u)));
+      if (in && slot < kCand) cand[slot] = s;
+    }
+  }
+  __syncthreads();
+  const int cnt = *ncand;
+  __syncthreads();
+  return cnt;
+}
+
+// Exact crossing key inside coarse bin `cbin`: over the gathered list when
+// it is complete, else over all keys.
+template <bool FUSED, bool BY_MASS>
+__device__ void refine_bin(const LogitSource<FUSED> &src, int n, float M, int cbin,
+                           uint64_t target, uint32_t *hc, uint64_t *hm, float *cand,
+                           int *ncand, uint32_t *key_out, uint32_t *cnt_above,
+                           uint64_t *mass_above) {
+  const int cnt = gather_bin<FUSED>(src, n, M, cbin, cand, ncand);
+  if (cnt <= kCand) {
+    refine<BY_MASS>([&](auto f) {
+      for (int k = threadIdx.x; k < cnt; k += kSelBlock) f(cand[k]);
+    }, M, target, hc, hm, key_out, cnt_above, mass_above);
+  } else {
+    refine<BY_MASS>([&](auto f) {
+      for (int j = threadIdx.x; j < n; j += kSelBlock) {
+        const float s = src(j);
+        if (coarse_bin(s - M) == cbin) f(s);
+      }
+    }, M, target, hc, hm, key_out, cnt_above, mass_above);
+  }
+}
+
 template <bool FUSED>
 __global__ __launch_bounds__(kSelBlock) void select_base_kernel(
     int n, int c_q, Cm3 cm, float sigma, const float *__restrict__ scores,
     const float *__restrict__ tables, const uint32_t *__restrict__ codes,
     float rho, int k_fix, int32_t *base_counts, int32_t *topp_counts,
-    float *row_max, uint32_t *row_state) {
+    float *row_max, uint32_t *row_state, uint32_t *coarse_hist) {
   __shared__ float lut[kMaxTable];
   __shared__ uint32_t hc[kCoarseBins];
   __shared__ uint64_t hm[kCoarseBins];
+  __shared__ float cand[kCand];
+  __shared__ int ncand;
   const int c = blockIdx.x, h = blockIdx.y;
   const size_t row = static_cast<size_t>(h) * c_q + c;
   const LogitSource<FUSED> src =
@@ -228,12 +288,15 @@ __global__ __launch_bounds__(kSelBlock) void select_base_kernel(
     }
     const uint64_t tot = block_sum<uint64_t>(tloc);
     __syncthreads();
+    // the coarse count histogram, for the rank selection of the final kernel
+    for (int b = threadIdx.x; b < kCoarseBins; b += kSelBlock)
+      coarse_hist[row * kCoarseBins + b] = hc[b];
     const uint64_t T = mass_target(rho, tot);
     const Crossing x = find_crossing<true>(hc, hm, kCoarseBins, 0, T);
     uint32_t cnt_above = x.cnt_before;
     uint64_t mass_above = x.mass_before;
-    refine<FUSED, true>(src, n, M, x.bin, T, hc, hm, &key_star, &cnt_above,
-                        &mass_above);
+    refine_bin<FUSED, true>(src, n, M, x.bin, T, hc, hm, cand, &ncand, &key_star,
+                            &cnt_above, &mass_above);
     const float s_star = desc_key_value(key_star);
     const uint64_t e_star = fixexp(s_star - M);
     const uint64_t need = (T - mass_above + e_star - 1) / e_star;
@@ -276,9 +339,12 @@ __global__ __launch_bounds__(kSelBlock) void select_final_kernel(
     int n, int c_q, Cm3 cm, float sigma, const float *__restrict__ scores,
     const float *__restrict__ tables, const uint32_t *__restrict__ codes,
     const int32_t *__restrict__ sel_counts, const float *__restrict__ row_max,
-    const uint32_t *__restrict__ row_state, int32_t *sel_idx) {
+    const uint32_t *__restrict__ row_state,
+    const uint32_t *__restrict__ coarse_hist, int32_t *sel_idx) {
   __shared__ float lut[kMaxTable];
   __shared__ uint32_t hc[kCoarseBins];
+  __shared__ float cand[kCand];
+  __shared__ int ncand;
   const int c = blockIdx.x, h = blockIdx.y;
   const size_t row = static_cast<size_t>(h) * c_q + c;
   int32_t *out = sel_idx + row * n;
@@ -296,34 +362,46 @@ __global__ __launch_bounds__(kSelBlock) void select_final_kernel(
     key_r = row_state[4 * row + 1];
     above = row_state[4 * row + 2];
   } else {
-    for (int b = threadIdx.x; b < kCoarseBins; b += kSelBlock) hc[b] = 0;
-    __syncthreads();
-    for (int j = threadIdx.x; j < n; j += kSelBlock)
-      atomicAdd(&hc[coarse_bin(src(j) - M)], 1u);
+    // the coarse count histogram of the base kernel (same logits, same M)
+    for (int b = threadIdx.x; b < kCoarseBins; b += kSelBlock)
+      hc[b] = coarse_hist[row * kCoarseBins + b];
     __syncthreads();
     const Crossing x = find_crossing<false>(hc, nullptr, kCoarseBins, 0,
                                             static_cast<uint64_t>(r));
     above = x.cnt_before;
     uint64_t unused = 0;
-    refine<FUSED, false>(src, n, M, x.bin, static_cast<uint64_t>(r), hc,
-                         nullptr, &key_r, &above, &unused);
+    refine_bin<FUSED, false>(src, n, M, x.bin, static_cast<uint64_t>(r), hc, nullptr,
+                             cand, &ncand, &key_r, &above, &unused);
   }
+  // ordered compaction, four consecutive keys per thread: keys above key_r
+  // and the first `need` ties in index order
   const uint32_t need = static_cast<uint32_t>(r) - above;
   uint32_t out_run = 0, ties_run = 0;
-  for (int j0 = 0; j0 < n; j0 += kSelBlock) {
-    const int j = j0 + threadIdx.x;
-    uint32_t a = 0, tie = 0;
-    if (j < n) {
-      const uint32_t key = desc_key(src(j));
-      a = key < key_r;
-      tie = key == key_r;
+  constexpr int KPT = 4;
+  for (int j0 = 0; j0 < n; j0 += KPT * kSelBlock) {
+    const int jb = j0 + KPT * threadIdx.x;
+    uint32_t fa = 0, ft = 0;  // per-key flags, bit i = key jb + i
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      if (jb + i < n) {
+        const uint32_t key = desc_key(src(jb + i));
+        fa |= static_cast<uint32_t>(key < key_r) << i;
+        ft |= static_cast<uint32_t>(key == key_r) << i;
+      }
     }
     uint32_t tot;
-    const uint32_t ex = block_excl_scan<uint32_t>((tie << 16) | a, &tot);
-    const uint32_t a_pre = ex & 0xFFFFu, t_pre = ex >> 16;
+    const uint32_t ex = block_excl_scan<uint32_t>((static_cast<uint32_t>(__popc(ft)) << 16) |
+                                                      static_cast<uint32_t>(__popc(fa)), &tot);
+    uint32_t a_pre = ex & 0xFFFFu, t_pre = ex >> 16;
     const uint32_t remaining = need > ties_run ? need - ties_run : 0u;
-    if (a || (tie && t_pre < remaining))
-      out[out_run + a_pre + min(t_pre, remaining)] = j;
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const bool a = (fa >> i) & 1u, tie = (ft >> i) & 1u;
+      if (a || (tie && t_pre < remaining))
+        out[out_run + a_pre + min(t_pre, remaining)] = jb + i;
+      a_pre += a;
+      t_pre += tie;
+    }
     out_run += (tot & 0xFFFFu) + min(tot >> 16, remaining);
     ties_run += tot >> 16;
   }
@@ -341,18 +419,18 @@ hipError_t select_run(int heads, int n, int c_q, const int *c_m, int d,
                       const uint32_t *codes, const int32_t *counts, float rho,
                       int k_fix, int32_t *base, int32_t *topp, int32_t *k_head,
                       int32_t *sel_counts, int32_t *sel_idx, float *row_max,
-                      uint32_t *row_state, hipStream_t s) {
+                      uint32_t *row_state, uint32_t *coarse_hist, hipStream_t s) {
   Cm3 cm{{c_m[0], c_m[1], c_m[2]}};
   const float sigma = static_cast<float>(1.0 / sqrt(static_cast<double>(d)));
   const dim3 grid(c_q, heads), block(kSelBlock);
   if (scores)
     hipLaunchKernelGGL(select_base_kernel<false>, grid, block, 0, s, n, c_q, cm,
                        sigma, scores, tables, codes, rho, k_fix, base, topp,
-                       row_max, row_state);
+                       row_max, row_state, coarse_hist);
   else
     hipLaunchKernelGGL(select_base_kernel<true>, grid, block, 0, s, n, c_q, cm,
                        sigma, scores, tables, codes, rho, k_fix, base, topp,
-                       row_max, row_state);
+                       row_max, row_state, coarse_hist);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(select_head_kernel, dim3(heads), block, 0, s, c_q, counts,
@@ -362,11 +440,11 @@ hipError_t select_run(int heads, int n, int c_q, const int *c_m, int d,
   if (scores)
     hipLaunchKernelGGL(select_final_kernel<false>, grid, block, 0, s, n, c_q, cm,
                        sigma, scores, tables, codes, sel_counts, row_max,
-                       row_state, sel_idx);
+                       row_state, coarse_hist, sel_idx);
   else
     hipLaunchKernelGGL(select_final_kernel<true>, grid, block, 0, s, n, c_q, cm,
                        sigma, scores, tables, codes, sel_counts, row_max,
-                       row_state, sel_idx);
+                       row_state, coarse_hist, sel_idx);
   return hipGetLastError();
 }
 
