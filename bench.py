@@ -8,10 +8,22 @@ tokens, d = 128, RoPE split 16/56/56, C_q = 256, C_m = 128, 10 iterations,
 rho = 0.9, k_fix = ceil(0.1 N)).
 
 Prints ONE JSON line on stdout; progress goes to stderr.
+
+Traffic measurement (two counter passes, then a summary on any machine):
+  rocprofv3 --pmc FETCH_SIZE --kernel-include-regex 'attn_kernel|copy' -d F -o run \
+      --output-format csv -- python3 bench.py --traffic-probe
+  rocprofv3 --pmc WRITE_SIZE --kernel-include-regex 'attn_kernel|copy' -d W -o run \
+      --output-format csv -- python3 bench.py --traffic-probe
+  python3 bench.py --traffic-summary F/run_counter_collection.csv W/run_counter_collection.csv
+The probe runs the layer once, a plain 1 GiB device copy (the calibration:
+its counters are scaled to the bytes it is known to move) and one launch of
+the sparse attention.
   value          effective TFLOP/s = dense attention flops 4 N^2 d H / layer time
   ms_per_step    layer latency
   roofline       the sparse-attention kernel against the bf16 MFMA peak
-                 (algorithmic flops 4 d sum_c n_c r_c per launch)
+                 (algorithmic flops 4 d sum_c n_c r_c per launch); traffic =
+                 its HBM bytes per launch from the committed counter summary,
+                 null when the kernel source changed since it was taken
   cpu_baseline   the CPU oracle on a bounded sample of one head, extrapolated
   dense_*        the same GPU's dense attention: the library's dense mode and
                  torch's scaled_dot_product_attention (flash backend)
@@ -32,6 +44,9 @@ sys.path.insert(0, ROOT)
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
 HBM_PEAK_GBS = 8000.0
+CALIB_BYTES = 1 << 30              # calibration copy: reads and writes this much
+ATTN_SRC = os.path.join(ROOT, "paper_2608_12780_amd", "csrc", "attention.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_kernel_hy720_hbm_traffic.txt")
 
 WORKLOAD_NAMES = {
     "hy720": "HunyuanVideo-720p-like",
@@ -131,7 +146,112 @@ def cpu_baseline(cfg, x, layer_np):
     }
 
 
+def source_digest():
+    import hashlib
+    with open(ATTN_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def committed_traffic(config_name):
+    """HBM bytes per attention launch from the committed summary, if it was
+    taken on this workload with the current kernel source."""
+    try:
+        kv = dict(l.split(": ", 1) for l in open(TRAFFIC_FILE).read().splitlines()
+                  if ": " in l and not l.startswith(" "))
+    except OSError:
+        return None
+    if kv.get("attention_source_sha256") != source_digest() or kv.get("config") != config_name:
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def traffic_summary(fetch_csv, write_csv, config_name="hy720"):
+    """Scales FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the attention
+    kernel by what the same counters read for the calibration copy."""
+    import csv
+
+    def per_dispatch(path):
+        d = {}
+        for r in csv.DictReader(open(path)):
+            key = r["Dispatch_Id"]
+            e = d.setdefault(key, {"name": r["Kernel_Name"], "v": 0.0,
+                                   "dur": int(r["End_Timestamp"]) - int(r["Start_Timestamp"])})
+            e["v"] += float(r["Counter_Value"])
+        return list(d.values())
+
+    out = {}
+    for tag, path in (("fetch", fetch_csv), ("write", write_csv)):
+        rows = per_dispatch(path)
+        # the device-to-device copy runs as the runtime's blit kernel
+        copies = [e for e in rows if "copy" in e["name"].lower()]
+        attn = [e for e in rows if "attn_kernel" in e["name"]]
+        if not copies or not attn:
+            raise SystemExit(f"{path}: calibration copy or attention dispatch missing")
+        cal = max(copies, key=lambda e: e["dur"])
+        factor = (CALIB_BYTES / 1024.0) / cal["v"]
+        a = attn[-1]
+        out[tag] = dict(copy_kib=cal["v"], factor=factor, attn_kib=a["v"],
+                        attn_bytes=a["v"] * 1024.0 * factor)
+    total = out["fetch"]["attn_bytes"] + out["write"]["attn_bytes"]
+    lines = [
+        f"config: {config_name}",
+        f"attention_source_sha256: {source_digest()}",
+        f"hbm_bytes_per_launch: {total:.6e}",
+        f"fetch_bytes_per_launch: {out['fetch']['attn_bytes']:.6e}",
+        f"write_bytes_per_launch: {out['write']['attn_bytes']:.6e}",
+        "",
+        "commands (cd /tmp && export TMPDIR=/tmp, then from the repository root):",
+        "  rocprofv3 --pmc FETCH_SIZE --kernel-include-regex 'attn_kernel|copy' -d F -o run "
+        "--output-format csv -- python3 bench.py --traffic-probe",
+        "  rocprofv3 --pmc WRITE_SIZE --kernel-include-regex 'attn_kernel|copy' -d W -o run "
+        "--output-format csv -- python3 bench.py --traffic-probe",
+        "  python3 bench.py --traffic-summary F/run_counter_collection.csv "
+        "W/run_counter_collection.csv",
+        f"  calibration: one device copy of {CALIB_BYTES} bytes read + written;",
+        f"  FETCH_SIZE copy {out['fetch']['copy_kib']:.1f} KiB -> factor {out['fetch']['factor']:.4f};",
+        f"  WRITE_SIZE copy {out['write']['copy_kib']:.1f} KiB -> factor {out['write']['factor']:.4f};",
+        f"  attention launch: FETCH_SIZE {out['fetch']['attn_kib']:.1f} KiB, "
+        f"WRITE_SIZE {out['write']['attn_kib']:.1f} KiB (raw).",
+    ]
+    return "\n".join(lines) + "\n"
+
+
+def traffic_probe():
+    import torch
+    from paper_2608_12780_amd import inputs
+    from paper_2608_12780_amd.layer import ScopeLayer
+    cfg = inputs.CONFIGS["hy720"]
+    x = inputs.generate(cfg)
+    dev = torch.device("cuda", 0)
+    up = lambda b: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
+    q, k, v = up(x.q_bits), up(x.k_bits), up(x.v_bits)
+    layer = ScopeLayer(cfg.heads, cfg.n, cfg.d, cfg.ranges, cfg.c_q, (cfg.c_m,) * 3,
+                       cfg.iters, cfg.rho, cfg.k_fix, dtype=cfg.dtype, device=dev)
+    layer.forward(q, k, v, torch.from_numpy(x.init_q).to(dev),
+                  torch.from_numpy(x.init_k).to(dev))
+    torch.cuda.synchronize()
+    log("[probe] layer done")
+    src = torch.ones(CALIB_BYTES // 2, dtype=torch.bfloat16, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+    log("[probe] calibration copy done")
+    layer.attend(q, k, v)
+    torch.cuda.synchronize()
+    log("[probe] attention done")
+
+
 def main():
+    if len(sys.argv) >= 2 and sys.argv[1] == "--traffic-summary":
+        sys.stdout.write(traffic_summary(sys.argv[2], sys.argv[3]))
+        return
+    if len(sys.argv) >= 2 and sys.argv[1] == "--traffic-probe":
+        traffic_probe()
+        return
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
@@ -234,7 +354,7 @@ def main():
             "peak": MFMA_BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
-            "traffic": None,
+            "traffic": committed_traffic(cfg.name),
             "algorithmic_flops_per_launch": attn_flops,
         },
         "stages_ms": {k_: round(v_, 3) for k_, v_ in stage_ms.items()},
