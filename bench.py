@@ -97,9 +97,9 @@ def sdpa_ms(torch, q, k, v, reps):
 def cpu_baseline(cfg, x, layer_np):
     """The oracle on one head of the workload, timed on this host's cores.
 
-    Sample: head 0; query k-means with 2 of the iterations; key-subspace
+    Sample: head 0; query k-means with 3 of the iterations; key-subspace
     k-means with 1 iteration plus the final assignment; score tables and
-    proxy logits; selection for every query cluster; attention for 64 query
+    proxy logits; selection for every query cluster; attention for 256 query
     rows.  Each stage is scaled to its full per-head work (iterations, rows)
     and the per-head sum to all heads."""
     import oracle
@@ -135,6 +135,7 @@ def cpu_baseline(cfg, x, layer_np):
         "value": dense_flops(cfg) / layer_s / 1e12,
         "unit": "TFLOP/s",
         "cores": oracle.num_threads(),
+        "cpu_model": cpu_model(),
         "kind": "oracle",
         "layer_s_extrapolated": layer_s,
         "per_head_stage_s": {k_: round(v_, 3) for k_, v_ in t.items()},
@@ -144,6 +145,16 @@ def cpu_baseline(cfg, x, layer_np):
                    f"clusters, attention for {rows}/{cfg.n} query rows; each "
                    f"stage scaled to its full work, x{cfg.heads} heads"),
     }
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def source_digest():
@@ -363,6 +374,21 @@ def main():
         "k_head_mean": float(khead.mean()),
         "floor_bound_fraction": round(floor_bound, 4),
     }
+
+    # one GPU's share of an 8-GPU node when the layer is sharded by head
+    share = max(1, math.ceil(cfg.heads / 8))
+    if share < cfg.heads:
+        sub = ScopeLayer(share, cfg.n, cfg.d, cfg.ranges, cfg.c_q, (cfg.c_m,) * 3,
+                         cfg.iters, cfg.rho, cfg.k_fix, dtype=cfg.dtype, device=dev)
+        qs, ks, vs = q[:share].contiguous(), k[:share].contiguous(), v[:share].contiguous()
+        iqs, iks = iq[:share].contiguous(), ik[:share].contiguous()
+        sub.forward(qs, ks, vs, iqs, iks)
+        torch.cuda.synchronize()
+        sh_ms = time_events(torch, lambda: sub.forward(qs, ks, vs, iqs, iks), 3, stream)
+        result["one_gpu_share"] = {"heads": share, "of_heads": cfg.heads, "gpus": 8,
+                                   "ms_per_step": round(sh_ms, 3)}
+        log(f"[bench] one GPU's share ({share} of {cfg.heads} heads): {sh_ms:.2f} ms")
+        del sub
 
     if not args.no_dense:
         dense = DenseAttention(cfg.heads, cfg.n, cfg.d, cfg.dtype, dev)

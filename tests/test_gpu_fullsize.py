@@ -1,7 +1,7 @@
 """Full-size parity in the benchmark's launch configuration.
 
 The whole layer runs on every head of a 480p/720p workload exactly as
-bench.py runs it; the oracle then recomputes one sampled head end to end
+bench.py runs it; the oracle then recomputes sampled heads end to end
 (clustering, tables, logits, selection: bit-exact) and attention for sampled
 query rows (tolerance).
 """
@@ -26,11 +26,11 @@ def _gpu():
     oracle.lib()
 
 
-@pytest.mark.parametrize("name,head", [("hy720", 13), ("wan720", 7), ("wan480", 31)])
-def test_full_size_layer_sampled_head(name, head):
+@pytest.mark.parametrize("name,heads", [("hy720", (13, 2)), ("wan720", (7,)), ("wan480", (31,))])
+def test_full_size_layer_sampled_heads(name, heads):
     cfg = inputs.CONFIGS[name]
     G.say(f"[fullsize] {name}: heads={cfg.heads} n={cfg.n} split={cfg.split}; "
-          f"oracle head {head}")
+          f"oracle heads {heads}")
     x = inputs.generate(cfg)
     layer = ScopeLayer(cfg.heads, cfg.n, cfg.d, cfg.ranges, cfg.c_q, (cfg.c_m,) * 3,
                        cfg.iters, cfg.rho, cfg.k_fix, dtype=cfg.dtype)
@@ -39,17 +39,25 @@ def test_full_size_layer_sampled_head(name, head):
                   torch.from_numpy(x.init_k).cuda())
     torch.cuda.synchronize()
     assert int(layer.status.item()) == 0
-    g = lambda t: t[head:head + 1].cpu().numpy()
-    gpu = dict(assign=g(layer.assign), counts=g(layer.counts), offsets=g(layer.offsets),
-               perm=g(layer.perm), centroids=g(layer.q_centroids),
-               k_centroids=g(layer.k_centroids), codes=g(layer.codes).view(np.uint32),
-               tables=g(layer.tables), base=g(layer.base_counts), topp=g(layer.topp_counts),
-               k_head=g(layer.k_head), sel_counts=g(layer.sel_counts),
-               sel_idx=g(layer.sel_idx), out=layer.out[head:head + 1].float().cpu().numpy())
+    gpus = {}
+    for head in heads:
+        g = lambda t: t[head:head + 1].cpu().numpy()
+        gpus[head] = dict(assign=g(layer.assign), counts=g(layer.counts), offsets=g(layer.offsets),
+                          perm=g(layer.perm), centroids=g(layer.q_centroids),
+                          k_centroids=g(layer.k_centroids), codes=g(layer.codes).view(np.uint32),
+                          tables=g(layer.tables), base=g(layer.base_counts),
+                          topp=g(layer.topp_counts), k_head=g(layer.k_head),
+                          sel_counts=g(layer.sel_counts), sel_idx=g(layer.sel_idx),
+                          out=layer.out[head:head + 1].float().cpu().numpy())
     del layer, q, k, v
     torch.cuda.empty_cache()
-    G.say(f"[fullsize] {name}: GPU layer done; running the oracle on head {head}")
+    G.say(f"[fullsize] {name}: GPU layer done")
+    for head in heads:
+        check_head(cfg, x, head, gpus.pop(head), name)
 
+
+def check_head(cfg, x, head, gpu, name):
+    G.say(f"[fullsize] {name}: oracle on head {head}")
     hq, hk, hv = x.q[head:head + 1], x.k[head:head + 1], x.v[head:head + 1]
     cm = (cfg.c_m,) * 3
     qr = oracle.cluster_queries(hq, cfg.c_q, cfg.iters, x.init_q[head:head + 1])
@@ -67,7 +75,7 @@ def test_full_size_layer_sampled_head(name, head):
     sel = oracle.select(S, qr["counts"], cfg.rho, cfg.k_fix)
     del S
     G.assert_same_selection(gpu, sel)
-    G.say(f"[fullsize] {name}: clustering, tables and selection bit-exact; "
+    G.say(f"[fullsize] {name}: head {head} clustering, tables and selection bit-exact; "
           f"k_head {int(gpu['k_head'][0])}")
 
     # attention for 4 x 32 sampled rows of 4 sampled clusters
@@ -83,5 +91,5 @@ def test_full_size_layer_sampled_head(name, head):
                            sel["sel_idx"], row_mask=mask)
     rows = np.flatnonzero(mask[0])
     mx, mr = G.assert_attention_close(gpu["out"][0, rows], ref[0, rows])
-    G.say(f"[fullsize] {name}: attention on {len(rows)} rows max-abs {mx:.3e} "
+    G.say(f"[fullsize] {name}: head {head} attention on {len(rows)} rows max-abs {mx:.3e} "
           f"mean-rel {mr:.3e}")

@@ -23,6 +23,11 @@ MID_HY = inputs.LayerConfig("mid_hy", 2, (5, 19, 23), 128, (16, 56, 56), 32, 16,
                             4, 0.9, inputs.ceil_tenth(5 * 19 * 23), "bf16", 8, 7)
 MID_WAN = inputs.LayerConfig("mid_wan", 1, (4, 10, 13), 128, (44, 42, 42), 16, 8,
                              3, 0.9, inputs.ceil_tenth(520), "bf16", 8, 8)
+# the paper's operating point: C_q = 300 and C_m = 333 (not powers of two;
+# C_q = 300 at d = 128 takes the fp32 VALU assignment, C_m = 333 padded
+# bf16 codebooks on the matrix cores)
+PAPER_POINT = inputs.LayerConfig("paper_point", 1, (6, 20, 24), 128, (16, 56, 56), 300, 333,
+                                 3, 0.9, inputs.ceil_tenth(6 * 20 * 24), "bf16", 8, 9)
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -95,6 +100,10 @@ def test_mid_layer_hunyuan_split_ragged():
 
 def test_mid_layer_wan_split():
     check_layer(MID_WAN)
+
+
+def test_paper_operating_point_cluster_counts():
+    check_layer(PAPER_POINT)
 
 
 def test_selection_from_materialised_scores_is_identical():
