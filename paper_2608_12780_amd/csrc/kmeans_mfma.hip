@@ -205,9 +205,8 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
       const float beta = (2.0f * nx * (E + kappa * Nmax) +
                           0x1p-23f * (numax + 2.02f * nx * Nmax)) * 1.01f + 1e-25f;
 
-      // one pass: smallest and second-smallest packed score per point
-      float m1 = INFINITY, m2 = INFINITY;
-      for (int rb = 0; rb < cpad; rb += 32) {
+      // approximate scores of the 32 centroids rb .. rb+31 for the 32 points
+      auto chain = [&](int rb) {
         f32x16 acc;
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
@@ -219,15 +218,31 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
           acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_hi, xf[s], acc, 0, 0, 0);
           acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_lo, xf[s], acc, 0, 0, 0);
         }
+        return acc;
+      };
+      // one pass: smallest and second-smallest packed score per point (med3
+      // keeps the two smallest of {m1, m2, sp}; the start value lies above
+      // every score of valid inputs)
+      float m1 = 0x1.1p127f, m2 = 0x1.1p127f;
+      auto fold = [&](const f32x16 &acc, int rb) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const uint32_t r = static_cast<uint32_t>(rb + 8 * (e >> 2) + 4 * hf + (e & 3));
           const float sc = fmaf(-2.0f, acc[e], nus[r]);
           const float sp = __uint_as_float((__float_as_uint(sc) & ~imask) | r);
-          m2 = fminf(m2, fmaxf(m1, sp));
-          m1 = fminf(m1, sp);
+          m2 = __builtin_amdgcn_fmed3f(m1, m2, sp);
+          m1 = __builtin_amdgcn_fmed3f(m1, sp, -0x1.1p127f);
         }
+      };
+      // software pipeline: the scores of block rb are folded while the
+      // MFMAs of block rb + 32 run
+      f32x16 prev = chain(0);
+      for (int rb = 32; rb < cpad; rb += 32) {
+        const f32x16 cur = chain(rb);
+        fold(prev, rb - 32);
+        prev = cur;
       }
+      fold(prev, cpad - 32);
       {
         const float o1 = __shfl_xor(m1, 32), o2 = __shfl_xor(m2, 32);
         m2 = fminf(fmaxf(m1, o1), fminf(m2, o2));
@@ -247,17 +262,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
         wave_sync();
         bool over = false;
         for (int rb = 0; rb < cpad; rb += 32) {
-          f32x16 acc;
-#pragma unroll
-          for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
-          const uint16_t *urow = &Us[(rb + l32) * US + 8 * hf];
-#pragma unroll
-          for (int s = 0; s < KS; ++s) {
-            const bf16x8 a_hi = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(urow + 16 * s));
-            const bf16x8 a_lo = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(urow + DXP + 16 * s));
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_hi, xf[s], acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_lo, xf[s], acc, 0, 0, 0);
-          }
+          const f32x16 acc = chain(rb);
           if (needy) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
