@@ -113,7 +113,7 @@ size_t query_ws(const scope_shape *s, int c_q, void *base, QueryWs *w) {
   const int cpad = scope::km_cpad(c_q);
   q.ubf = cv.take<uint16_t>(static_cast<size_t>(s->heads) * cpad * 2 * scope::km_dxp(s->d));
   q.nu = cv.take<float>(static_cast<size_t>(s->heads) * cpad);
-  q.bnd = cv.take<float>(static_cast<size_t>(s->heads) * 4);
+  q.bnd = cv.take<float>(static_cast<size_t>(s->heads) * cpad * 2);
   if (w) *w = q;
   return cv.used;
 }
@@ -138,7 +138,7 @@ size_t key_ws(const scope_shape *s, const int32_t *c_m, void *base, KeyWs *w) {
     const int cpad = scope::km_cpad(C);
     k.ubf[m] = cv.take<uint16_t>(H * cpad * 2 * scope::km_dxp(dx));
     k.nu[m] = cv.take<float>(H * cpad);
-    k.bnd[m] = cv.take<float>(H * 4);
+    k.bnd[m] = cv.take<float>(H * cpad * 2);
   }
   if (w) *w = k;
   return cv.used;

@@ -31,7 +31,7 @@ struct KmProblem {
   int cpad, dxp;          // centroids padded to 32, channels padded to 16
   uint16_t *ubf;          // [heads][cpad][2 * dxp]: bf16 hi then lo terms
   float *nu;              // [heads][cpad]
-  float *bnd;             // [heads][4]
+  float *bnd;             // [heads][cpad][2]: per-row bound parts
 };
 
 // Whether the matrix-core assignment applies: bf16 rows at even offsets and

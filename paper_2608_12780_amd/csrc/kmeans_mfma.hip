@@ -58,69 +58,61 @@ __device__ __forceinline__ uint32_t asc_key(float f) {
 }
 
 // Per pass: two-term bf16 codebook [cpad][2*DXP] (hi then lo, zero padded),
-// canonical squared norms (FLT_MAX for padding rows, which never win), the
-// bound constants of each head, and zeroed chunk histograms.
+// canonical squared norms (FLT_MAX for padding rows, which never win), and
+// per-row bound parts [cpad][2] = (|u - hi - lo|, max(|u|, |hi| + |lo|)),
+// evaluated in fp64; the assignment kernel takes the per-head maxima.  One
+// wave per row: lanes split the channels, lane 0 keeps the norm's fma chain
+// in channel order.
 template <int DXP>
-__global__ __launch_bounds__(1024) void km_prep_kernel(
+__global__ __launch_bounds__(256) void km_prep_kernel(
     const float *__restrict__ U, size_t u_hs, int C, int cpad, int dx,
     uint16_t *ubf, float *nu, float *bnd) {
-  __shared__ float red[3][16];
-  const int h = blockIdx.x, t = threadIdx.x;
-  float e_max = 0.0f, n_max = 0.0f, nu_max = 0.0f;
-  for (int r = t; r < cpad; r += blockDim.x) {
-    uint16_t *dst = ubf + (static_cast<size_t>(h) * cpad + r) * (2 * DXP);
-    if (r < C) {
-      const float *u = U + h * u_hs + static_cast<size_t>(r) * dx;
-      float nr = 0.0f;
-      double e2 = 0.0, n2 = 0.0, h2 = 0.0, l2 = 0.0;
-      for (int c = 0; c < dx; ++c) {
-        nr = fmaf(u[c], u[c], nr);
-        const uint16_t bh = to_bf16(u[c]);
-        const float rest = u[c] - bf16_to_f32(bh);  // exact
-        const uint16_t bl = to_bf16(rest);
-        const double df = static_cast<double>(rest) - static_cast<double>(bf16_to_f32(bl));
-        e2 += df * df;
-        n2 += static_cast<double>(u[c]) * static_cast<double>(u[c]);
-        h2 += static_cast<double>(bf16_to_f32(bh)) * static_cast<double>(bf16_to_f32(bh));
-        l2 += static_cast<double>(bf16_to_f32(bl)) * static_cast<double>(bf16_to_f32(bl));
-        dst[c] = bh;
-        dst[DXP + c] = bl;
-      }
-      for (int c = dx; c < DXP; ++c) {
-        dst[c] = 0;
-        dst[DXP + c] = 0;
-      }
-      nu[static_cast<size_t>(h) * cpad + r] = nr;
-      e_max = fmaxf(e_max, static_cast<float>(sqrt(e2)));
-      n_max = fmaxf(n_max, static_cast<float>(fmax(sqrt(n2), sqrt(h2) + sqrt(l2))));
-      nu_max = fmaxf(nu_max, fabsf(nr));
-    } else {
-      for (int c = 0; c < 2 * DXP; ++c) dst[c] = 0;
-      nu[static_cast<size_t>(h) * cpad + r] = 0x1.fffffep127f;
+  const int h = blockIdx.y, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= cpad) return;
+  uint16_t *dst = ubf + (static_cast<size_t>(h) * cpad + r) * (2 * DXP);
+  const size_t row = static_cast<size_t>(h) * cpad + r;
+  if (r >= C) {
+    for (int c = lane; c < 2 * DXP; c += 64) dst[c] = 0;
+    if (lane == 0) {
+      nu[row] = 0x1.fffffep127f;
+      bnd[2 * row + 0] = 0.0f;
+      bnd[2 * row + 1] = 0.0f;
     }
+    return;
   }
-  e_max = wave_max(e_max);
-  n_max = wave_max(n_max);
-  nu_max = wave_max(nu_max);
-  const int lane = t & 63, w = t >> 6;
+  const float *u = U + h * u_hs + static_cast<size_t>(r) * dx;
+  double e2 = 0.0, n2 = 0.0, h2 = 0.0, l2 = 0.0;
+  for (int c = lane; c < DXP; c += 64) {
+    uint16_t bh = 0, bl = 0;
+    if (c < dx) {
+      const float x = u[c];
+      bh = to_bf16(x);
+      const float rest = x - bf16_to_f32(bh);  // exact
+      bl = to_bf16(rest);
+      const double df = static_cast<double>(rest) - static_cast<double>(bf16_to_f32(bl));
+      const double fh = bf16_to_f32(bh), fl = bf16_to_f32(bl);
+      e2 += df * df;
+      n2 += static_cast<double>(x) * static_cast<double>(x);
+      h2 += fh * fh;
+      l2 += fl * fl;
+    }
+    dst[c] = bh;
+    dst[DXP + c] = bl;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    e2 += __shfl_xor(e2, o);
+    n2 += __shfl_xor(n2, o);
+    h2 += __shfl_xor(h2, o);
+    l2 += __shfl_xor(l2, o);
+  }
   if (lane == 0) {
-    red[0][w] = e_max;
-    red[1][w] = n_max;
-    red[2][w] = nu_max;
-  }
-  __syncthreads();
-  if (t == 0) {
-    float a = 0.0f, b = 0.0f, c = 0.0f;
-    for (int i = 0; i < static_cast<int>(blockDim.x >> 6); ++i) {
-      a = fmaxf(a, red[0][i]);
-      b = fmaxf(b, red[1][i]);
-      c = fmaxf(c, red[2][i]);
-    }
-    // small upward slack on top of the fp64 evaluation
-    bnd[4 * h + 0] = a * 1.001f + 1e-30f;
-    bnd[4 * h + 1] = b * 1.001f;
-    bnd[4 * h + 2] = c * 1.001f;
-    bnd[4 * h + 3] = 0.0f;
+    float nr = 0.0f;
+    for (int c = 0; c < dx; ++c) nr = fmaf(u[c], u[c], nr);
+    nu[row] = nr;
+    bnd[2 * row + 0] = static_cast<float>(sqrt(e2));
+    bnd[2 * row + 1] = static_cast<float>(fmax(sqrt(n2), sqrt(h2) + sqrt(l2)));
   }
 }
 
@@ -146,6 +138,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
   __shared__ uint32_t cand[kWavesPerBlock][kWaveCand];
   __shared__ unsigned long long best[kWavesPerBlock][32];
   __shared__ int ncand[kWavesPerBlock];
+  __shared__ float red[3][kWavesPerBlock];
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6, l32 = lane & 31, hf = lane >> 5;
 
@@ -173,10 +166,38 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
       *reinterpret_cast<uint4 *>(&Us[r * US + 8 * q]) =
           *reinterpret_cast<const uint4 *>(ub + static_cast<size_t>(r) * (2 * DXP) + 8 * q);
     }
-    for (int r = t; r < cpad; r += 64 * kWavesPerBlock) nus[r] = nu[static_cast<size_t>(h) * cpad + r];
+    // the head's bound constants: maxima of the per-row parts, with a small
+    // upward slack on top of their fp64 evaluation
+    float e_max = 0.0f, n_max = 0.0f, nu_max = 0.0f;
+    for (int r = t; r < cpad; r += 64 * kWavesPerBlock) {
+      const size_t row = static_cast<size_t>(h) * cpad + r;
+      const float v = nu[row];
+      nus[r] = v;
+      if (r < C) {
+        e_max = fmaxf(e_max, bnd[2 * row + 0]);
+        n_max = fmaxf(n_max, bnd[2 * row + 1]);
+        nu_max = fmaxf(nu_max, fabsf(v));
+      }
+    }
+    e_max = wave_max(e_max);
+    n_max = wave_max(n_max);
+    nu_max = wave_max(nu_max);
+    if (lane == 0) {
+      red[0][w] = e_max;
+      red[1][w] = n_max;
+      red[2][w] = nu_max;
+    }
     __syncthreads();
-
-    const float E = bnd[4 * h + 0], Nmax = bnd[4 * h + 1], numax = bnd[4 * h + 2];
+    float E = 0.0f, Nmax = 0.0f, numax = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kWavesPerBlock; ++i) {
+      E = fmaxf(E, red[0][i]);
+      Nmax = fmaxf(Nmax, red[1][i]);
+      numax = fmaxf(numax, red[2][i]);
+    }
+    E = E * 1.001f + 1e-30f;
+    Nmax *= 1.001f;
+    numax *= 1.001f;
     const float *Uh = U + h * u_hs;
     for (long long g = beg + w; g < seg_end; g += kWavesPerBlock) {
       const int sl = static_cast<int>(g - static_cast<long long>(h) * nslices);
@@ -331,7 +352,7 @@ __global__ void km_zero_kernel(int32_t *p, size_t count) {
 
 template <int DXP>
 hipError_t launch_mfma(const KmProblem &p, bool with_hist, hipStream_t s) {
-  hipLaunchKernelGGL(km_prep_kernel<DXP>, dim3(p.heads), dim3(1024), 0, s, p.u,
+  hipLaunchKernelGGL(km_prep_kernel<DXP>, dim3((p.cpad + 3) / 4, p.heads), dim3(256), 0, s, p.u,
                      p.u_head_stride, p.C, p.cpad, p.dx, p.ubf, p.nu, p.bnd);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
