@@ -23,6 +23,10 @@ MID_HY = inputs.LayerConfig("mid_hy", 2, (5, 19, 23), 128, (16, 56, 56), 32, 16,
                             4, 0.9, inputs.ceil_tenth(5 * 19 * 23), "bf16", 8, 7)
 MID_WAN = inputs.LayerConfig("mid_wan", 1, (4, 10, 13), 128, (44, 42, 42), 16, 8,
                              3, 0.9, inputs.ceil_tenth(520), "bf16", 8, 8)
+# d = 64 in bf16: 16- and 32-channel codebooks on the matrix cores and the
+# d = 64 attention kernel inside the sparse layer
+MID_D64 = inputs.LayerConfig("mid_d64", 2, (4, 12, 17), 64, (16, 24, 24), 24, 12,
+                             3, 0.9, inputs.ceil_tenth(4 * 12 * 17), "bf16", 6, 10)
 # the paper's operating point: C_q = 300 and C_m = 333 (not powers of two;
 # C_q = 300 at d = 128 takes the fp32 VALU assignment, C_m = 333 padded
 # bf16 codebooks on the matrix cores)
@@ -104,6 +108,10 @@ def test_mid_layer_wan_split():
 
 def test_paper_operating_point_cluster_counts():
     check_layer(PAPER_POINT)
+
+
+def test_mid_layer_d64_bf16():
+    check_layer(MID_D64)
 
 
 def test_selection_from_materialised_scores_is_identical():
