@@ -114,6 +114,12 @@ def test_mid_layer_d64_bf16():
     check_layer(MID_D64)
 
 
+@pytest.mark.parametrize("rho", [0.5, 0.95])
+def test_mid_layer_stress_temperatures(rho):
+    # per-head temperatures on Q spread the proxy softmax from flat to peaked
+    check_layer(MID_HY.with_(name=f"mid_stress_{rho}", stress=True, rho=rho, seed=11))
+
+
 def test_selection_from_materialised_scores_is_identical():
     cfg = MID_HY
     x = inputs.generate(cfg)
