@@ -8,7 +8,9 @@
 // The rows are streamed once, in storage order.  A block owns a contiguous
 // row range of one head and one channel window; for every row it adds the
 // window's channels to the sums of the row's cluster in LDS (int64 LDS
-// atomics) and counts the row.  All three key subspaces fit one window, so
+// atomics, laid out so the lanes of a row hit consecutive slots) and counts
+// the row.  Lanes take 4 channels (8-byte loads) where the channel ranges
+// allow, else 2.  All three key subspaces fit one window, so
 // one pass over K updates T, H and W together; the query codebook is split
 // over two windows.  Each block writes its sums to a slab laid out like the
 // centroids; a second kernel reduces the slabs and divides.
@@ -43,35 +45,47 @@ __device__ __forceinline__ void check_value(float x, int &bad) {
     bad |= isfinite(x) ? kStatusRange : (kStatusRange | kStatusNonFinite);
 }
 
-// Two adjacent channels of a row: one aligned load when VEC (every pair
-// complete and aligned), else two loads, the second repeating the first
-// where the pair has one channel.
-template <typename T, bool VEC> struct Pair;
-template <bool VEC> struct Pair<uint16_t, VEC> {
-  typedef uint32_t type;
-  static __device__ __forceinline__ type load(const uint16_t *p, bool two) {
-    if (VEC) return *reinterpret_cast<const uint32_t *>(p);
-    return static_cast<uint32_t>(p[0]) | (static_cast<uint32_t>(p[two ? 1 : 0]) << 16);
+// CPL (2 or 4) adjacent channels of a row as floats.  VEC: one aligned load
+// of the whole chunk (every chunk complete); else scalar loads, repeating the
+// first element past the `nvalid` channels the chunk has.
+template <typename T, int CPL, bool VEC>
+__device__ __forceinline__ void load_chunk(const T *p, int nvalid, float (&x)[CPL]) {
+  if constexpr (sizeof(T) == 2) {
+    if constexpr (VEC && CPL == 4) {
+      const uint2 v = *reinterpret_cast<const uint2 *>(p);
+      x[0] = __uint_as_float(v.x << 16);
+      x[1] = __uint_as_float(v.x & 0xFFFF0000u);
+      x[2] = __uint_as_float(v.y << 16);
+      x[3] = __uint_as_float(v.y & 0xFFFF0000u);
+    } else if constexpr (VEC) {
+      const uint32_t v = *reinterpret_cast<const uint32_t *>(p);
+      x[0] = __uint_as_float(v << 16);
+      x[1] = __uint_as_float(v & 0xFFFF0000u);
+    } else {
+#pragma unroll
+      for (int e = 0; e < CPL; ++e) x[e] = bf16_to_f32(p[e < nvalid ? e : 0]);
+    }
+  } else {
+    if constexpr (VEC && CPL == 4) {
+      const float4 v = *reinterpret_cast<const float4 *>(p);
+      x[0] = v.x; x[1] = v.y; x[2] = v.z; x[3] = v.w;
+    } else if constexpr (VEC) {
+      const float2 v = *reinterpret_cast<const float2 *>(p);
+      x[0] = v.x; x[1] = v.y;
+    } else {
+#pragma unroll
+      for (int e = 0; e < CPL; ++e) x[e] = p[e < nvalid ? e : 0];
+    }
   }
-  static __device__ __forceinline__ float first(type v) { return __uint_as_float(v << 16); }
-  static __device__ __forceinline__ float second(type v) { return __uint_as_float(v & 0xFFFF0000u); }
-};
-template <bool VEC> struct Pair<float, VEC> {
-  typedef float2 type;
-  static __device__ __forceinline__ type load(const float *p, bool two) {
-    if (VEC) return *reinterpret_cast<const float2 *>(p);
-    return make_float2(p[0], p[two ? 1 : 0]);
-  }
-  static __device__ __forceinline__ float first(type v) { return v.x; }
-  static __device__ __forceinline__ float second(type v) { return v.y; }
-};
+}
 
-template <typename T, bool VEC, bool CHECK>
+template <typename T, int CPL, bool VEC, bool CHECK>
 __global__ __launch_bounds__(kAccThreads) void km_accum_kernel(
     const T *__restrict__ X, size_t x_hs, int ld, int n, const AccPlan plan,
     const int32_t *__restrict__ assign, size_t a_hs, size_t a_ss,
     long long *slab, int32_t *cslab, int32_t *status) {
-  __shared__ unsigned long long sums[kAccLds];
+  // the last CPL sums are a sink for lanes that hold no channels
+  __shared__ unsigned long long sums[kAccLds + 4];
   __shared__ int cnts[kAccCnt];
   const int b = blockIdx.x, wi = blockIdx.y, h = blockIdx.z, t = threadIdx.x;
   const AccWindow &W = plan.win[wi];
@@ -79,59 +93,69 @@ __global__ __launch_bounds__(kAccThreads) void km_accum_kernel(
   for (int e = t; e < W.cnt_elems; e += kAccThreads) cnts[e] = 0;
   __syncthreads();
 
-  // lane -> (row within the wave's row group, piece, channel pair)
+  // lanes per row: one per CPL channels of each piece
+  int lanes = 0;
+  for (int q = 0; q < W.npieces; ++q) lanes += (W.piece[q].width + CPL - 1) / CPL;
+  // lane -> (row within the wave's row group, piece, channel chunk)
   const int lane = t & 63, wv = t >> 6;
-  const int rpw = 64 / W.lanes;
-  const int rr = lane / W.lanes, pl = lane % W.lanes;
+  const int rpw = 64 / lanes;
+  const int rr = lane / lanes, pl = lane % lanes;
   const bool active = rr < rpw;
   int p = 0, first = 0;
-  while (p + 1 < W.npieces && pl >= first + (W.piece[p].width + 1) / 2) {
-    first += (W.piece[p].width + 1) / 2;
+  while (p + 1 < W.npieces && pl >= first + (W.piece[p].width + CPL - 1) / CPL) {
+    first += (W.piece[p].width + CPL - 1) / CPL;
     ++p;
   }
   // the piece's fields, held in registers for the row loop
-  const int pm = W.piece[p].m, p_width = W.piece[p].width, p_lds = W.piece[p].lds;
+  const int pm = W.piece[p].m, p_width = W.piece[p].width;
   const int p_cnt = W.piece[p].cnt, p_sub0 = W.piece[p].sub0;
-  const int j = 2 * (pl - first);                // channel of the pair in the piece
-  const bool two = j + 1 < p_width;
+  const int j = CPL * (pl - first);              // first channel of the chunk in the piece
+  const int nvalid = min(CPL, p_width - j);
   const int Cm = plan.C[pm];
   const T *xb = X + h * x_hs + plan.col0[pm] + p_sub0 + j;
   const int32_t *ab = assign + h * a_hs + pm * a_ss;
-  const bool counter = p_cnt >= 0 && j == 0;
+  const bool counter = active && p_cnt >= 0 && j == 0;
+  // LDS sums of a cluster's piece: with vector loads, element e of chunk c
+  // at e * (width / CPL) + c, so for each e the lanes of a row add to
+  // consecutive slots (no bank conflicts); idle lanes add into the sink
+  const int e_stride = VEC ? p_width / CPL : 1;
+  const int lds_base = active ? W.piece[p].lds + (VEC ? j / CPL : j) : kAccLds;
+  const int lds_stride = active ? p_width : 0;
   int bad = 0;
 
   const int lo = static_cast<int>((static_cast<long long>(n) * b) / gridDim.x);
   const int hi = static_cast<int>((static_cast<long long>(n) * (b + 1)) / gridDim.x);
   const int step = kAccWaves * rpw;  // rows per block step
   constexpr int U = 4;
-  for (int g = lo + wv * rpw + rr; g - rr < hi; g += U * step) {
-    typename Pair<T, VEC>::type xv[U];
+  // one group of U rows per lane; FULL: every row of the group is in range
+  auto group = [&](int g, bool full) {
+    float xv[U][CPL];
     int av[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int row = g + u * step;
-      const int rc = (active && row < hi) ? row : lo;
+      const int rc = (active && (full || row < hi)) ? row : lo;
       av[u] = ab[rc];
-      xv[u] = Pair<T, VEC>::load(xb + static_cast<size_t>(rc) * ld, two);
+      load_chunk<T, CPL, VEC>(xb + static_cast<size_t>(rc) * ld, nvalid, xv[u]);
     }
-    // branch-free: rows past the range (and idle lanes) add zeros
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int row = g + u * step;
-      const bool ok = active && row < hi;
+      const bool ok = full || row < hi;
       const int a = min(static_cast<unsigned>(av[u]), static_cast<unsigned>(Cm - 1));
-      const int idx = p_lds + a * p_width + j;
-      const float x0 = ok ? Pair<T, VEC>::first(xv[u]) : 0.0f;
-      const float x1 = ok ? Pair<T, VEC>::second(xv[u]) : 0.0f;
-      if (CHECK) {
-        check_value(x0, bad);
-        check_value(x1, bad);
+      const int idx = lds_base + a * lds_stride;
+#pragma unroll
+      for (int e = 0; e < CPL; ++e) {
+        const float x = ok ? xv[u][e] : 0.0f;
+        if (CHECK && e < nvalid) check_value(x, bad);
+        if (VEC || e < nvalid) atomicAdd(&sums[idx + (active ? e * e_stride : e)], fixed24(x));
       }
-      atomicAdd(&sums[idx], fixed24(x0));
-      if (VEC || two) atomicAdd(&sums[idx + 1], fixed24(x1));
       if (counter) atomicAdd(&cnts[p_cnt + a], ok ? 1 : 0);
     }
-  }
+  };
+  int g = lo + wv * rpw + rr;
+  for (; (g - rr) + (U - 1) * step + rpw - 1 < hi; g += U * step) group(g, true);
+  if (g - rr < hi) group(g, false);
   if (CHECK && status && bad) atomicOr(status, bad);
   __syncthreads();
 
@@ -140,10 +164,12 @@ __global__ __launch_bounds__(kAccThreads) void km_accum_kernel(
   for (int q = 0; q < W.npieces; ++q) {
     const AccPiece &Q = W.piece[q];
     const int m = Q.m, cnt = plan.C[m] * Q.width;
+    const int cw = Q.width / CPL;
     for (int e = t; e < cnt; e += kAccThreads) {
       const int r = e / Q.width, k = e - r * Q.width;
+      const int off = VEC ? (k % CPL) * cw + k / CPL : k;
       sl[plan.ucol[m] + static_cast<size_t>(r) * plan.dx[m] + Q.sub0 + k] =
-          static_cast<long long>(sums[Q.lds + e]);
+          static_cast<long long>(sums[Q.lds + r * Q.width + off]);
     }
     if (Q.cnt >= 0) {
       int32_t *cs = cslab + (static_cast<size_t>(h) * gridDim.x + b) * plan.SC + plan.ccol[m];
@@ -258,21 +284,32 @@ hipError_t km_accum(const AccPlan &plan, const void *x, bool bf16, size_t x_hs,
                     float *U, size_t u_hs, int32_t *status, hipStream_t s) {
   const dim3 grid(plan.blocks, plan.nwin, heads);
   const bool check = status != nullptr;
-  // paired loads need complete pairs starting on pair boundaries
-  bool vec = (ld % 2 == 0) && (x_hs % 2 == 0) &&
-             reinterpret_cast<uintptr_t>(x) % (bf16 ? 4 : 8) == 0;
-  for (int m = 0; m < plan.nsub; ++m) vec = vec && plan.col0[m] % 2 == 0 && plan.dx[m] % 2 == 0;
-#define SCOPE_ACCUM(T, V, K)                                                     \
-  hipLaunchKernelGGL((km_accum_kernel<T, V, K>), grid, dim3(kAccThreads), 0, s,  \
-                     static_cast<const T *>(x), x_hs, ld, n, plan, assign, a_hs,  \
+  // vector loads need complete chunks starting on chunk boundaries
+  auto aligned = [&](int cpl) {
+    const size_t bytes = static_cast<size_t>(cpl) * (bf16 ? 2 : 4);
+    if (ld % cpl || x_hs % cpl || reinterpret_cast<uintptr_t>(x) % bytes) return false;
+    for (int w = 0; w < plan.nwin; ++w)
+      for (int q = 0; q < plan.win[w].npieces; ++q) {
+        const AccPiece &pc = plan.win[w].piece[q];
+        if ((plan.col0[pc.m] + pc.sub0) % cpl || pc.width % cpl) return false;
+      }
+    return true;
+  };
+  const bool v4 = aligned(4), v2 = aligned(2);
+#define SCOPE_ACCUM(T, CPL, V, K)                                                    \
+  hipLaunchKernelGGL((km_accum_kernel<T, CPL, V, K>), grid, dim3(kAccThreads), 0, s, \
+                     static_cast<const T *>(x), x_hs, ld, n, plan, assign, a_hs,      \
                      a_ss, slab, cslab, status)
-#define SCOPE_ACCUM_T(T)                       \
-  if (vec) {                                   \
-    if (check) SCOPE_ACCUM(T, true, true);     \
-    else SCOPE_ACCUM(T, true, false);          \
-  } else {                                     \
-    if (check) SCOPE_ACCUM(T, false, true);    \
-    else SCOPE_ACCUM(T, false, false);         \
+#define SCOPE_ACCUM_K(T, CPL, V)            \
+  if (check) SCOPE_ACCUM(T, CPL, V, true);  \
+  else SCOPE_ACCUM(T, CPL, V, false);
+#define SCOPE_ACCUM_T(T)                    \
+  if (v4) {                                 \
+    SCOPE_ACCUM_K(T, 4, true)               \
+  } else if (v2) {                          \
+    SCOPE_ACCUM_K(T, 2, true)               \
+  } else {                                  \
+    SCOPE_ACCUM_K(T, 2, false)              \
   }
   if (bf16) {
     SCOPE_ACCUM_T(uint16_t)
@@ -280,6 +317,7 @@ hipError_t km_accum(const AccPlan &plan, const void *x, bool bf16, size_t x_hs,
     SCOPE_ACCUM_T(float)
   }
 #undef SCOPE_ACCUM_T
+#undef SCOPE_ACCUM_K
 #undef SCOPE_ACCUM
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
