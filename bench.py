@@ -147,6 +147,98 @@ def cpu_baseline(cfg, x, layer_np):
     }
 
 
+def stage_bytes(cfg, sel_total):
+    """Algorithmic HBM bytes per stage of one layer: every input read once
+    per pass over it, every output written once (int32 indices, bf16 or fp32
+    rows).  sel_total = sum over heads and clusters of r_c."""
+    H, N, d, it = cfg.heads, cfg.n, cfg.d, cfg.iters
+    e = 2 if cfg.dtype == "bf16" else 4
+    rows = H * N * d * e
+    i32 = H * N * 4
+    return {
+        # per iteration: assignment reads Q and writes g; the update reads Q
+        # and g; the grouping of the last assignment reads g, writes perm
+        "cluster_queries": it * (2 * rows + 2 * i32) + 2 * i32,
+        # per iteration: three assignments read K's channel ranges (K once)
+        # and write three label arrays, the update reads K and the labels;
+        # the final assignment, then the packing into codes
+        "cluster_key_subspaces": it * (2 * rows + 6 * i32) + rows + 3 * i32 + 4 * i32,
+        # centroids in, tables out (a few MB)
+        "proxy_scores": H * (cfg.c_q * d + 3 * cfg.c_m * d // 3 + cfg.c_q * 3 * cfg.c_m) * 4,
+        # codes read once per head, the selected index lists written
+        "select": i32 + 4 * sel_total,
+    }
+
+
+def trace_summary(trace_csv, cmd, bench_line=None, config_name="hy720"):
+    """Per-kernel table of a rocprofv3 kernel trace with algorithmic bytes
+    (or flops) per call for the kernels of the workload's layer."""
+    import csv
+    import re
+    from paper_2608_12780_amd import inputs
+    cfg = inputs.CONFIGS[config_name]
+    H, N, d = cfg.heads, cfg.n, cfg.d
+    e = 2 if cfg.dtype == "bf16" else 4
+    dx_of = {128: d, 64: max(cfg.split[1], cfg.split[2]), 16: cfg.split[0]}
+    rows = []
+    for r in csv.DictReader(open(trace_csv)):
+        name = re.sub(r"scope::\(anonymous namespace\)::", "", r["Kernel_Name"])
+        name = re.sub(r"^void ", "", name).split("(")[0]
+        grid = (int(r["Grid_Size_X"]), int(r["Grid_Size_Y"]), int(r["Grid_Size_Z"]))
+        rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), name, grid))
+    rows.sort()
+    # the layer's own steps come first; the one-GPU-share layer (fewer
+    # heads), the dense mode and torch's SDPA follow.  The share run begins
+    # with the query initialisation over fewer heads.
+    share = max(1, math.ceil(H / 8))
+    cut = next((t0 for t0, _, nm, g in rows
+                if nm.startswith("km_init_kernel") and g[1] == share and share < H), None)
+
+    def table(sel):
+        agg = {}
+        for t0, t1, name, g in sel:
+            key = (name, f"{g[0]}x{g[1]}x{g[2]}")
+            a = agg.setdefault(key, [0, 0.0])
+            a[0] += 1
+            a[1] += (t1 - t0) / 1e3
+        return agg
+
+    def model(name, grid):
+        m = re.match(r"km_assign_mfma_kernel<(\d+)>", name)
+        if m:
+            dx = dx_of.get(int(m.group(1)))
+            return None if dx is None else ("B", H * N * (dx * e + 4))
+        if name.startswith("km_accum_kernel"):
+            gy = int(grid.split("x")[1])
+            nsub = 1 if gy > 1 else 3     # queries: two channel windows; keys: one
+            return ("B", H * N * (d * e + 4 * nsub))
+        return None
+
+    lines = [f"command: {cmd}", "",
+             "per (kernel, grid in work-items); durations from the kernel trace;",
+             "algorithmic bytes per call: rows read once (+ int32 labels) for the k-means",
+             f"assignment and update kernels of the {config_name} layer (8000 GB/s peak)"]
+    head = f"{'total ms':>10} {'calls':>6} {'avg us':>11} {'pct':>6} {'GB/s':>8} {'of peak':>8} {'grid':>20}  kernel"
+    parts = [("layer steps (warmup + timed)", [r for r in rows if cut is None or r[0] < cut], True),
+             (f"then: one GPU's share ({share} heads), the library's dense mode, torch SDPA",
+              [r for r in rows if cut is not None and r[0] >= cut], False)]
+    for title, sel, with_model in parts:
+        if not sel:
+            continue
+        agg = table(sel)
+        tot = sum(v[1] for v in agg.values())
+        lines += ["", title, head]
+        for (name, grid), (c, dsum) in sorted(agg.items(), key=lambda kv: -kv[1][1]):
+            avg = dsum / c
+            mdl = model(name, grid) if with_model else None
+            gbs = f"{mdl[1] / (avg * 1e-6) / 1e9:8.0f}" if mdl else f"{'':>8}"
+            frac = f"{mdl[1] / (avg * 1e-6) / 1e9 / HBM_PEAK_GBS:8.2f}" if mdl else f"{'':>8}"
+            lines.append(f"{dsum / 1e3:10.2f} {c:>6} {avg:11.1f} {100 * dsum / tot:6.2f} {gbs} {frac} {grid:>20}  {name}")
+    if bench_line:
+        lines += ["", "bench.py JSON line of the same run:", bench_line.strip()]
+    return "\n".join(lines) + "\n"
+
+
 def cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -263,6 +355,13 @@ def main():
     if len(sys.argv) >= 2 and sys.argv[1] == "--traffic-probe":
         traffic_probe()
         return
+    if len(sys.argv) >= 2 and sys.argv[1] == "--trace-summary":
+        # --trace-summary TRACE_CSV "COMMAND" [BENCH_LOG]
+        line = None
+        if len(sys.argv) > 4:
+            line = [l for l in open(sys.argv[4]).read().splitlines() if l.startswith("{")][-1]
+        sys.stdout.write(trace_summary(sys.argv[2], sys.argv[3], line))
+        return
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
@@ -336,6 +435,7 @@ def main():
     achieved = attn_flops / (attn_ms * 1e-3) / 1e12
     retained = pairs / (cfg.heads * float(cfg.n) * cfg.n)
     khead = layer.k_head.cpu().numpy()
+    sbytes = stage_bytes(cfg, float(selc.sum()))
     topp = layer.topp_counts.cpu().numpy().astype(np.float64)
     floor_bound = float((topp < cfg.k_fix).mean())
 
@@ -369,6 +469,9 @@ def main():
             "algorithmic_flops_per_launch": attn_flops,
         },
         "stages_ms": {k_: round(v_, 3) for k_, v_ in stage_ms.items()},
+        "hbm": {k_: {"bytes": b_, "gbs": round(b_ / (stage_ms[k_] * 1e-3) / 1e9, 1),
+                     "frac": round(b_ / (stage_ms[k_] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+                for k_, b_ in sbytes.items()},
         "wall_ms_per_step": round(wall_ms, 3),
         "retained_fraction": round(retained, 4),
         "k_head_mean": float(khead.mean()),
