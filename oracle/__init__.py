@@ -61,8 +61,8 @@ def lib():
         L.oracle_fixexp_batch.argtypes = [P, P, ctypes.c_long]
         L.oracle_mass_target.argtypes = [ctypes.c_float, ctypes.c_uint64]
         L.oracle_mass_target.restype = ctypes.c_uint64
-        L.oracle_select.argtypes = [I, I, I, P, P, ctypes.c_float, I, P, P, P, P,
-                                    P]
+        L.oracle_select.argtypes = [I, I, I, P, P, ctypes.c_float, I, I, P, P, P,
+                                    P, P]
         L.oracle_attention.argtypes = [I, I, I, P, P, P, I, P, P, P, P,
                                        ctypes.c_double, P, P]
         for name in ("oracle_kmeans", "oracle_group", "oracle_assign_rows",
@@ -219,8 +219,13 @@ def mass_target(rho: float, tot: int) -> int:
     return int(lib().oracle_mass_target(float(np.float32(rho)), int(tot)))
 
 
-def select(scores, counts, rho, k_fix):
-    """Alg. 3: base counts, k_head, r_c and key sets (ascending indices)."""
+POLICIES = {"online": 0, "fixed": 1, "topp": 2}
+
+
+def select(scores, counts, rho, k_fix, policy="online"):
+    """Alg. 3: base counts, k_head, r_c and key sets (ascending indices).
+    policy: "online" (Eq. 10), or the Fig. 6 ablations "fixed" (r_c = b_c,
+    no top-up) and "topp" (r_c = t_c)."""
     S = _c(scores, np.float32)
     heads, c_q, n = S.shape
     counts = _c(counts, np.int32).reshape(heads, c_q)
@@ -230,8 +235,8 @@ def select(scores, counts, rho, k_fix):
     idx = np.full((heads, c_q, n), -1, np.int32)
     topp = np.empty((heads, c_q), np.int32)
     _check(lib().oracle_select(heads, n, c_q, _p(S), _p(counts),
-                               float(np.float32(rho)), int(k_fix), _p(base),
-                               _p(kh), _p(sc), _p(idx), _p(topp)), "select")
+                               float(np.float32(rho)), int(k_fix), POLICIES[policy],
+                               _p(base), _p(kh), _p(sc), _p(idx), _p(topp)), "select")
     return dict(base_counts=base, k_head=kh, sel_counts=sc, sel_idx=idx,
                 topp=topp)
 

@@ -327,16 +327,21 @@ static int cmp_int(const void *pa, const void *pb) {
   return (a > b) - (a < b);
 }
 
+/* policy: 0 = online (Eq. 10, r_c = max(b_c, k_head)); 1 = fixed floor
+ * without top-up (r_c = b_c = max(t_c, k_fix)); 2 = pure Top-p (r_c = t_c).
+ * The last two are the selection-policy ablation of Fig. 6.                */
 int oracle_select(int heads, int n, int c_q, const float *scores,
-                  const int *counts, float rho, int k_fix, int *base,
+                  const int *counts, float rho, int k_fix, int policy, int *base,
                   int *k_head, int *sel_counts, int *sel_idx, int *topp) {
   if (!(rho > 0.0f && rho <= 1.0f) || k_fix < 1 || k_fix > n) return OR_ERR_ARG;
+  if (policy < 0 || policy > 2) return OR_ERR_ARG;
   for (int h = 0; h < heads; ++h) {
     const float *S = scores + (size_t)h * c_q * n;
     int *b = base + (size_t)h * c_q;
     /* Eq. 7-8 for every query cluster; the rankings are kept for Eq. 10. */
     keyed *order = (keyed *)malloc(sizeof(keyed) * (size_t)c_q * n);
-    if (!order) return OR_ERR_MEM;
+    int *tcs = (int *)malloc(sizeof(int) * (size_t)c_q);
+    if (!order || !tcs) { free(order); free(tcs); return OR_ERR_MEM; }
 #pragma omp parallel for schedule(dynamic, 1)
     for (int c = 0; c < c_q; ++c) {
       keyed *pi = order + (size_t)c * n;
@@ -358,6 +363,7 @@ int oracle_select(int heads, int n, int c_q, const float *scores,
           if (acc >= T) { t = l + 1; break; }
         }
       }
+      tcs[c] = t;
       if (topp) topp[(size_t)h * c_q + c] = t;
       b[c] = t > k_fix ? t : k_fix;                        /* Eq. 8 */
     }
@@ -367,14 +373,14 @@ int oracle_select(int heads, int n, int c_q, const float *scores,
       num += (uint64_t)counts[(size_t)h * c_q + c] * (uint64_t)b[c];
       den += (uint64_t)counts[(size_t)h * c_q + c];
     }
-    if (den == 0) { free(order); return OR_ERR_ARG; }
+    if (den == 0) { free(order); free(tcs); return OR_ERR_ARG; }
     int kh = (int)((num + den - 1) / den);
     k_head[h] = kh;
-    /* Eq. 10: r_c = max(b_c, k_head); S_c = first r_c keys of pi_c, emitted
-     * in ascending key index.                                               */
+    /* Eq. 10: r_c = max(b_c, k_head) (or the policy's count); S_c = first r_c
+     * keys of pi_c, emitted in ascending key index.                         */
 #pragma omp parallel for schedule(dynamic, 1)
     for (int c = 0; c < c_q; ++c) {
-      int r = b[c] > kh ? b[c] : kh;
+      int r = policy == 0 ? (b[c] > kh ? b[c] : kh) : policy == 1 ? b[c] : tcs[c];
       sel_counts[(size_t)h * c_q + c] = r;
       int *out = sel_idx + ((size_t)h * c_q + c) * n;
       keyed *pi = order + (size_t)c * n;
@@ -382,6 +388,7 @@ int oracle_select(int heads, int n, int c_q, const float *scores,
       qsort(out, (size_t)r, sizeof(int), cmp_int);
     }
     free(order);
+    free(tcs);
   }
   return OR_OK;
 }

@@ -274,9 +274,9 @@ def test_mass_target_is_exact_ceiling(oracle_lib):
 # --------------------------------------------------------------------------
 # selection (Eq. 7-10, Alg. 3)
 
-def _referee_select(S, counts, rho, k_fix):
+def _referee_select(S, counts, rho, k_fix, policy="online"):
     """Alg. 3 by the definition, in exact rationals over the oracle's
-    integer softmax masses."""
+    integer softmax masses (policy: Eq. 10, or the Fig. 6 ablations)."""
     cq, n = S.shape
     t, b = [], []
     ranks = []
@@ -300,7 +300,7 @@ def _referee_select(S, counts, rho, k_fix):
         b.append(max(tc, k_fix))
     kh = math.ceil(Fraction(sum(int(counts[c]) * b[c] for c in range(cq)),
                             int(sum(counts))))
-    r = [max(bc, kh) for bc in b]
+    r = {"online": [max(bc, kh) for bc in b], "fixed": list(b), "topp": list(t)}[policy]
     sets = [sorted(ranks[c][:r[c]]) for c in range(cq)]
     return t, b, kh, r, sets
 
@@ -333,8 +333,9 @@ def test_select_brute_force_small(oracle_lib, seed):
     counts = np.bincount(g, minlength=cq).astype(np.int32)
     rho = float(np.float32(rng.choice([0.3, 0.5, 0.9, 0.95, 1.0, rng.uniform()])))
     k_fix = int(rng.integers(1, n + 1))
-    r = oracle.select(S[None], counts[None], rho, k_fix)
-    t, b, kh, rr, sets = _referee_select(S, counts, rho, k_fix)
+    policy = ("online", "fixed", "topp")[seed % 3]
+    r = oracle.select(S[None], counts[None], rho, k_fix, policy)
+    t, b, kh, rr, sets = _referee_select(S, counts, rho, k_fix, policy)
     assert r["topp"][0].tolist() == t
     assert r["base_counts"][0].tolist() == b
     assert int(r["k_head"][0]) == kh
@@ -343,6 +344,25 @@ def test_select_brute_force_small(oracle_lib, seed):
         assert r["sel_idx"][0, c, :rr[c]].tolist() == sets[c]
     # Eq. 9 closed form as a per-query average of b_{g_i}
     assert kh == math.ceil(Fraction(sum(b[gi] for gi in g), n))
+
+
+def test_select_policies_nest(oracle_lib):
+    """Top-p sets are contained in the fixed-floor sets, which are contained
+    in the online sets; each is a prefix of the same ranking."""
+    rng = np.random.default_rng(7)
+    n, cq = 300, 5
+    S = rng.normal(0, 2, size=(1, cq, n)).astype(np.float32)
+    counts = rng.integers(1, 50, size=(1, cq)).astype(np.int32)
+    out = {p: oracle.select(S, counts, 0.8, 40, p) for p in ("topp", "fixed", "online")}
+    t, b = out["online"]["topp"][0], out["online"]["base_counts"][0]
+    kh = int(out["online"]["k_head"][0])
+    assert out["topp"]["sel_counts"][0].tolist() == t.tolist()
+    assert out["fixed"]["sel_counts"][0].tolist() == b.tolist()
+    assert out["online"]["sel_counts"][0].tolist() == np.maximum(b, kh).tolist()
+    for c in range(cq):
+        sets = [set(out[p]["sel_idx"][0, c, :out[p]["sel_counts"][0, c]].tolist())
+                for p in ("topp", "fixed", "online")]
+        assert sets[0] <= sets[1] <= sets[2]
 
 
 def test_select_invariants_and_float64_softmax(oracle_lib):
