@@ -239,6 +239,66 @@ def trace_summary(trace_csv, cmd, bench_line=None, config_name="hy720"):
     return "\n".join(lines) + "\n"
 
 
+def policy_study(config_name="hy720", heads=4):
+    """The selection-policy ablation (Fig. 6) on synthetic inputs: the online
+    policy at the workload's rho sets a realised density (fraction of query-
+    key pairs kept); rho of the fixed-floor and pure Top-p policies is
+    bisected to the same density; each policy's attention output is then
+    compared with dense attention on the same heads."""
+    import torch
+    from paper_2608_12780_amd import inputs
+    from paper_2608_12780_amd.layer import DenseAttention, ScopeLayer
+    cfg = inputs.CONFIGS[config_name]
+    x = inputs.generate(cfg.with_(heads=heads))
+    dev = torch.device("cuda", 0)
+    up = lambda b: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
+    q, k, v = up(x.q_bits), up(x.k_bits), up(x.v_bits)
+    L = ScopeLayer(heads, cfg.n, cfg.d, cfg.ranges, cfg.c_q, (cfg.c_m,) * 3, cfg.iters,
+                   cfg.rho, cfg.k_fix, dtype=cfg.dtype, device=dev)
+    L.cluster_queries(q, torch.from_numpy(x.init_q).to(dev))
+    L.cluster_keys(k, torch.from_numpy(x.init_k).to(dev))
+    L.proxy_scores()
+    dense = DenseAttention(heads, cfg.n, cfg.d, cfg.dtype, dev)
+    ref = dense.forward(q, k, v).float()
+    torch.cuda.synchronize()
+    counts = L.counts.double()
+
+    def density(policy, rho):
+        L.select(policy=policy, rho=rho)
+        return float((counts * L.sel_counts.double()).sum()) / (heads * float(cfg.n) ** 2)
+
+    target = density("online", cfg.rho)
+    rows = []
+    for policy in ("online", "fixed", "topp"):
+        if policy == "online":
+            rho = cfg.rho
+        else:
+            lo, hi = 1e-4, 1.0
+            for _ in range(24):
+                mid = 0.5 * (lo + hi)
+                if density(policy, mid) < target:
+                    lo = mid
+                else:
+                    hi = mid
+            rho = hi
+        dens = density(policy, rho)
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        L.attend(q, k, v)
+        e.record()
+        e.synchronize()
+        out = L.out.float()
+        err = out - ref
+        rows.append({"policy": policy, "rho": round(rho, 6), "density": round(dens, 5),
+                     "rel_l2_vs_dense": float(err.norm() / ref.norm()),
+                     "max_abs_vs_dense": float(err.abs().max()),
+                     "attention_ms": round(s.elapsed_time(e), 3),
+                     "k_head_mean": float(L.k_head.double().mean())})
+        log(f"[policy] {rows[-1]}")
+    return {"study": "selection policy at matched density", "workload": WORKLOAD_NAMES.get(cfg.name),
+            "heads": heads, "n": cfg.n, "target_density": round(target, 5), "rows": rows}
+
+
 def cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -354,6 +414,9 @@ def main():
         return
     if len(sys.argv) >= 2 and sys.argv[1] == "--traffic-probe":
         traffic_probe()
+        return
+    if len(sys.argv) >= 2 and sys.argv[1] == "--policy-study":
+        print(json.dumps(policy_study()), flush=True)
         return
     if len(sys.argv) >= 2 and sys.argv[1] == "--trace-summary":
         # --trace-summary TRACE_CSV "COMMAND" [BENCH_LOG]

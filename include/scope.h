@@ -63,6 +63,14 @@ typedef enum {
 
 typedef enum { SCOPE_F32 = 0, SCOPE_BF16 = 1 } scope_dtype;
 
+/* Selection policies (call 4b): the online per-head Top-k of Eq. 9-10, and
+ * the two variants it is compared with in Fig. 6. */
+typedef enum {
+  SCOPE_POLICY_ONLINE = 0, /* r_c = max(b_c, k_head)              (Eq. 10) */
+  SCOPE_POLICY_FIXED = 1,  /* r_c = b_c = max(t_c, k_fix), no top-up      */
+  SCOPE_POLICY_TOPP = 2    /* r_c = t_c, pure Top-p                       */
+} scope_policy;
+
 /* Problem shape.  The three RoPE channel ranges I_T, I_H, I_W (Sec. 3.3;
  * App. A: disjoint, covering all d channels) are given as (offset, length)
  * in T, H, W order.  Supported: 1 <= heads <= 65535, 1 <= n <= 2^24, 2 <= d <= 128
@@ -160,6 +168,20 @@ int32_t scope_select(const scope_shape *shape, int32_t c_q,
                      int32_t *base_counts, int32_t *topp_counts,
                      int32_t *k_head, int32_t *sel_counts, int32_t *sel_idx,
                      void *workspace, size_t ws_bytes, void *stream);
+
+/* 4b. Selection under a named policy (the ablation of Fig. 6).  Arguments,
+ * layouts, outputs and errors as call 4, plus `policy` (a scope_policy):
+ * ONLINE is call 4; FIXED keeps b_c keys per cluster (Eq. 8) and TOPP the
+ * t_c keys of Eq. 7, with no top-up to k_head.  k_head (Eq. 9) is written
+ * for every policy.  An unknown policy is SCOPE_ERR_INVALID_ARGUMENT.     */
+int32_t scope_select_policy(const scope_shape *shape, int32_t c_q,
+                            const int32_t c_m[3], const float *scores,
+                            const float *tables, const uint32_t *codes,
+                            const int32_t *counts, float rho, int32_t k_fix,
+                            int32_t *base_counts, int32_t *topp_counts,
+                            int32_t *k_head, int32_t *sel_counts,
+                            int32_t *sel_idx, void *workspace, size_t ws_bytes,
+                            int32_t policy, void *stream);
 
 /* 5. Sparse attention over the selected keys (Eq. 11; Alg. 1 last step).
  * For every cluster c and every query i in perm[offsets[c] .. offsets[c+1]):

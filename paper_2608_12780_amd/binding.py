@@ -21,9 +21,10 @@ F32, BF16 = 0, 1
 ENTRY_POINTS = (
     "scope_abi_version", "scope_status_string", "scope_workspace_size",
     "scope_cluster_queries", "scope_cluster_key_subspaces",
-    "scope_proxy_scores", "scope_select", "scope_sparse_attention",
-    "scope_debug_fixexp",
+    "scope_proxy_scores", "scope_select", "scope_select_policy",
+    "scope_sparse_attention", "scope_debug_fixexp",
 )
+POLICIES = {"online": 0, "fixed": 1, "topp": 2}
 
 
 class ScopeError(RuntimeError):
@@ -69,6 +70,8 @@ def lib() -> ctypes.CDLL:
         L.scope_proxy_scores.argtypes = [SP, P, I, P, P, P, P, P, P]
         L.scope_select.argtypes = [SP, I, P, P, P, P, P, ctypes.c_float, I, P, P,
                                    P, P, P, P, Z, P]
+        L.scope_select_policy.argtypes = [SP, I, P, P, P, P, P, ctypes.c_float, I, P,
+                                          P, P, P, P, P, Z, I, P]
         L.scope_sparse_attention.argtypes = [SP, P, P, P, I, P, P, P, P,
                                              ctypes.c_float, P, P, Z, P]
         L.scope_debug_fixexp.argtypes = [P, P, ctypes.c_int64, P]
@@ -184,9 +187,19 @@ def scope_proxy_scores(shape, q_centroids, c_q, k_centroids, c_m, codes,
 def scope_select(shape, c_q, c_m, scores, tables, codes, counts, rho, k_fix,
                  base_counts, topp_counts, k_head, sel_counts, sel_idx,
                  workspace, stream=None):
+    scope_select_policy(shape, c_q, c_m, scores, tables, codes, counts, rho, k_fix,
+                        base_counts, topp_counts, k_head, sel_counts, sel_idx,
+                        workspace, "online", stream, name="scope_select")
+
+
+def scope_select_policy(shape, c_q, c_m, scores, tables, codes, counts, rho, k_fix,
+                        base_counts, topp_counts, k_head, sel_counts, sel_idx,
+                        workspace, policy="online", stream=None, name="scope_select_policy"):
     H, N = shape.heads, shape.n
     cs = int(sum(c_m))
-    _check("scope_select", lib().scope_select(
+    fn = lib().scope_select if name == "scope_select" else lib().scope_select_policy
+    extra = () if name == "scope_select" else (POLICIES[policy],)
+    _check(name, fn(
         ctypes.byref(shape), int(c_q), _cm(c_m),
         _ptr(scores, torch.float32, H * c_q * N, "scores", optional=True),
         _ptr(tables, torch.float32, H * c_q * cs, "tables", optional=True),
@@ -198,7 +211,7 @@ def scope_select(shape, c_q, c_m, scores, tables, codes, counts, rho, k_fix,
         _ptr(sel_counts, torch.int32, H * c_q, "sel_counts"),
         _ptr(sel_idx, torch.int32, H * c_q * N, "sel_idx"),
         _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(),
-        _stream(stream)))
+        *extra, _stream(stream)))
 
 
 def scope_sparse_attention(shape, q, k, v, c_q, offsets, perm, sel_counts,

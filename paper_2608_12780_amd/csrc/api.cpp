@@ -359,14 +359,18 @@ int32_t scope_proxy_scores(const scope_shape *shape, const float *q_centroids,
   return SCOPE_OK;
 }
 
-int32_t scope_select(const scope_shape *shape, int32_t c_q,
-                     const int32_t c_m[3], const float *scores,
-                     const float *tables, const uint32_t *codes,
-                     const int32_t *counts, float rho, int32_t k_fix,
-                     int32_t *base_counts, int32_t *topp_counts,
-                     int32_t *k_head, int32_t *sel_counts, int32_t *sel_idx,
-                     void *workspace, size_t ws_bytes, void *stream) {
+int32_t scope_select_policy(const scope_shape *shape, int32_t c_q,
+                            const int32_t c_m[3], const float *scores,
+                            const float *tables, const uint32_t *codes,
+                            const int32_t *counts, float rho, int32_t k_fix,
+                            int32_t *base_counts, int32_t *topp_counts,
+                            int32_t *k_head, int32_t *sel_counts,
+                            int32_t *sel_idx, void *workspace, size_t ws_bytes,
+                            int32_t policy, void *stream) {
   int32_t st = check_shape(shape);
+  if (policy != SCOPE_POLICY_ONLINE && policy != SCOPE_POLICY_FIXED &&
+      policy != SCOPE_POLICY_TOPP)
+    return SCOPE_ERR_INVALID_ARGUMENT;
   if (st) return st;
   if ((st = check_cq(shape, c_q))) return st;
   if ((st = check_cm(shape, c_m))) return st;
@@ -382,9 +386,22 @@ int32_t scope_select(const scope_shape *shape, int32_t c_q,
   SCOPE_TRY(scope::select_run(shape->heads, shape->n, c_q, c_m, shape->d,
                               scores, tables, codes, counts, rho, k_fix,
                               base_counts, topp_counts, k_head, sel_counts,
-                              sel_idx, w.row_max, w.row_state, w.coarse_hist,
+                              sel_idx, w.row_max, w.row_state, w.coarse_hist, policy,
                               static_cast<hipStream_t>(stream)));
   return SCOPE_OK;
+}
+
+int32_t scope_select(const scope_shape *shape, int32_t c_q,
+                     const int32_t c_m[3], const float *scores,
+                     const float *tables, const uint32_t *codes,
+                     const int32_t *counts, float rho, int32_t k_fix,
+                     int32_t *base_counts, int32_t *topp_counts,
+                     int32_t *k_head, int32_t *sel_counts, int32_t *sel_idx,
+                     void *workspace, size_t ws_bytes, void *stream) {
+  return scope_select_policy(shape, c_q, c_m, scores, tables, codes, counts, rho,
+                             k_fix, base_counts, topp_counts, k_head, sel_counts,
+                             sel_idx, workspace, ws_bytes, SCOPE_POLICY_ONLINE,
+                             stream);
 }
 
 int32_t scope_sparse_attention(const scope_shape *shape, const void *q,

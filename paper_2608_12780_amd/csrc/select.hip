@@ -14,7 +14,8 @@
 //   b = max(t, k_fix) (Eq. 8).  The coarse count histogram is kept for the
 //   final kernel.
 // head kernel: k_head = ceil(sum n_c b_c / sum n_c) in integers (Eq. 9),
-//   r_c = max(b_c, k_head) (Eq. 10).
+//   r_c = max(b_c, k_head) (Eq. 10), or for the Fig. 6 variants r_c = b_c
+//   (fixed floor) or r_c = t_c (pure Top-p).
 // final kernel: the rank-r_c logit by the same radix selection on counts
 //   (reused from the base kernel when r_c == t_c; otherwise from the kept
 //   coarse histogram, one gathering pass and the digit rounds), then an
@@ -316,7 +317,8 @@ __global__ __launch_bounds__(kSelBlock) void select_base_kernel(
 
 __global__ __launch_bounds__(kSelBlock) void select_head_kernel(
     int c_q, const int32_t *__restrict__ counts, const int32_t *__restrict__ base,
-    int32_t *k_head, int32_t *sel_counts) {
+    const uint32_t *__restrict__ row_state, int policy, int32_t *k_head,
+    int32_t *sel_counts) {
   const int h = blockIdx.x;
   uint64_t num = 0, den = 0;
   for (int c = threadIdx.x; c < c_q; c += kSelBlock) {
@@ -328,9 +330,12 @@ __global__ __launch_bounds__(kSelBlock) void select_head_kernel(
   den = block_sum<uint64_t>(den);
   const int kh = den ? static_cast<int>((num + den - 1) / den) : 0;
   if (threadIdx.x == 0) k_head[h] = kh;
+  // r_c per policy: online (Eq. 10), fixed floor (Eq. 8), pure Top-p (Eq. 7)
   for (int c = threadIdx.x; c < c_q; c += kSelBlock) {
-    const int b = base[static_cast<size_t>(h) * c_q + c];
-    sel_counts[static_cast<size_t>(h) * c_q + c] = b > kh ? b : kh;
+    const size_t row = static_cast<size_t>(h) * c_q + c;
+    const int b = base[row];
+    const int t = static_cast<int>(row_state[4 * row + 0]);
+    sel_counts[row] = policy == 0 ? (b > kh ? b : kh) : policy == 1 ? b : t;
   }
 }
 
@@ -419,7 +424,8 @@ hipError_t select_run(int heads, int n, int c_q, const int *c_m, int d,
                       const uint32_t *codes, const int32_t *counts, float rho,
                       int k_fix, int32_t *base, int32_t *topp, int32_t *k_head,
                       int32_t *sel_counts, int32_t *sel_idx, float *row_max,
-                      uint32_t *row_state, uint32_t *coarse_hist, hipStream_t s) {
+                      uint32_t *row_state, uint32_t *coarse_hist, int policy,
+                      hipStream_t s) {
   Cm3 cm{{c_m[0], c_m[1], c_m[2]}};
   const float sigma = static_cast<float>(1.0 / sqrt(static_cast<double>(d)));
   const dim3 grid(c_q, heads), block(kSelBlock);
@@ -434,7 +440,7 @@ hipError_t select_run(int heads, int n, int c_q, const int *c_m, int d,
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(select_head_kernel, dim3(heads), block, 0, s, c_q, counts,
-                     base, k_head, sel_counts);
+                     base, row_state, policy, k_head, sel_counts);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (scores)

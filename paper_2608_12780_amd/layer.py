@@ -65,12 +65,19 @@ class ScopeLayer:
                              self.k_centroids, self.c_m, self.codes,
                              self.tables, self.scores, stream)
 
-    def select(self, stream=None, use_scores=False):
-        B.scope_select(self.shape, self.c_q, self.c_m,
-                       self.scores if use_scores else None, self.tables,
-                       self.codes, self.counts, self.rho, self.k_fix,
-                       self.base_counts, self.topp_counts, self.k_head,
-                       self.sel_counts, self.sel_idx, self.workspace, stream)
+    def select(self, stream=None, use_scores=False, policy="online", rho=None):
+        """policy "online" is call 4 (Eq. 10); "fixed" and "topp" are the
+        Fig. 6 variants through call 4b.  rho overrides the layer's."""
+        rho = self.rho if rho is None else rho
+        args = (self.shape, self.c_q, self.c_m,
+                self.scores if use_scores else None, self.tables,
+                self.codes, self.counts, rho, self.k_fix,
+                self.base_counts, self.topp_counts, self.k_head,
+                self.sel_counts, self.sel_idx, self.workspace)
+        if policy == "online":
+            B.scope_select(*args, stream)
+        else:
+            B.scope_select_policy(*args, policy, stream)
 
     def attend(self, q, k, v, scale=0.0, stream=None):
         B.scope_sparse_attention(self.shape, q, k, v, self.c_q, self.offsets,

@@ -45,14 +45,14 @@ def make_layer(cfg: inputs.LayerConfig, heads=None, materialize=True, **over):
     return ScopeLayer(**a)
 
 
-def run_gpu(layer: ScopeLayer, x: inputs.LayerInputs, use_scores=False):
+def run_gpu(layer: ScopeLayer, x: inputs.LayerInputs, use_scores=False, policy="online"):
     q, k, v = to_device(x)
     iq = torch.from_numpy(x.init_q).cuda()
     ik = torch.from_numpy(x.init_k).cuda()
     layer.cluster_queries(q, iq)
     layer.cluster_keys(k, ik)
     layer.proxy_scores()
-    layer.select(use_scores=use_scores)
+    layer.select(use_scores=use_scores, policy=policy)
     layer.attend(q, k, v)
     torch.cuda.synchronize()
     g = lambda t: None if t is None else t.cpu().numpy()
@@ -66,9 +66,9 @@ def run_gpu(layer: ScopeLayer, x: inputs.LayerInputs, use_scores=False):
                 out=layer.out.float().cpu().numpy(), status=int(layer.status.item()))
 
 
-def oracle_all(x: inputs.LayerInputs, c_q, c_m, iters, rho, k_fix):
+def oracle_all(x: inputs.LayerInputs, c_q, c_m, iters, rho, k_fix, policy="online"):
     return oracle.layer(x.q, x.k, x.v, x.cfg.ranges, c_q, c_m, iters, x.init_q,
-                        x.init_k, rho, k_fix)
+                        x.init_k, rho, k_fix, policy)
 
 
 def assert_same_selection(gpu, ref_sel):

@@ -116,6 +116,13 @@ def test_select_validation():
     assert call(k_fix=118801) == INVALID
     assert call(tables=None) == INVALID            # neither scores nor tables
     assert call(codes=None) == INVALID
+    # the policy variant rejects unknown policies before anything else
+    sh = hy_shape()
+    cm = (ctypes.c_int32 * 3)(128, 128, 128)
+    for bad in (-1, 3, 99):
+        assert L.scope_select_policy(ctypes.byref(sh), 256, cm, FAKE, FAKE, FAKE, FAKE,
+                                     ctypes.c_float(0.9), 100, FAKE, None, FAKE, FAKE,
+                                     FAKE, FAKE, 1 << 40, bad, None) == INVALID
 
 
 def test_attention_validation():

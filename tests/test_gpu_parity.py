@@ -42,13 +42,13 @@ def _gpu():
     oracle.lib()
 
 
-def check_layer(cfg, use_scores=False):
+def check_layer(cfg, use_scores=False, policy="online"):
     G.say(f"[parity] {cfg.name}: heads={cfg.heads} n={cfg.n} d={cfg.d} "
           f"split={cfg.split} c_q={cfg.c_q} c_m={cfg.c_m} iters={cfg.iters}")
     x = inputs.generate(cfg)
     layer = G.make_layer(cfg)
-    gpu = G.run_gpu(layer, x, use_scores=use_scores)
-    ref = G.oracle_all(x, cfg.c_q, (cfg.c_m,) * 3, cfg.iters, cfg.rho, cfg.k_fix)
+    gpu = G.run_gpu(layer, x, use_scores=use_scores, policy=policy)
+    ref = G.oracle_all(x, cfg.c_q, (cfg.c_m,) * 3, cfg.iters, cfg.rho, cfg.k_fix, policy)
     assert gpu["status"] == 0
     # query clustering (Eq. 2)
     assert np.array_equal(gpu["assign"], ref["q"]["assign"])
@@ -112,6 +112,14 @@ def test_paper_operating_point_cluster_counts():
 
 def test_mid_layer_d64_bf16():
     check_layer(MID_D64)
+
+
+@pytest.mark.parametrize("policy", ["fixed", "topp"])
+def test_selection_policies_of_the_ablation(policy):
+    # the Fig. 6 variants: fixed floor without top-up, pure Top-p
+    gpu, ref = check_layer(MID_HY.with_(name=f"mid_{policy}"), policy=policy)
+    want = ref["sel"]["base_counts"] if policy == "fixed" else ref["sel"]["topp"]
+    assert np.array_equal(gpu["sel_counts"], want)
 
 
 @pytest.mark.parametrize("rho", [0.5, 0.95])
