@@ -272,14 +272,15 @@ def dense_attention(q, k, v, scale=None, row_mask=None):
     return attention(q, k, v, offsets, perm, sc, idx, scale, row_mask)
 
 
-def layer(q, k, v, ranges, c_q, c_m, iters, init_q, init_k, rho, k_fix):
+def layer(q, k, v, ranges, c_q, c_m, iters, init_q, init_k, rho, k_fix,
+          policy="online"):
     """The whole layer of Alg. 1 for every head; returns every intermediate."""
     d = np.shape(q)[2]
     qr = cluster_queries(q, c_q, iters, init_q)
     kr = cluster_key_subspaces(k, ranges, c_m, iters, init_k)
     P = tables(qr["centroids"], kr["centroids"], ranges, c_m)
     S = proxy_scores(P, kr["codes"], d, c_m)
-    sel = select(S, qr["counts"], rho, k_fix)
+    sel = select(S, qr["counts"], rho, k_fix, policy)
     O = attention(q, k, v, qr["offsets"], qr["perm"], sel["sel_counts"],
                   sel["sel_idx"])
     return dict(q=qr, k=kr, tables=P, scores=S, sel=sel, out=O)
