@@ -53,6 +53,10 @@ def lib():
         L.oracle_cluster_key_subspaces.argtypes = [I, I, I, P, P, P, P, I, P, I,
                                                    P, P, P]
         L.oracle_tables.argtypes = [I, I, P, P, I, P, P, P, P]
+        L.oracle_cluster_key_partition.argtypes = [I, I, I, I, P, P, P, P, I, P, I,
+                                                   P, P, P]
+        L.oracle_tables_partition.argtypes = [I, I, I, P, P, I, P, P, P, P]
+        L.oracle_proxy_scores_partition.argtypes = [I, I, I, I, I, P, P, P, P]
         L.oracle_proxy_scores.argtypes = [I, I, I, I, P, P, P, P]
         L.oracle_sigma.argtypes = [I]
         L.oracle_sigma.restype = ctypes.c_float
@@ -68,7 +72,9 @@ def lib():
         for name in ("oracle_kmeans", "oracle_group", "oracle_assign_rows",
                      "oracle_mean_rows", "oracle_cluster_queries",
                      "oracle_cluster_key_subspaces", "oracle_tables",
-                     "oracle_proxy_scores", "oracle_select", "oracle_attention"):
+                     "oracle_proxy_scores", "oracle_select", "oracle_attention",
+                     "oracle_cluster_key_partition", "oracle_tables_partition",
+                     "oracle_proxy_scores_partition"):
             getattr(L, name).restype = I
         _lib = L
     return _lib
@@ -168,6 +174,8 @@ def cluster_key_subspaces(k, ranges, c_m, iters, init):
     cm = _c(c_m, np.int32)
     init = _c(init, np.int32)
     stride = init.shape[-1]
+    if init.shape != (heads, 3, stride) or stride < int(cm.max()):
+        raise ValueError("init must be [heads][3][stride >= max c_m]")
     per_head = int(sum(int(cm[m]) * int(ln[m]) for m in range(3)))
     cen = np.empty((heads, per_head), np.float32)
     codes = np.empty((heads, n), np.uint32)
@@ -201,6 +209,63 @@ def proxy_scores(tables_, codes, d, c_m):
     S = np.empty((heads, c_q, n), np.float32)
     lib().oracle_proxy_scores(heads, n, d, c_q, _p(_c(c_m, np.int32)), _p(P),
                               _p(codes), _p(S))
+    return S
+
+
+def _partition(sets):
+    """Channel sets I_1..I_M -> (M, concatenated channels, lengths)."""
+    sets = [np.asarray(x, np.int32).ravel() for x in sets]
+    return (len(sets), _c(np.concatenate(sets), np.int32),
+            _c([x.size for x in sets], np.int32))
+
+
+def cluster_key_partition(k, sets, c_m, iters, init):
+    """App. B / Table 3: k-means of K[:, I_m] for any disjoint channel sets
+    I_1..I_M (each ascending, together all d channels).  Codes per subspace,
+    [heads][M][n] uint16; centroids per head U^1..U^M back to back.
+    init: [heads][M][stride]."""
+    k = _c(k, np.float32)
+    heads, n, d = k.shape
+    M, chan, ln = _partition(sets)
+    cm = _c(c_m, np.int32)
+    init = _c(init, np.int32)
+    stride = init.shape[-1]
+    if init.shape != (heads, M, stride) or stride < int(cm.max()):
+        raise ValueError("init must be [heads][M][stride >= max c_m]")
+    per_head = int(sum(int(cm[m]) * int(ln[m]) for m in range(M)))
+    cen = np.empty((heads, per_head), np.float32)
+    codes = np.empty((heads, M, n), np.uint16)
+    a = np.empty((heads, M, n), np.int32)
+    st = lib().oracle_cluster_key_partition(heads, n, d, M, _p(chan), _p(ln), _p(k),
+                                            _p(cm), iters, _p(init), stride,
+                                            _p(cen), _p(codes), _p(a))
+    _check(st, "cluster_key_partition")
+    return dict(centroids=cen, codes=codes, assign=a, status=st)
+
+
+def tables_partition(q_centroids, k_centroids, sets, c_m):
+    """Eq. 5 over M subspaces: [heads][c_q][C_1 + ... + C_M]."""
+    qc = _c(q_centroids, np.float32)
+    kc = _c(k_centroids, np.float32)
+    heads, c_q, d = qc.shape
+    M, chan, ln = _partition(sets)
+    cm = _c(c_m, np.int32)
+    P = np.empty((heads, c_q, int(cm.sum())), np.float32)
+    _check(lib().oracle_tables_partition(heads, d, M, _p(chan), _p(ln), c_q, _p(cm),
+                                         _p(qc), _p(kc), _p(P)), "tables_partition")
+    return P
+
+
+def proxy_scores_partition(tables_, codes, d, c_m):
+    """Eq. 6 over M subspaces, codes [heads][M][n]: [heads][c_q][n]."""
+    P = _c(tables_, np.float32)
+    codes = _c(codes, np.uint16)
+    heads, M, n = codes.shape
+    c_q = P.shape[1]
+    S = np.empty((heads, c_q, n), np.float32)
+    _check(lib().oracle_proxy_scores_partition(heads, n, d, M, c_q,
+                                               _p(_c(c_m, np.int32)), _p(P),
+                                               _p(codes), _p(S)), "proxy_scores_partition")
     return S
 
 
@@ -270,6 +335,20 @@ def dense_attention(q, k, v, scale=None, row_mask=None):
     sc = np.full((heads, 1), n, np.int32)
     idx = np.tile(np.arange(n, dtype=np.int32), (heads, 1, 1))
     return attention(q, k, v, offsets, perm, sc, idx, scale, row_mask)
+
+
+def layer_partition(q, k, v, sets, c_q, c_m, iters, init_q, init_k, rho, k_fix,
+                    policy="online"):
+    """The layer with the keys split into the channel sets I_1..I_M."""
+    d = np.shape(q)[2]
+    qr = cluster_queries(q, c_q, iters, init_q)
+    kr = cluster_key_partition(k, sets, c_m, iters, init_k)
+    P = tables_partition(qr["centroids"], kr["centroids"], sets, c_m)
+    S = proxy_scores_partition(P, kr["codes"], d, c_m)
+    sel = select(S, qr["counts"], rho, k_fix, policy)
+    O = attention(q, k, v, qr["offsets"], qr["perm"], sel["sel_counts"],
+                  sel["sel_idx"])
+    return dict(q=qr, k=kr, tables=P, scores=S, sel=sel, out=O)
 
 
 def layer(q, k, v, ranges, c_q, c_m, iters, init_q, init_k, rho, k_fix,

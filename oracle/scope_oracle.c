@@ -15,6 +15,8 @@
  *   5. softmax + Top-p count, fixed floor, online per-head k,
  *      top-up and final key sets                                 (Eq. 7-10, Alg. 3)
  *   6. exact attention of each query cluster over its key set    (Eq. 11; Eq. 1)
+ *   7. general M-way key partitions (any disjoint channel sets,
+ *      M <= 8) for the partition ablation                       (App. B; Table 3)
  *
  * Arithmetic.  The method is stated over the reals.  Steps 1-5 decide
  * integers (assignments, counts, index sets), so both this oracle and the GPU
@@ -267,6 +269,135 @@ int oracle_proxy_scores(int heads, int n, int d, int c_q, const int *c_m,
       float *S = scores + ((size_t)h * c_q + c) * n;
       for (int j = 0; j < n; ++j)
         S[j] = proxy_logit(P, c_m, codes[(size_t)h * n + j], sigma);
+    }
+  return OR_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* General M-way key partitions (App. B; the partition ablation of Table 3).
+ * The d channels are split into M disjoint sets I_1 .. I_M that cover all of
+ * them; chan lists I_1, then I_2, ... (d entries), each set in ascending
+ * channel order, and len[m] = d_m = |I_m|.  Subspace m is the key matrix
+ * restricted to I_m, K^m = K[:, I_m], clustered exactly like a T/H/W
+ * subspace above (Eq. 3).  Codes stay per subspace: z[h][m][j] (Eq. 4 with
+ * M entries).  Centroids per head: U^1 .. U^M back to back, each
+ * [C_m][d_m], column k of U^m belonging to channel I_m[k].  With the three
+ * RoPE ranges as the sets, everything equals the T/H/W functions above.   */
+#define OR_MAX_SUB 8
+
+static int check_partition(int n, int d, int M, const int *chan,
+                           const int *len, const int *c_m) {
+  if (M < 1 || M > OR_MAX_SUB || d < 1) return OR_ERR_ARG;
+  unsigned char seen[1024];
+  if (d > 1024) return OR_ERR_ARG;
+  memset(seen, 0, sizeof seen);
+  int o = 0;
+  for (int m = 0; m < M; ++m) {
+    if (len[m] < 1 || o + len[m] > d) return OR_ERR_ARG;
+    if (c_m && (c_m[m] < 1 || c_m[m] > 1024 || c_m[m] > n)) return OR_ERR_ARG;
+    for (int k = 0; k < len[m]; ++k) {
+      int ch = chan[o + k];
+      if (ch < 0 || ch >= d || seen[ch]) return OR_ERR_ARG;
+      if (k > 0 && ch <= chan[o + k - 1]) return OR_ERR_ARG;
+      seen[ch] = 1;
+    }
+    o += len[m];
+  }
+  return o == d ? OR_OK : OR_ERR_ARG;
+}
+
+int oracle_cluster_key_partition(int heads, int n, int d, int M,
+                                 const int *chan, const int *len,
+                                 const float *k, const int *c_m, int iters,
+                                 const int *init, int init_stride,
+                                 float *centroids, uint16_t *codes,
+                                 int *assign) {
+  if (check_partition(n, d, M, chan, len, c_m) != OR_OK) return OR_ERR_ARG;
+  int per_head = 0;
+  for (int m = 0; m < M; ++m) per_head += c_m[m] * len[m];
+  int status = OR_OK;
+  int *cnt = (int *)malloc(sizeof(int) * 1024);
+  float *X = (float *)malloc(sizeof(float) * (size_t)n * d);
+  if (!cnt || !X) { free(cnt); free(X); return OR_ERR_MEM; }
+  for (int h = 0; h < heads; ++h) {
+    const float *Kh = k + (size_t)h * n * d;
+    float *U = centroids + (size_t)h * per_head;
+    int o = 0;
+    for (int m = 0; m < M; ++m) {
+      /* K^m = K[:, I_m] as a dense [n][d_m] matrix */
+      for (int j = 0; j < n; ++j)
+        for (int kk = 0; kk < len[m]; ++kk)
+          X[(size_t)j * len[m] + kk] = Kh[(size_t)j * d + chan[o + kk]];
+      int *a = assign + ((size_t)h * M + m) * n;
+      int s = oracle_kmeans(X, len[m], n, len[m], c_m[m], iters,
+                            init + ((size_t)h * M + m) * init_stride, 1, U, a, cnt);
+      if (s == OR_ERR_ARG || s == OR_ERR_MEM) { free(cnt); free(X); return s; }
+      if (s != OR_OK) status = s;
+      for (int j = 0; j < n; ++j) codes[((size_t)h * M + m) * n + j] = (uint16_t)a[j];
+      U += (size_t)c_m[m] * len[m];
+      o += len[m];
+    }
+  }
+  free(cnt);
+  free(X);
+  return status;
+}
+
+/* Eq. 5 for M subspaces: P_m[c, r] = <qbar_c[I_m], u_r^m>, the centroid's
+ * channels of I_m taken in the listed (ascending) order.  Tables per head:
+ * [c_q][C_1 + ... + C_M].                                                   */
+int oracle_tables_partition(int heads, int d, int M, const int *chan,
+                            const int *len, int c_q, const int *c_m,
+                            const float *qc, const float *kc, float *tables) {
+  if (check_partition(1 << 30, d, M, chan, len, c_m) != OR_OK) return OR_ERR_ARG;
+  int cs = 0, per_head = 0;
+  for (int m = 0; m < M; ++m) {
+    cs += c_m[m];
+    per_head += c_m[m] * len[m];
+  }
+  float qs[1024];
+  for (int h = 0; h < heads; ++h) {
+    const float *Q = qc + (size_t)h * c_q * d;
+    float *P = tables + (size_t)h * c_q * cs;
+    const float *U = kc + (size_t)h * per_head;
+    int col = 0, o = 0;
+    for (int m = 0; m < M; ++m) {
+      for (int c = 0; c < c_q; ++c) {
+        for (int kk = 0; kk < len[m]; ++kk) qs[kk] = Q[(size_t)c * d + chan[o + kk]];
+        for (int r = 0; r < c_m[m]; ++r)
+          P[(size_t)c * cs + col + r] = cdot(qs, U + (size_t)r * len[m], len[m]);
+      }
+      U += (size_t)c_m[m] * len[m];
+      col += c_m[m];
+      o += len[m];
+    }
+  }
+  return OR_OK;
+}
+
+/* Eq. 6 for M subspaces: s_cj = (1/sqrt d) * sum_m P_m[c, z_j^m], the sum
+ * taken left to right in subspace order, then scaled; + 0.0f as above.     */
+int oracle_proxy_scores_partition(int heads, int n, int d, int M, int c_q,
+                                  const int *c_m, const float *tables,
+                                  const uint16_t *codes, float *scores) {
+  if (M < 1 || M > OR_MAX_SUB) return OR_ERR_ARG;
+  int col[OR_MAX_SUB], cs = 0;
+  for (int m = 0; m < M; ++m) {
+    col[m] = cs;
+    cs += c_m[m];
+  }
+  float sigma = oracle_sigma(d);
+  for (int h = 0; h < heads; ++h)
+#pragma omp parallel for schedule(static)
+    for (int c = 0; c < c_q; ++c) {
+      const float *P = tables + ((size_t)h * c_q + c) * cs;
+      float *S = scores + ((size_t)h * c_q + c) * n;
+      for (int j = 0; j < n; ++j) {
+        float s = P[col[0] + codes[((size_t)h * M + 0) * n + j]];
+        for (int m = 1; m < M; ++m) s = s + P[col[m] + codes[((size_t)h * M + m) * n + j]];
+        s = s * sigma;
+        S[j] = s + 0.0f;
+      }
     }
   return OR_OK;
 }

@@ -82,6 +82,41 @@ CONFIGS = {
 }
 
 
+PARTITIONS = ("1", "2", "3-random", "3-rope", "4", "8")
+
+
+def partition_sets(cfg: LayerConfig, kind: str, seed: int = 0):
+    """Channel sets I_1..I_M of the key-partition ablation (Table 3), each
+    ascending: "1" all channels (full-dimensional clustering); "2", "4",
+    "8" equal contiguous ranges; "3-rope" the t/h/w RoPE ranges of the
+    workload; "3-random" a seeded random split of the channels into sets of
+    the RoPE range sizes."""
+    d = cfg.d
+    if kind == "3-rope":
+        off, ln = cfg.ranges
+        return [np.arange(o, o + l, dtype=np.int32) for o, l in zip(off, ln)]
+    if kind == "3-random":
+        perm = np.random.default_rng([cfg.seed, 1009, seed]).permutation(d)
+        cuts = np.cumsum(cfg.split)[:-1]
+        return [np.sort(x).astype(np.int32) for x in np.split(perm, cuts)]
+    m = int(kind)
+    if m < 1 or d % m:
+        raise ValueError(f"cannot split {d} channels into {m} equal ranges")
+    return [np.arange(i * d // m, (i + 1) * d // m, dtype=np.int32) for i in range(m)]
+
+
+def partition_init(cfg: LayerConfig, M: int, c_m: int, heads: int | None = None,
+                   head_offset: int = 0, seed: int = 0) -> np.ndarray:
+    """Seeded k-means starting rows for M key subspaces: [heads][M][c_m]."""
+    nh = cfg.heads if heads is None else heads
+    out = np.empty((nh, M, c_m), np.int32)
+    for hi in range(nh):
+        rng = np.random.default_rng([cfg.seed, 2003, seed, head_offset + hi])
+        for m in range(M):
+            out[hi, m] = init_rows(rng, cfg.n, c_m)
+    return out
+
+
 def bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round fp32 to bf16 (nearest, ties to even); returns the uint16 bits."""
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)

@@ -496,3 +496,115 @@ def test_layer_tiny_is_deterministic_and_consistent(oracle_lib):
     assert np.array_equal(a["sel"]["sel_idx"], b["sel"]["sel_idx"])
     codes = a["k"]["codes"]
     assert (codes >> 30 == 0).all() and ((codes & 1023) < cfg.c_m).all()
+
+
+# --------------------------------------------------------------------------
+# general key partitions (App. B; Table 3)
+
+def _planes(codes, M=3):
+    return np.stack([(codes >> (10 * m)) & 1023 for m in range(M)], 1).astype(np.uint16)
+
+
+def test_partition_with_rope_sets_reduces_to_the_three_ranges(oracle_lib):
+    cfg = inputs.CONFIGS["tiny"]
+    x = inputs.generate(cfg)
+    sets = inputs.partition_sets(cfg, "3-rope")
+    cm = [cfg.c_m] * 3
+    a = oracle.cluster_key_subspaces(x.k, cfg.ranges, cm, cfg.iters, x.init_k)
+    b = oracle.cluster_key_partition(x.k, sets, cm, cfg.iters, x.init_k)
+    assert np.array_equal(a["centroids"].view(np.uint32), b["centroids"].view(np.uint32))
+    assert np.array_equal(_planes(a["codes"]), b["codes"])
+    qc = oracle.cluster_queries(x.q, cfg.c_q, cfg.iters, x.init_q)["centroids"]
+    Pa = oracle.tables(qc, a["centroids"], cfg.ranges, cm)
+    Pb = oracle.tables_partition(qc, b["centroids"], sets, cm)
+    assert np.array_equal(Pa.view(np.uint32), Pb.view(np.uint32))
+    Sa = oracle.proxy_scores(Pa, a["codes"], cfg.d, cm)
+    Sb = oracle.proxy_scores_partition(Pb, b["codes"], cfg.d, cm)
+    assert np.array_equal(Sa.view(np.uint32), Sb.view(np.uint32))
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_partition_equals_ranges_of_channel_permuted_inputs(oracle_lib, seed):
+    # relabelling the channels so that the random sets become consecutive
+    # ranges leaves every dot product (same channels, same order) unchanged
+    cfg = inputs.CONFIGS["tiny"]
+    x = inputs.generate(cfg)
+    sets = inputs.partition_sets(cfg, "3-random", seed)
+    perm = np.concatenate(sets)
+    ln = [len(s) for s in sets]
+    ranges = ((0, ln[0], ln[0] + ln[1]), tuple(ln))
+    cm = [7, 5, 8]
+    init = x.init_k
+    a = oracle.cluster_key_partition(x.k, sets, cm, 4, init)
+    b = oracle.cluster_key_subspaces(x.k[:, :, perm], ranges, cm, 4, init)
+    assert np.array_equal(a["centroids"].view(np.uint32), b["centroids"].view(np.uint32))
+    assert np.array_equal(a["codes"], _planes(b["codes"]))
+    qc = oracle.cluster_queries(x.q, cfg.c_q, 3, x.init_q)["centroids"]
+    Pa = oracle.tables_partition(qc, a["centroids"], sets, cm)
+    Pb = oracle.tables(qc[:, :, perm], b["centroids"], ranges, cm)
+    assert np.array_equal(Pa.view(np.uint32), Pb.view(np.uint32))
+    Sa = oracle.proxy_scores_partition(Pa, a["codes"], cfg.d, cm)
+    Sb = oracle.proxy_scores(Pb, b["codes"], cfg.d, cm)
+    assert np.array_equal(Sa.view(np.uint32), Sb.view(np.uint32))
+
+
+@pytest.mark.parametrize("M", [1, 2, 5, 8])
+def test_partition_lookup_sum_equals_full_centroid_dot(oracle_lib, M):
+    # App. B for M subspaces: sum_m P_m[c, z^m] = <qbar_c, khat_j>, where khat_j
+    # puts each subspace centroid back on its channels; exact on dyadic data
+    rng = np.random.default_rng(40 + M)
+    d, cq, n = 16, 4, 50
+    perm = rng.permutation(d)
+    cuts = np.sort(rng.choice(np.arange(1, d), M - 1, replace=False))
+    sets = [np.sort(s) for s in np.split(perm, cuts)]
+    cm = [int(rng.integers(2, 6)) for _ in range(M)]
+    qc = (rng.integers(-8, 8, size=(1, cq, d)) / 4).astype(np.float32)
+    U = [(rng.integers(-8, 8, size=(cm[m], len(sets[m]))) / 4).astype(np.float32)
+         for m in range(M)]
+    kc = np.concatenate([u.ravel() for u in U])[None]
+    z = np.stack([rng.integers(0, cm[m], size=n) for m in range(M)], 0)
+    P = oracle.tables_partition(qc, kc, sets, cm)
+    S = oracle.proxy_scores_partition(P, z.astype(np.uint16)[None], d, cm)
+    khat = np.zeros((n, d))
+    for m in range(M):
+        khat[:, sets[m]] = U[m][z[m]]
+    full = qc[0].astype(np.float64) @ khat.T
+    col = np.concatenate([[0], np.cumsum(cm)])
+    sums = sum(P[0][:, col[m] + z[m]].astype(np.float64) for m in range(M))
+    assert np.array_equal(sums, full)
+    assert np.array_equal(S[0], (full * 0.25).astype(np.float32))
+
+
+def test_partition_codes_are_argmins_of_returned_centroids(oracle_lib):
+    # each subspace is k-means of K[:, I_m]: labels are exact argmins of the
+    # returned centroids (fp64 distances where the margin is clear)
+    rng = np.random.default_rng(7)
+    n, d = 300, 12
+    sets = [np.array([0, 5, 7]), np.array([1, 2, 3, 4, 6, 8]), np.array([9, 10, 11])]
+    cm = [4, 6, 3]
+    k = rng.standard_normal((1, n, d)).astype(np.float32)
+    init = np.stack([inputs.init_rows(rng, n, 6) for _ in range(3)])[None]
+    r = oracle.cluster_key_partition(k, sets, cm, 6, init)
+    U = np.split(r["centroids"][0], np.cumsum([cm[m] * len(sets[m]) for m in range(3)])[:-1])
+    for m in range(3):
+        Um = U[m].reshape(cm[m], len(sets[m])).astype(np.float64)
+        X = k[0][:, sets[m]].astype(np.float64)
+        D = ((X[:, None, :] - Um[None]) ** 2).sum(-1)
+        srt = np.sort(D, 1)
+        clear = srt[:, 1] - srt[:, 0] > 1e-4
+        assert np.array_equal(r["codes"][0, m][clear], D.argmin(1)[clear])
+        # a final assignment over the returned centroids changes no label
+        assert np.array_equal(r["codes"][0, m], oracle.assign_rows(X.astype(np.float32),
+                                                                   U[m].reshape(cm[m], -1)))
+
+
+def test_partition_rejects_bad_sets(oracle_lib):
+    k = np.zeros((1, 20, 6), np.float32)
+    init = np.zeros((1, 2, 4), np.int32)
+    init[:] = np.arange(4)
+    for sets in ([[0, 1, 2], [2, 3, 4, 5]],      # overlap
+                 [[0, 1], [2, 3, 4]],            # channel 5 missing
+                 [[1, 0, 2], [3, 4, 5]],         # not ascending
+                 [[0, 1, 2], [3, 4, 6]]):        # out of range
+        with pytest.raises(ValueError):
+            oracle.cluster_key_partition(k, sets, [2, 2], 1, init)
