@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define SCOPE_ABI_VERSION 1
+#define SCOPE_ABI_VERSION 2
 
 typedef enum {
   SCOPE_OK = 0,
@@ -83,6 +83,23 @@ typedef struct {
   int32_t range_off[3];
   int32_t range_len[3];
 } scope_shape;
+
+/* A general key partition (App. B; the partition ablation of Table 3): the
+ * d channels split into M disjoint sets I_1 .. I_M that together cover all
+ * of them, subspace m clustered into c[m] centroids.  `channels` lists I_1,
+ * then I_2, ... (len[0] + ... + len[M-1] = d entries), each set in strictly
+ * ascending channel order; entries past d are ignored.  The three RoPE
+ * ranges in T, H, W order give exactly the results of calls 2-4.
+ * Supported: 1 <= M <= 8, 1 <= c[m] <= min(n, 1024), c[0] + ... + c[M-1]
+ * <= 3072 (one table row of a cluster is staged on chip during selection). */
+#define SCOPE_MAX_SUBSPACES 8
+#define SCOPE_MAX_D 128
+typedef struct {
+  int32_t m;
+  int32_t c[SCOPE_MAX_SUBSPACES];
+  int32_t len[SCOPE_MAX_SUBSPACES];
+  int32_t channels[SCOPE_MAX_D];
+} scope_partition;
 
 int32_t scope_abi_version(void);
 const char *scope_status_string(int32_t status);
@@ -182,6 +199,63 @@ int32_t scope_select_policy(const scope_shape *shape, int32_t c_q,
                             int32_t *k_head, int32_t *sel_counts,
                             int32_t *sel_idx, void *workspace, size_t ws_bytes,
                             int32_t policy, void *stream);
+
+/* 2p-4p. Calls 2-4 for a general key partition (App. B; Table 3).  The
+ * shape's range fields are ignored (checked only by calls 2-4); `part`
+ * (host memory) gives the sets and codebook sizes.  Errors as calls 2-4, and
+ * SCOPE_ERR_INVALID_ARGUMENT for sets that are not a partition of the d
+ * channels or not ascending, SCOPE_ERR_UNSUPPORTED beyond the limits above.
+ *
+ * Workspace bytes that suffice for the three partition calls and for calls 1
+ * and 5 with these sizes.  When the sets are not the contiguous ranges
+ * [0, len[0]), [len[0], len[0] + len[1]), ... this includes a channel-
+ * reordered copy of K (heads * n * d elements).                            */
+int32_t scope_partition_workspace_size(const scope_shape *shape, int32_t c_q,
+                                       const scope_partition *part,
+                                       size_t *bytes);
+
+/* Key subspace clustering over the sets of `part`: for each m, k-means of
+ * K[:, I_m] (the channels of I_m in ascending order) into c[m] centroids,
+ * exactly as call 2 (same arithmetic, iterations plus one last assignment).
+ * init_idx[(h * M + m) * init_stride + r] are the starting rows (NULL =
+ * default rows), init_stride >= max c[m].
+ * Outputs: k_centroids [heads][sum_m c[m] * len[m]] fp32, per head U^1 ..
+ * U^M back to back, each [c[m]][len[m]] with column k on channel I_m[k];
+ * codes [heads][M][n] uint16, z^m of key j at codes[(h * M + m) * n + j].  */
+int32_t scope_cluster_key_partition(const scope_shape *shape, const void *k,
+                                    const scope_partition *part, int32_t iters,
+                                    const int32_t *init_idx,
+                                    int32_t init_stride, float *k_centroids,
+                                    uint16_t *codes, void *workspace,
+                                    size_t ws_bytes, int32_t *dev_status,
+                                    void *stream);
+
+/* Tables and proxy logits over the sets of `part` (Eq. 5-6): tables
+ * [heads][c_q][c[0] + ... + c[M-1]], P_m[c][r] = <qbar_c[I_m], u_r^m> as an
+ * fp32 fma chain over I_m in ascending channel order; if `scores` is not
+ * NULL, s_cj = fl(fl(...fl(P_1[z^1] + P_2[z^2]) ... + P_M[z^M]) *
+ * fl32(1/sqrt(d))) + 0.0, summed left to right (M = 1: no addition).
+ * Uses the workspace when the sets are not contiguous ranges in order.    */
+int32_t scope_proxy_scores_partition(const scope_shape *shape,
+                                     const float *q_centroids, int32_t c_q,
+                                     const float *k_centroids,
+                                     const scope_partition *part,
+                                     const uint16_t *codes, float *tables,
+                                     float *scores, void *workspace,
+                                     size_t ws_bytes, void *stream);
+
+/* Selection (call 4b) with the logits of `part`: from `scores` if not
+ * NULL, else from (tables, codes) exactly as scope_proxy_scores_partition
+ * computes them.  Arguments, outputs and errors otherwise as call 4b.      */
+int32_t scope_select_partition(const scope_shape *shape, int32_t c_q,
+                               const scope_partition *part,
+                               const float *scores, const float *tables,
+                               const uint16_t *codes, const int32_t *counts,
+                               float rho, int32_t k_fix, int32_t *base_counts,
+                               int32_t *topp_counts, int32_t *k_head,
+                               int32_t *sel_counts, int32_t *sel_idx,
+                               void *workspace, size_t ws_bytes, int32_t policy,
+                               void *stream);
 
 /* 5. Sparse attention over the selected keys (Eq. 11; Alg. 1 last step).
  * For every cluster c and every query i in perm[offsets[c] .. offsets[c+1]):

@@ -23,7 +23,10 @@ ENTRY_POINTS = (
     "scope_cluster_queries", "scope_cluster_key_subspaces",
     "scope_proxy_scores", "scope_select", "scope_select_policy",
     "scope_sparse_attention", "scope_debug_fixexp",
+    "scope_partition_workspace_size", "scope_cluster_key_partition",
+    "scope_proxy_scores_partition", "scope_select_partition",
 )
+MAX_SUBSPACES, MAX_D = 8, 128
 POLICIES = {"online": 0, "fixed": 1, "topp": 2}
 
 
@@ -45,6 +48,31 @@ def make_shape(heads, n, d, dtype, ranges) -> Shape:
     return Shape(int(heads), int(n), int(d), int(dtype),
                  (ctypes.c_int32 * 3)(*map(int, off)),
                  (ctypes.c_int32 * 3)(*map(int, ln)))
+
+
+class Partition(ctypes.Structure):
+    """A general key partition: M channel sets and their codebook sizes."""
+    _fields_ = [("m", ctypes.c_int32), ("c", ctypes.c_int32 * MAX_SUBSPACES),
+                ("len", ctypes.c_int32 * MAX_SUBSPACES),
+                ("channels", ctypes.c_int32 * MAX_D)]
+
+
+def make_partition(sets, c_m) -> Partition:
+    """sets: M sequences of channel indices (each ascending); c_m: M sizes."""
+    sets = [list(map(int, x)) for x in sets]
+    if len(sets) != len(c_m) or not 1 <= len(sets) <= MAX_SUBSPACES:
+        raise ValueError("need 1..8 channel sets, one codebook size each")
+    chan = [ch for x in sets for ch in x]
+    if len(chan) > MAX_D:
+        raise ValueError("more than 128 channels")
+    p = Partition()
+    p.m = len(sets)
+    for m, x in enumerate(sets):
+        p.c[m] = int(c_m[m])
+        p.len[m] = len(x)
+    for t, ch in enumerate(chan):
+        p.channels[t] = ch
+    return p
 
 
 _lib = None
@@ -75,6 +103,12 @@ def lib() -> ctypes.CDLL:
         L.scope_sparse_attention.argtypes = [SP, P, P, P, I, P, P, P, P,
                                              ctypes.c_float, P, P, Z, P]
         L.scope_debug_fixexp.argtypes = [P, P, ctypes.c_int64, P]
+        PP = ctypes.POINTER(Partition)
+        L.scope_partition_workspace_size.argtypes = [SP, I, PP, ctypes.POINTER(Z)]
+        L.scope_cluster_key_partition.argtypes = [SP, P, PP, I, P, I, P, P, P, Z, P, P]
+        L.scope_proxy_scores_partition.argtypes = [SP, P, I, P, PP, P, P, P, P, Z, P]
+        L.scope_select_partition.argtypes = [SP, I, PP, P, P, P, P, ctypes.c_float, I,
+                                             P, P, P, P, P, P, Z, I, P]
         for name in ENTRY_POINTS[2:]:
             getattr(L, name).restype = I
         _lib = L
@@ -234,3 +268,76 @@ def scope_debug_fixexp(y, out, stream=None):
     _check("scope_debug_fixexp", lib().scope_debug_fixexp(
         _ptr(y, torch.float32, None, "y"), _ptr(out, torch.int64, y.numel(), "out"),
         y.numel(), _stream(stream)))
+
+
+def scope_partition_workspace_size(shape: Shape, c_q: int, part: Partition) -> int:
+    out = ctypes.c_size_t(0)
+    _check("scope_partition_workspace_size",
+           lib().scope_partition_workspace_size(ctypes.byref(shape), int(c_q),
+                                                ctypes.byref(part), ctypes.byref(out)))
+    return int(out.value)
+
+
+def alloc_partition_workspace(shape: Shape, c_q: int, part: Partition, device="cuda"):
+    return torch.empty(max(scope_partition_workspace_size(shape, c_q, part), 1),
+                       dtype=torch.uint8, device=device)
+
+
+def _part_sizes(part: Partition):
+    per_head = sum(int(part.c[m]) * int(part.len[m]) for m in range(part.m))
+    cs = sum(int(part.c[m]) for m in range(part.m))
+    return per_head, cs
+
+
+def scope_cluster_key_partition(shape, k, part, iters, init_idx, init_stride,
+                                k_centroids, codes, workspace, dev_status=None,
+                                stream=None):
+    """codes: int16 tensor holding the uint16 codes [heads][M][n]."""
+    H, N, D = shape.heads, shape.n, shape.d
+    per_head, _ = _part_sizes(part)
+    _check("scope_cluster_key_partition", lib().scope_cluster_key_partition(
+        ctypes.byref(shape), _ptr(k, _data_dtype(shape), H * N * D, "k"),
+        ctypes.byref(part), int(iters),
+        _ptr(init_idx, torch.int32, H * part.m * int(init_stride), "init_idx",
+             optional=True), int(init_stride),
+        _ptr(k_centroids, torch.float32, H * per_head, "k_centroids"),
+        _ptr(codes, torch.int16, H * part.m * N, "codes"),
+        _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(),
+        _ptr(dev_status, torch.int32, 1, "dev_status", optional=True),
+        _stream(stream)))
+
+
+def scope_proxy_scores_partition(shape, q_centroids, c_q, k_centroids, part, codes,
+                                 tables, scores, workspace, stream=None):
+    H, N, D = shape.heads, shape.n, shape.d
+    per_head, cs = _part_sizes(part)
+    _check("scope_proxy_scores_partition", lib().scope_proxy_scores_partition(
+        ctypes.byref(shape),
+        _ptr(q_centroids, torch.float32, H * c_q * D, "q_centroids"), int(c_q),
+        _ptr(k_centroids, torch.float32, H * per_head, "k_centroids"),
+        ctypes.byref(part),
+        _ptr(codes, torch.int16, H * part.m * N, "codes", optional=scores is None),
+        _ptr(tables, torch.float32, H * c_q * cs, "tables"),
+        _ptr(scores, torch.float32, H * c_q * N, "scores", optional=True),
+        _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(),
+        _stream(stream)))
+
+
+def scope_select_partition(shape, c_q, part, scores, tables, codes, counts, rho,
+                           k_fix, base_counts, topp_counts, k_head, sel_counts,
+                           sel_idx, workspace, policy="online", stream=None):
+    H, N = shape.heads, shape.n
+    _, cs = _part_sizes(part)
+    _check("scope_select_partition", lib().scope_select_partition(
+        ctypes.byref(shape), int(c_q), ctypes.byref(part),
+        _ptr(scores, torch.float32, H * c_q * N, "scores", optional=True),
+        _ptr(tables, torch.float32, H * c_q * cs, "tables", optional=True),
+        _ptr(codes, torch.int16, H * part.m * N, "codes", optional=True),
+        _ptr(counts, torch.int32, H * c_q, "counts"), float(rho), int(k_fix),
+        _ptr(base_counts, torch.int32, H * c_q, "base_counts"),
+        _ptr(topp_counts, torch.int32, H * c_q, "topp_counts", optional=True),
+        _ptr(k_head, torch.int32, H, "k_head"),
+        _ptr(sel_counts, torch.int32, H * c_q, "sel_counts"),
+        _ptr(sel_idx, torch.int32, H * c_q * N, "sel_idx"),
+        _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(),
+        POLICIES[policy], _stream(stream)))

@@ -33,12 +33,19 @@ struct Carver {
   }
 };
 
-int32_t check_shape(const scope_shape *s) {
+// Sizes and dtype only (the partition calls ignore the range fields).
+int32_t check_dims(const scope_shape *s) {
   if (!s) return SCOPE_ERR_INVALID_ARGUMENT;
   if (s->heads < 1 || s->n < 1 || s->d < 2) return SCOPE_ERR_INVALID_ARGUMENT;
   if (s->dtype != SCOPE_F32 && s->dtype != SCOPE_BF16) return SCOPE_ERR_UNSUPPORTED;
   if (s->n > kMaxN || s->d > 128 || s->heads > 65535) return SCOPE_ERR_UNSUPPORTED;
   if (static_cast<long long>(s->heads) * s->n > (1LL << 31) - 1) return SCOPE_ERR_UNSUPPORTED;
+  return SCOPE_OK;
+}
+
+int32_t check_shape(const scope_shape *s) {
+  const int32_t st = check_dims(s);
+  if (st) return st;
   int total = 0;
   for (int m = 0; m < 3; ++m) {
     const int o = s->range_off[m], l = s->range_len[m];
@@ -92,6 +99,13 @@ scope::AccPlan key_plan(const scope_shape *s, const int32_t *c_m) {
   const int C[3] = {c_m[0], c_m[1], c_m[2]};
   scope::km_accum_plan(3, s->range_off, s->range_len, C, s->heads, s->n, &p);
   return p;
+}
+
+scope::Subspaces three_subspaces(const int32_t *c_m) {
+  scope::Subspaces sub{};
+  sub.M = 3;
+  for (int m = 0; m < 3; ++m) sub.c[m] = c_m[m];
+  return sub;
 }
 
 struct QueryWs {
@@ -163,6 +177,114 @@ size_t attn_ws(const scope_shape *s, int c_q, void *base, int4 **items) {
   Carver cv(base);
   int4 *it = cv.take<int4>(static_cast<size_t>(s->heads) * scope::attn_items_per_head(s->n, c_q));
   if (items) *items = it;
+  return cv.used;
+}
+
+// --- general key partitions ----------------------------------------------
+int32_t check_partition(const scope_shape *s, const scope_partition *p) {
+  if (!p || p->m < 1) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (p->m > scope::kMaxSub) return SCOPE_ERR_UNSUPPORTED;
+  int total = 0, cs = 0;
+  for (int m = 0; m < p->m; ++m) {
+    if (p->len[m] < 1 || p->c[m] < 1 || p->c[m] > s->n) return SCOPE_ERR_INVALID_ARGUMENT;
+    if (p->c[m] > kMaxC) return SCOPE_ERR_UNSUPPORTED;
+    total += p->len[m];
+    cs += p->c[m];
+  }
+  if (total != s->d) return SCOPE_ERR_INVALID_ARGUMENT;
+  bool seen[SCOPE_MAX_D] = {};
+  int t = 0;
+  for (int m = 0; m < p->m; ++m)
+    for (int k = 0; k < p->len[m]; ++k, ++t) {
+      const int ch = p->channels[t];
+      if (ch < 0 || ch >= s->d || seen[ch]) return SCOPE_ERR_INVALID_ARGUMENT;
+      if (k > 0 && ch <= p->channels[t - 1]) return SCOPE_ERR_INVALID_ARGUMENT;
+      seen[ch] = true;
+    }
+  if (cs > scope::kSelMaxTable) return SCOPE_ERR_UNSUPPORTED;
+  return SCOPE_OK;
+}
+
+// The sets are the ranges [0, len0), [len0, len0 + len1), ...: no reordering.
+bool partition_in_order(const scope_shape *s, const scope_partition *p) {
+  for (int t = 0; t < s->d; ++t)
+    if (p->channels[t] != t) return false;
+  return true;
+}
+
+struct PartGeom {
+  int M;
+  int off[scope::kMaxSub], len[scope::kMaxSub], C[scope::kMaxSub];
+  size_t per_head;  // centroid floats of one head
+};
+PartGeom part_geom(const scope_partition *p) {
+  PartGeom g{};
+  g.M = p->m;
+  int off = 0;
+  for (int m = 0; m < p->m; ++m) {
+    g.off[m] = off;  // position of subspace m in the reordered channels
+    g.len[m] = p->len[m];
+    g.C[m] = p->c[m];
+    off += p->len[m];
+    g.per_head += static_cast<size_t>(p->c[m]) * p->len[m];
+  }
+  return g;
+}
+scope::Subspaces part_subspaces(const PartGeom &g) {
+  scope::Subspaces sub{};
+  sub.M = g.M;
+  for (int m = 0; m < g.M; ++m) sub.c[m] = g.C[m];
+  return sub;
+}
+scope::ChannelMap part_map(const scope_shape *s, const scope_partition *p) {
+  scope::ChannelMap map{};
+  for (int t = 0; t < s->d; ++t) map.chan[t] = p->channels[t];
+  return map;
+}
+scope::AccPlan part_plan(const scope_shape *s, const PartGeom &g) {
+  scope::AccPlan plan;
+  scope::km_accum_plan(g.M, g.off, g.len, g.C, s->heads, s->n, &plan);
+  return plan;
+}
+
+struct PartKeyWs {
+  void *kp;  // channel-reordered K, or null
+  int32_t *assign;
+  long long *slab;
+  int32_t *cslab;
+  uint16_t *ubf[scope::kMaxSub];
+  float *nu[scope::kMaxSub], *bnd[scope::kMaxSub];
+};
+size_t part_key_ws(const scope_shape *s, const scope_partition *p, void *base,
+                   PartKeyWs *w) {
+  Carver cv(base);
+  const size_t H = static_cast<size_t>(s->heads);
+  const PartGeom g = part_geom(p);
+  const scope::AccPlan plan = part_plan(s, g);
+  PartKeyWs k{};
+  if (!partition_in_order(s, p)) {
+    const size_t elems = H * s->n * s->d;
+    k.kp = s->dtype == SCOPE_BF16 ? static_cast<void *>(cv.take<uint16_t>(elems))
+                                  : static_cast<void *>(cv.take<float>(elems));
+  }
+  k.assign = cv.take<int32_t>(H * g.M * s->n);
+  k.slab = cv.take<long long>(scope::km_accum_slab_bytes(plan, s->heads) / sizeof(long long));
+  k.cslab = cv.take<int32_t>(scope::km_accum_cslab_bytes(plan, s->heads) / sizeof(int32_t));
+  for (int m = 0; m < g.M; ++m) {
+    const int cpad = scope::km_cpad(g.C[m]);
+    k.ubf[m] = cv.take<uint16_t>(H * cpad * 2 * scope::km_dxp(g.len[m]));
+    k.nu[m] = cv.take<float>(H * cpad);
+    k.bnd[m] = cv.take<float>(H * cpad * 2);
+  }
+  if (w) *w = k;
+  return cv.used;
+}
+
+// channel-reordered query centroids for the tables
+size_t part_table_ws(const scope_shape *s, int c_q, void *base, float **qp) {
+  Carver cv(base);
+  float *q = cv.take<float>(static_cast<size_t>(s->heads) * c_q * s->d);
+  if (qp) *qp = q;
   return cv.used;
 }
 
@@ -350,12 +472,13 @@ int32_t scope_proxy_scores(const scope_shape *shape, const float *q_centroids,
   if (!q_centroids || !k_centroids || !tables) return SCOPE_ERR_INVALID_ARGUMENT;
   if (scores && !codes) return SCOPE_ERR_INVALID_ARGUMENT;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  const scope::Subspaces sub = three_subspaces(c_m);
   SCOPE_TRY(scope::score_tables(shape->heads, shape->d, shape->range_off,
-                                shape->range_len, c_q, c_m, q_centroids,
+                                shape->range_len, c_q, sub, q_centroids,
                                 k_centroids, tables, s));
   if (scores)
-    SCOPE_TRY(scope::score_logits(shape->heads, shape->n, shape->d, c_q, c_m,
-                                  tables, codes, scores, s));
+    SCOPE_TRY(scope::score_logits(shape->heads, shape->n, shape->d, c_q, sub,
+                                  tables, codes, nullptr, scores, s));
   return SCOPE_OK;
 }
 
@@ -383,8 +506,9 @@ int32_t scope_select_policy(const scope_shape *shape, int32_t c_q,
   if ((st = check_ws(workspace, ws_bytes, need))) return st;
   SelectWs w;
   select_ws(shape, c_q, workspace, &w);
-  SCOPE_TRY(scope::select_run(shape->heads, shape->n, c_q, c_m, shape->d,
-                              scores, tables, codes, counts, rho, k_fix,
+  SCOPE_TRY(scope::select_run(shape->heads, shape->n, c_q, three_subspaces(c_m),
+                              shape->d, scores, tables, codes, nullptr, counts,
+                              rho, k_fix,
                               base_counts, topp_counts, k_head, sel_counts,
                               sel_idx, w.row_max, w.row_state, w.coarse_hist, policy,
                               static_cast<hipStream_t>(stream)));
@@ -402,6 +526,169 @@ int32_t scope_select(const scope_shape *shape, int32_t c_q,
                              k_fix, base_counts, topp_counts, k_head, sel_counts,
                              sel_idx, workspace, ws_bytes, SCOPE_POLICY_ONLINE,
                              stream);
+}
+
+int32_t scope_partition_workspace_size(const scope_shape *shape, int32_t c_q,
+                                       const scope_partition *part,
+                                       size_t *bytes) {
+  int32_t st = check_dims(shape);
+  if (st) return st;
+  if ((st = check_cq(shape, c_q))) return st;
+  if ((st = check_partition(shape, part))) return st;
+  if (!bytes) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (query_plan(shape, c_q).nwin == 0 || part_plan(shape, part_geom(part)).nwin == 0)
+    return SCOPE_ERR_UNSUPPORTED;
+  size_t need = query_ws(shape, c_q, nullptr, nullptr);
+  for (size_t x : {part_key_ws(shape, part, nullptr, nullptr),
+                   part_table_ws(shape, c_q, nullptr, nullptr),
+                   select_ws(shape, c_q, nullptr, nullptr),
+                   attn_ws(shape, c_q, nullptr, nullptr)})
+    if (x > need) need = x;
+  *bytes = need;
+  return SCOPE_OK;
+}
+
+int32_t scope_cluster_key_partition(const scope_shape *shape, const void *k,
+                                    const scope_partition *part, int32_t iters,
+                                    const int32_t *init_idx,
+                                    int32_t init_stride, float *k_centroids,
+                                    uint16_t *codes, void *workspace,
+                                    size_t ws_bytes, int32_t *dev_status,
+                                    void *stream) {
+  int32_t st = check_dims(shape);
+  if (st) return st;
+  if ((st = check_partition(shape, part))) return st;
+  if (iters < 1) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (!k || !k_centroids || !codes) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (!aligned_data(k, shape)) return SCOPE_ERR_INVALID_ARGUMENT;
+  const PartGeom g = part_geom(part);
+  if (init_idx) {
+    int mx = 0;
+    for (int m = 0; m < g.M; ++m) mx = g.C[m] > mx ? g.C[m] : mx;
+    if (init_stride < mx) return SCOPE_ERR_INVALID_ARGUMENT;
+  }
+  const scope::AccPlan plan = part_plan(shape, g);
+  if (plan.nwin == 0) return SCOPE_ERR_UNSUPPORTED;
+  const size_t need = part_key_ws(shape, part, nullptr, nullptr);
+  if ((st = check_ws(workspace, ws_bytes, need))) return st;
+  PartKeyWs w;
+  part_key_ws(shape, part, workspace, &w);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int n = shape->n, d = shape->d, M = g.M;
+  const bool bf16 = shape->dtype == SCOPE_BF16;
+  const void *x = k;
+  if (w.kp) {
+    SCOPE_TRY(scope::gather_channels(k, w.kp, static_cast<size_t>(shape->heads) * n, d,
+                                     bf16 ? 2 : 4, part_map(shape, part), s));
+    x = w.kp;
+  }
+  KmProblem p[scope::kMaxSub];
+  size_t ucol = 0;
+  for (int m = 0; m < M; ++m) {
+    KmProblem &pm = p[m];
+    pm = KmProblem{};
+    pm.x = x;
+    pm.bf16 = bf16;
+    pm.x_head_stride = static_cast<size_t>(n) * d;
+    pm.ld = d;
+    pm.col0 = g.off[m];
+    pm.dx = g.len[m];
+    pm.n = n;
+    pm.C = g.C[m];
+    pm.u = k_centroids + ucol;
+    pm.u_head_stride = g.per_head;
+    pm.assign = w.assign + static_cast<size_t>(m) * n;
+    pm.a_head_stride = static_cast<size_t>(M) * n;
+    pm.heads = shape->heads;
+    pm.mfma = scope::km_mfma_ok(pm.bf16, pm.ld, pm.col0, pm.dx, pm.C);
+    pm.cpad = scope::km_cpad(pm.C);
+    pm.dxp = scope::km_dxp(pm.dx);
+    pm.ubf = w.ubf[m];
+    pm.nu = w.nu[m];
+    pm.bnd = w.bnd[m];
+    ucol += static_cast<size_t>(g.C[m]) * pm.dx;
+    // rows of head h, subspace m at init_idx[(h*M + m)*init_stride]
+    const int32_t *init = init_idx ? init_idx + static_cast<size_t>(m) * init_stride : nullptr;
+    SCOPE_TRY(scope::km_init(pm, init, M * init_stride, dev_status, s));
+  }
+  for (int it = 0; it < iters; ++it) {
+    for (int m = 0; m < M; ++m) SCOPE_TRY(scope::km_assign(p[m], false, s));
+    SCOPE_TRY(scope::km_accum(plan, x, bf16, p[0].x_head_stride, d, n, shape->heads,
+                              w.assign, static_cast<size_t>(M) * n, n, w.slab, w.cslab,
+                              k_centroids, g.per_head, it == 0 ? dev_status : nullptr, s));
+  }
+  for (int m = 0; m < M; ++m) SCOPE_TRY(scope::km_assign(p[m], false, s));
+  SCOPE_TRY(scope::km_codes16(w.assign, static_cast<size_t>(shape->heads) * M * n, codes, s));
+  return SCOPE_OK;
+}
+
+int32_t scope_proxy_scores_partition(const scope_shape *shape,
+                                     const float *q_centroids, int32_t c_q,
+                                     const float *k_centroids,
+                                     const scope_partition *part,
+                                     const uint16_t *codes, float *tables,
+                                     float *scores, void *workspace,
+                                     size_t ws_bytes, void *stream) {
+  int32_t st = check_dims(shape);
+  if (st) return st;
+  if ((st = check_cq(shape, c_q))) return st;
+  if ((st = check_partition(shape, part))) return st;
+  if (!q_centroids || !k_centroids || !tables) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (scores && !codes) return SCOPE_ERR_INVALID_ARGUMENT;
+  const bool in_order = partition_in_order(shape, part);
+  if (!in_order &&
+      (st = check_ws(workspace, ws_bytes, part_table_ws(shape, c_q, nullptr, nullptr))))
+    return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const PartGeom g = part_geom(part);
+  const scope::Subspaces sub = part_subspaces(g);
+  const float *qc = q_centroids;
+  if (!in_order) {
+    float *qp = nullptr;
+    part_table_ws(shape, c_q, workspace, &qp);
+    SCOPE_TRY(scope::gather_channels(q_centroids, qp, static_cast<size_t>(shape->heads) * c_q,
+                                     shape->d, 4, part_map(shape, part), s));
+    qc = qp;
+  }
+  SCOPE_TRY(scope::score_tables(shape->heads, shape->d, g.off, g.len, c_q, sub, qc,
+                                k_centroids, tables, s));
+  if (scores)
+    SCOPE_TRY(scope::score_logits(shape->heads, shape->n, shape->d, c_q, sub, tables,
+                                  nullptr, codes, scores, s));
+  return SCOPE_OK;
+}
+
+int32_t scope_select_partition(const scope_shape *shape, int32_t c_q,
+                               const scope_partition *part,
+                               const float *scores, const float *tables,
+                               const uint16_t *codes, const int32_t *counts,
+                               float rho, int32_t k_fix, int32_t *base_counts,
+                               int32_t *topp_counts, int32_t *k_head,
+                               int32_t *sel_counts, int32_t *sel_idx,
+                               void *workspace, size_t ws_bytes, int32_t policy,
+                               void *stream) {
+  int32_t st = check_dims(shape);
+  if (policy != SCOPE_POLICY_ONLINE && policy != SCOPE_POLICY_FIXED &&
+      policy != SCOPE_POLICY_TOPP)
+    return SCOPE_ERR_INVALID_ARGUMENT;
+  if (st) return st;
+  if ((st = check_cq(shape, c_q))) return st;
+  if ((st = check_partition(shape, part))) return st;
+  if (!scores && (!tables || !codes)) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (!counts || !base_counts || !k_head || !sel_counts || !sel_idx)
+    return SCOPE_ERR_INVALID_ARGUMENT;
+  if (!(rho > 0.0f && rho <= 1.0f)) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (k_fix < 1 || k_fix > shape->n) return SCOPE_ERR_INVALID_ARGUMENT;
+  const size_t need = select_ws(shape, c_q, nullptr, nullptr);
+  if ((st = check_ws(workspace, ws_bytes, need))) return st;
+  SelectWs w;
+  select_ws(shape, c_q, workspace, &w);
+  SCOPE_TRY(scope::select_run(shape->heads, shape->n, c_q, part_subspaces(part_geom(part)),
+                              shape->d, scores, tables, nullptr, codes, counts, rho,
+                              k_fix, base_counts, topp_counts, k_head, sel_counts,
+                              sel_idx, w.row_max, w.row_state, w.coarse_hist, policy,
+                              static_cast<hipStream_t>(stream)));
+  return SCOPE_OK;
 }
 
 int32_t scope_sparse_attention(const scope_shape *shape, const void *q,

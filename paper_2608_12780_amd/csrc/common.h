@@ -75,6 +75,31 @@ __device__ __forceinline__ float proxy_logit(const float *P, int cT, int cTH,
   return s + 0.0f;
 }
 
+// The same sum over the M subspaces of a general partition, left to right
+// in subspace order (M = 3 gives the expression above), from one uint16
+// code plane per subspace: z^m of key j at planes[m * n + j].  col[m] is
+// the first table column of subspace m, col[M] the row length.
+constexpr int kCodeMaxSub = 8;
+struct CodePlanes {
+  int M;
+  int col[kCodeMaxSub + 1];
+};
+__device__ __forceinline__ float proxy_logit_planes(const float *P,
+                                                    const CodePlanes &cp,
+                                                    const uint16_t *planes,
+                                                    size_t n, int j, float sigma) {
+  float s = P[min(static_cast<int>(planes[j]), cp.col[1] - 1)];
+#pragma unroll
+  for (int m = 1; m < kCodeMaxSub; ++m) {
+    if (m < cp.M) {
+      const int z = min(static_cast<int>(planes[m * n + j]), cp.col[m + 1] - cp.col[m] - 1);
+      s = s + P[cp.col[m] + z];
+    }
+  }
+  s = s * sigma;
+  return s + 0.0f;
+}
+
 // Rank key: logits in DEScending order map to ascending unsigned keys.
 __device__ __forceinline__ uint32_t desc_key(float s) {
   uint32_t u = __float_as_uint(s);

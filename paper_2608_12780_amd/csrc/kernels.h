@@ -49,7 +49,7 @@ hipError_t km_init(const KmProblem &p, const int32_t *init, int init_stride,
 hipError_t km_assign(const KmProblem &p, bool with_hist, hipStream_t s);
 hipError_t km_group(const KmProblem &p, hipStream_t s);
 
-// Centroid update by one streaming pass over the rows.  Up to three
+// Centroid update by one streaming pass over the rows.  Up to kMaxSub
 // subspaces of the same rows (channels col0[m] .. col0[m]+dx[m], C[m]
 // clusters, centroids [C[m]][dx[m]] at float offset ucol[m] of a head) are
 // updated together; their channels are cut into windows whose int64 sums
@@ -58,6 +58,7 @@ constexpr int kAccLds = 16384;           // int64 sums per block
 constexpr int kAccCnt = 3072;            // int32 cluster counts per block
 constexpr int kAccMaxPieces = 4;
 constexpr int kAccMaxWindows = 16;
+constexpr int kMaxSub = 8;               // subspaces of a key partition
 constexpr int kAccTargetBlocks = 256;    // blocks per launch, about one per CU
 struct AccPiece {
   int m, sub0, width;   // channels sub0 .. sub0+width of subspace m
@@ -70,7 +71,7 @@ struct AccWindow {
 };
 struct AccPlan {
   int nsub;
-  int C[3], dx[3], col0[3], ucol[3], ccol[3];
+  int C[kMaxSub], dx[kMaxSub], col0[kMaxSub], ucol[kMaxSub], ccol[kMaxSub];
   int S, SC;            // centroid elements and clusters of one head
   int nwin, blocks;     // windows; blocks per (head, window)
   AccWindow win[kAccMaxWindows];
@@ -89,17 +90,39 @@ hipError_t km_accum(const AccPlan &plan, const void *x, bool bf16, size_t x_hs,
 hipError_t km_pack_codes(const int32_t *a3, size_t a_head_stride,
                          size_t a_sub_stride, int n, int heads,
                          uint32_t *codes, hipStream_t s);
+// Per-subspace codes of a general partition: z[h][m][j] = assign as uint16.
+hipError_t km_codes16(const int32_t *assign, size_t count, uint16_t *codes,
+                      hipStream_t s);
+// dst[r][t] = src[r][chan[t]] for rows r < rows (each of d elements of
+// elem_bytes = 2 or 4 bytes): the channels of a partition's sets, in order.
+struct ChannelMap {
+  int chan[128];
+};
+hipError_t gather_channels(const void *src, void *dst, size_t rows, int d,
+                           int elem_bytes, const ChannelMap &map, hipStream_t s);
 
+// Codebooks of the key subspaces: M sets, sizes c[0..M).  The logits read
+// codes packed as zT | zH << 10 | zW << 20 (M = 3, codes32) or one uint16
+// plane per subspace, [heads][M][n] (codes16).
+struct Subspaces {
+  int M;
+  int c[kMaxSub];
+};
+
+// Tables over the M channel ranges (off[m], len[m]) of the query centroids
+// (row stride d), one per subspace.
 hipError_t score_tables(int heads, int d, const int *off, const int *len,
-                        int c_q, const int *c_m, const float *qc,
+                        int c_q, const Subspaces &sub, const float *qc,
                         const float *kc, float *tables, hipStream_t s);
-hipError_t score_logits(int heads, int n, int d, int c_q, const int *c_m,
-                        const float *tables, const uint32_t *codes,
-                        float *scores, hipStream_t s);
+hipError_t score_logits(int heads, int n, int d, int c_q, const Subspaces &sub,
+                        const float *tables, const uint32_t *codes32,
+                        const uint16_t *codes16, float *scores, hipStream_t s);
 
-hipError_t select_run(int heads, int n, int c_q, const int *c_m, int d,
+constexpr int kSelMaxTable = 3072;    // LUT floats of one cluster row in LDS
+hipError_t select_run(int heads, int n, int c_q, const Subspaces &sub, int d,
                       const float *scores, const float *tables,
-                      const uint32_t *codes, const int32_t *counts, float rho,
+                      const uint32_t *codes32, const uint16_t *codes16,
+                      const int32_t *counts, float rho,
                       int k_fix, int32_t *base, int32_t *topp, int32_t *k_head,
                       int32_t *sel_counts, int32_t *sel_idx, float *row_max,
                       uint32_t *row_state, uint32_t *coarse_hist, int policy,

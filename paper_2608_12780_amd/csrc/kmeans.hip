@@ -7,7 +7,9 @@
 //           their centroid.
 // This file: initialisation, the VALU assignment, and the grouping of the
 // final query assignment (per-chunk cluster histograms -> column scan ->
-// stable scatter into the cluster-grouped permutation).
+// stable scatter into the cluster-grouped permutation);
+// also the packing of key codes and the channel gather of general key
+// partitions.
 #include <math.h>
 
 #include "common.h"
@@ -237,6 +239,22 @@ __global__ void km_pack_kernel(const int32_t *__restrict__ a3, size_t a_hs,
       (static_cast<uint32_t>(A[2 * a_ss + j]) << 20);
 }
 
+__global__ void km_codes16_kernel(const int32_t *__restrict__ a, size_t count,
+                                  uint16_t *codes) {
+  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i < count) codes[i] = static_cast<uint16_t>(a[i]);
+}
+
+template <typename T>
+__global__ void gather_channels_kernel(const T *__restrict__ src, T *dst,
+                                       size_t rows, int d, ChannelMap map) {
+  const size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= rows * d) return;
+  const size_t r = i / d;
+  const int t = static_cast<int>(i - r * d);
+  dst[i] = src[r * d + map.chan[t]];
+}
+
 template <typename T>
 hipError_t assign_dispatch(const KmProblem &p, bool with_hist, hipStream_t s) {
   const dim3 grid(km_nchunks(p.n), p.heads);
@@ -300,6 +318,30 @@ hipError_t km_pack_codes(const int32_t *a3, size_t a_head_stride,
                          uint32_t *codes, hipStream_t s) {
   hipLaunchKernelGGL(km_pack_kernel, dim3((n + 255) / 256, heads), dim3(256),
                      0, s, a3, a_head_stride, a_sub_stride, n, codes);
+  return hipGetLastError();
+}
+
+hipError_t km_codes16(const int32_t *assign, size_t count, uint16_t *codes,
+                      hipStream_t s) {
+  if (count == 0) return hipSuccess;
+  hipLaunchKernelGGL(km_codes16_kernel, dim3(static_cast<unsigned>((count + 255) / 256)),
+                     dim3(256), 0, s, assign, count, codes);
+  return hipGetLastError();
+}
+
+hipError_t gather_channels(const void *src, void *dst, size_t rows, int d,
+                           int elem_bytes, const ChannelMap &map, hipStream_t s) {
+  const size_t count = rows * d;
+  if (count == 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>((count + 255) / 256));
+  if (elem_bytes == 2)
+    hipLaunchKernelGGL(gather_channels_kernel<uint16_t>, grid, dim3(256), 0, s,
+                       static_cast<const uint16_t *>(src), static_cast<uint16_t *>(dst),
+                       rows, d, map);
+  else
+    hipLaunchKernelGGL(gather_channels_kernel<float>, grid, dim3(256), 0, s,
+                       static_cast<const float *>(src), static_cast<float *>(dst), rows,
+                       d, map);
   return hipGetLastError();
 }
 

@@ -206,7 +206,7 @@ bool km_accum_plan(int nsub, const int *col0, const int *dx, const int *C,
                    int heads, int n, AccPlan *plan) {
   AccPlan P{};
   if (plan) *plan = P;  // nwin == 0 marks a failed plan
-  if (nsub < 1 || nsub > 3) return false;
+  if (nsub < 1 || nsub > kMaxSub) return false;
   P.nsub = nsub;
   int S = 0, SC = 0;
   for (int m = 0; m < nsub; ++m) {

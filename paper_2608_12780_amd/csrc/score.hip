@@ -6,20 +6,27 @@
 
 namespace scope {
 
+static_assert(kCodeMaxSub == kMaxSub, "one bound on the number of subspaces");
+
 namespace {
 
 struct TableGeom {
-  int off[3], len[3], cm[3], col[3], ucol[3];  // ucol: float offset of U^m
+  int M;
+  int off[kMaxSub], len[kMaxSub];
+  int col[kMaxSub + 1];  // first table column of subspace m; col[M] = row length
+  int ucol[kMaxSub];     // float offset of U^m within a head's centroids
 };
 
 // P[h][c][col] = <qbar_c[I_m], u_r^m>, fp32 fma chain in channel order.
-__global__ void tables_kernel(int d, int c_q, int cs, int per_head, TableGeom g,
+__global__ void tables_kernel(int d, int c_q, int per_head, TableGeom g,
                               const float *__restrict__ qc,
                               const float *__restrict__ kc, float *tables) {
   const int col = blockIdx.x * blockDim.x + threadIdx.x;
   const int c = blockIdx.y, h = blockIdx.z;
+  const int cs = g.col[g.M];
   if (col >= cs) return;
-  const int m = col < g.col[1] ? 0 : (col < g.col[2] ? 1 : 2);
+  int m = 0;
+  while (m + 1 < g.M && col >= g.col[m + 1]) ++m;
   const int r = col - g.col[m];
   const float *q = qc + (static_cast<size_t>(h) * c_q + c) * d + g.off[m];
   const float *u = kc + static_cast<size_t>(h) * per_head + g.ucol[m] +
@@ -41,36 +48,58 @@ __global__ void logits_kernel(int n, int c_q, int cs, int cT, int cTH,
       proxy_logit(P, cT, cTH, cs, codes[static_cast<size_t>(h) * n + j], sigma);
 }
 
+__global__ void logits_planes_kernel(int n, int c_q, CodePlanes cp, float sigma,
+                                     const float *__restrict__ tables,
+                                     const uint16_t *__restrict__ codes,
+                                     float *scores) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  const int c = blockIdx.y, h = blockIdx.z;
+  if (j >= n) return;
+  const int cs = cp.col[cp.M];
+  const float *P = tables + (static_cast<size_t>(h) * c_q + c) * cs;
+  const uint16_t *planes = codes + static_cast<size_t>(h) * cp.M * n;
+  scores[(static_cast<size_t>(h) * c_q + c) * n + j] =
+      proxy_logit_planes(P, cp, planes, static_cast<size_t>(n), j, sigma);
+}
+
 }  // namespace
 
 hipError_t score_tables(int heads, int d, const int *off, const int *len,
-                        int c_q, const int *c_m, const float *qc,
+                        int c_q, const Subspaces &sub, const float *qc,
                         const float *kc, float *tables, hipStream_t s) {
-  TableGeom g;
+  TableGeom g{};
+  g.M = sub.M;
   int col = 0, ucol = 0;
-  for (int m = 0; m < 3; ++m) {
+  for (int m = 0; m < sub.M; ++m) {
     g.off[m] = off[m];
     g.len[m] = len[m];
-    g.cm[m] = c_m[m];
     g.col[m] = col;
     g.ucol[m] = ucol;
-    col += c_m[m];
-    ucol += c_m[m] * len[m];
+    col += sub.c[m];
+    ucol += sub.c[m] * len[m];
   }
-  const int cs = col;
-  hipLaunchKernelGGL(tables_kernel, dim3((cs + 127) / 128, c_q, heads),
-                     dim3(128), 0, s, d, c_q, cs, ucol, g, qc, kc, tables);
+  g.col[sub.M] = col;
+  hipLaunchKernelGGL(tables_kernel, dim3((col + 127) / 128, c_q, heads),
+                     dim3(128), 0, s, d, c_q, ucol, g, qc, kc, tables);
   return hipGetLastError();
 }
 
-hipError_t score_logits(int heads, int n, int d, int c_q, const int *c_m,
-                        const float *tables, const uint32_t *codes,
-                        float *scores, hipStream_t s) {
-  const int cs = c_m[0] + c_m[1] + c_m[2];
+hipError_t score_logits(int heads, int n, int d, int c_q, const Subspaces &sub,
+                        const float *tables, const uint32_t *codes32,
+                        const uint16_t *codes16, float *scores, hipStream_t s) {
   const float sigma = static_cast<float>(1.0 / sqrt(static_cast<double>(d)));
-  hipLaunchKernelGGL(logits_kernel, dim3((n + 255) / 256, c_q, heads),
-                     dim3(256), 0, s, n, c_q, cs, c_m[0], c_m[0] + c_m[1],
-                     sigma, tables, codes, scores);
+  const dim3 grid((n + 255) / 256, c_q, heads);
+  if (codes16) {
+    CodePlanes cp{};
+    cp.M = sub.M;
+    for (int m = 0; m < sub.M; ++m) cp.col[m + 1] = cp.col[m] + sub.c[m];
+    hipLaunchKernelGGL(logits_planes_kernel, grid, dim3(256), 0, s, n, c_q, cp,
+                       sigma, tables, codes16, scores);
+  } else {
+    const int cs = sub.c[0] + sub.c[1] + sub.c[2];
+    hipLaunchKernelGGL(logits_kernel, grid, dim3(256), 0, s, n, c_q, cs, sub.c[0],
+                       sub.c[0] + sub.c[1], sigma, tables, codes32, scores);
+  }
   return hipGetLastError();
 }
 

@@ -32,7 +32,7 @@ namespace {
 
 constexpr int kSelBlock = 1024;
 constexpr int kCoarseBins = kSelCoarseBins;
-constexpr int kMaxTable = 3072;
+constexpr int kMaxTable = kSelMaxTable;
 constexpr int kCand = 8192;      // logits of the crossing coarse bin held in LDS
 
 __device__ __forceinline__ int coarse_bin(float y) {
@@ -115,32 +115,45 @@ __device__ Crossing find_crossing(const uint32_t *hc, const uint64_t *hm,
   return out;
 }
 
-template <bool FUSED>
+// Where a cluster row's logits come from: the materialised scores, or the
+// table row (staged in LDS) and the key codes, packed (three subspaces) or
+// one uint16 plane per subspace.
+constexpr int kFromScores = 0, kFromPacked = 1, kFromPlanes = 2;
+
+struct CodeBooks {
+  const uint32_t *packed;  // [heads][n], KIND == kFromPacked
+  const uint16_t *planes;  // [heads][M][n], KIND == kFromPlanes
+  CodePlanes cp;           // M and the table columns of each subspace
+};
+
+template <int KIND>
 struct LogitSource {
-  const float *P;        // LDS table row (fused) or global score row
-  const uint32_t *codes; // [n] of this head
-  int cT, cTH, cs;
+  const float *P;          // LDS table row or global score row
+  const uint32_t *packed;  // codes of this head
+  const uint16_t *planes;
+  CodePlanes cp;
+  size_t n;
   float sigma;
   __device__ __forceinline__ float operator()(int j) const {
-    if (FUSED) return proxy_logit(P, cT, cTH, cs, codes[j], sigma);
-    return P[j];
+    if (KIND == kFromScores) return P[j];
+    if (KIND == kFromPacked)
+      return proxy_logit(P, cp.col[1], cp.col[2], cp.col[3], packed[j], sigma);
+    return proxy_logit_planes(P, cp, planes, n, j, sigma);
   }
 };
 
-template <bool FUSED>
-__device__ LogitSource<FUSED> make_source(float *lut, int h, int c, int n,
-                                          int c_q, const int *cm, float sigma,
-                                          const float *scores,
-                                          const float *tables,
-                                          const uint32_t *codes) {
-  LogitSource<FUSED> src;
-  src.cT = cm[0];
-  src.cTH = cm[0] + cm[1];
-  src.cs = cm[0] + cm[1] + cm[2];
+template <int KIND>
+__device__ LogitSource<KIND> make_source(float *lut, int h, int c, int n, int c_q,
+                                         const CodeBooks &cb, float sigma,
+                                         const float *scores, const float *tables) {
+  LogitSource<KIND> src;
+  src.cp = cb.cp;
+  src.n = static_cast<size_t>(n);
   src.sigma = sigma;
-  src.codes = codes + static_cast<size_t>(h) * n;
-  if (FUSED) {
-    const int cs = cm[0] + cm[1] + cm[2];
+  src.packed = cb.packed ? cb.packed + static_cast<size_t>(h) * n : nullptr;
+  src.planes = cb.planes ? cb.planes + static_cast<size_t>(h) * cb.cp.M * n : nullptr;
+  if (KIND != kFromScores) {
+    const int cs = cb.cp.col[cb.cp.M];
     const float *row = tables + (static_cast<size_t>(h) * c_q + c) * cs;
     for (int e = threadIdx.x; e < cs; e += kSelBlock) lut[e] = row[e];
     __syncthreads();
@@ -150,10 +163,6 @@ __device__ LogitSource<FUSED> make_source(float *lut, int h, int c, int n,
   }
   return src;
 }
-
-struct Cm3 {
-  int v[3];
-};
 
 // Radix refinement inside one coarse bin: three digit passes over the
 // order-preserving key of every logit the source visits (all keys of the
@@ -198,8 +207,8 @@ __device__ void refine(Visit visit, float M, uint64_t target, uint32_t *hc,
 // Gathers the logits of coarse bin `cbin` into cand (one LDS slot per key,
 // reserved per wave); returns how many there are (more than kCand: the
 // list is incomplete and the caller visits all keys instead).
-template <bool FUSED>
-__device__ int gather_bin(const LogitSource<FUSED> &src, int n, float M, int cbin,
+template <int KIND>
+__device__ int gather_bin(const LogitSource<KIND> &src, int n, float M, int cbin,
                           float *cand, int *ncand) {
   if (threadIdx.x == 0) *ncand = 0;
   __syncthreads();
@@ -231,12 +240,12 @@ __device__ int gather_bin(const LogitSource<FUSED> &src, int n, float M, int cbi
 
 // Exact crossing key inside coarse bin `cbin`: over the gathered list when
 // it is complete, else over all keys.
-template <bool FUSED, bool BY_MASS>
-__device__ void refine_bin(const LogitSource<FUSED> &src, int n, float M, int cbin,
+template <int KIND, bool BY_MASS>
+__device__ void refine_bin(const LogitSource<KIND> &src, int n, float M, int cbin,
                            uint64_t target, uint32_t *hc, uint64_t *hm, float *cand,
                            int *ncand, uint32_t *key_out, uint32_t *cnt_above,
                            uint64_t *mass_above) {
-  const int cnt = gather_bin<FUSED>(src, n, M, cbin, cand, ncand);
+  const int cnt = gather_bin<KIND>(src, n, M, cbin, cand, ncand);
   if (cnt <= kCand) {
     refine<BY_MASS>([&](auto f) {
       for (int k = threadIdx.x; k < cnt; k += kSelBlock) f(cand[k]);
@@ -251,11 +260,10 @@ __device__ void refine_bin(const LogitSource<FUSED> &src, int n, float M, int cb
   }
 }
 
-template <bool FUSED>
+template <int KIND>
 __global__ __launch_bounds__(kSelBlock) void select_base_kernel(
-    int n, int c_q, Cm3 cm, float sigma, const float *__restrict__ scores,
-    const float *__restrict__ tables, const uint32_t *__restrict__ codes,
-    float rho, int k_fix, int32_t *base_counts, int32_t *topp_counts,
+    int n, int c_q, CodeBooks cb, float sigma, const float *__restrict__ scores,
+    const float *__restrict__ tables, float rho, int k_fix, int32_t *base_counts, int32_t *topp_counts,
     float *row_max, uint32_t *row_state, uint32_t *coarse_hist) {
   __shared__ float lut[kMaxTable];
   __shared__ uint32_t hc[kCoarseBins];
@@ -264,8 +272,8 @@ __global__ __launch_bounds__(kSelBlock) void select_base_kernel(
   __shared__ int ncand;
   const int c = blockIdx.x, h = blockIdx.y;
   const size_t row = static_cast<size_t>(h) * c_q + c;
-  const LogitSource<FUSED> src =
-      make_source<FUSED>(lut, h, c, n, c_q, cm.v, sigma, scores, tables, codes);
+  const LogitSource<KIND> src =
+      make_source<KIND>(lut, h, c, n, c_q, cb, sigma, scores, tables);
   float mloc = -INFINITY;
   for (int j = threadIdx.x; j < n; j += kSelBlock) mloc = fmaxf(mloc, src(j));
   const float M = block_max(mloc);
@@ -296,7 +304,7 @@ __global__ __launch_bounds__(kSelBlock) void select_base_kernel(
     const Crossing x = find_crossing<true>(hc, hm, kCoarseBins, 0, T);
     uint32_t cnt_above = x.cnt_before;
     uint64_t mass_above = x.mass_before;
-    refine_bin<FUSED, true>(src, n, M, x.bin, T, hc, hm, cand, &ncand, &key_star,
+    refine_bin<KIND, true>(src, n, M, x.bin, T, hc, hm, cand, &ncand, &key_star,
                             &cnt_above, &mass_above);
     const float s_star = desc_key_value(key_star);
     const uint64_t e_star = fixexp(s_star - M);
@@ -339,11 +347,10 @@ __global__ __launch_bounds__(kSelBlock) void select_head_kernel(
   }
 }
 
-template <bool FUSED>
+template <int KIND>
 __global__ __launch_bounds__(kSelBlock) void select_final_kernel(
-    int n, int c_q, Cm3 cm, float sigma, const float *__restrict__ scores,
-    const float *__restrict__ tables, const uint32_t *__restrict__ codes,
-    const int32_t *__restrict__ sel_counts, const float *__restrict__ row_max,
+    int n, int c_q, CodeBooks cb, float sigma, const float *__restrict__ scores,
+    const float *__restrict__ tables, const int32_t *__restrict__ sel_counts, const float *__restrict__ row_max,
     const uint32_t *__restrict__ row_state,
     const uint32_t *__restrict__ coarse_hist, int32_t *sel_idx) {
   __shared__ float lut[kMaxTable];
@@ -359,8 +366,8 @@ __global__ __launch_bounds__(kSelBlock) void select_final_kernel(
     return;
   }
   if (r <= 0) return;
-  const LogitSource<FUSED> src =
-      make_source<FUSED>(lut, h, c, n, c_q, cm.v, sigma, scores, tables, codes);
+  const LogitSource<KIND> src =
+      make_source<KIND>(lut, h, c, n, c_q, cb, sigma, scores, tables);
   const float M = row_max[row];
   uint32_t key_r, above;
   if (static_cast<uint32_t>(r) == row_state[4 * row + 0]) {
@@ -375,7 +382,7 @@ __global__ __launch_bounds__(kSelBlock) void select_final_kernel(
                                             static_cast<uint64_t>(r));
     above = x.cnt_before;
     uint64_t unused = 0;
-    refine_bin<FUSED, false>(src, n, M, x.bin, static_cast<uint64_t>(r), hc, nullptr,
+    refine_bin<KIND, false>(src, n, M, x.bin, static_cast<uint64_t>(r), hc, nullptr,
                              cand, &ncand, &key_r, &above, &unused);
   }
   // ordered compaction, four consecutive keys per thread: keys above key_r
@@ -419,38 +426,43 @@ __global__ void fixexp_kernel(const float *y, uint64_t *out, int64_t count) {
 
 }  // namespace
 
-hipError_t select_run(int heads, int n, int c_q, const int *c_m, int d,
+hipError_t select_run(int heads, int n, int c_q, const Subspaces &sub, int d,
                       const float *scores, const float *tables,
-                      const uint32_t *codes, const int32_t *counts, float rho,
-                      int k_fix, int32_t *base, int32_t *topp, int32_t *k_head,
-                      int32_t *sel_counts, int32_t *sel_idx, float *row_max,
-                      uint32_t *row_state, uint32_t *coarse_hist, int policy,
-                      hipStream_t s) {
-  Cm3 cm{{c_m[0], c_m[1], c_m[2]}};
+                      const uint32_t *codes32, const uint16_t *codes16,
+                      const int32_t *counts, float rho, int k_fix, int32_t *base,
+                      int32_t *topp, int32_t *k_head, int32_t *sel_counts,
+                      int32_t *sel_idx, float *row_max, uint32_t *row_state,
+                      uint32_t *coarse_hist, int policy, hipStream_t s) {
+  CodeBooks cb{};
+  cb.packed = codes32;
+  cb.planes = codes16;
+  cb.cp.M = sub.M;
+  for (int m = 0; m < sub.M; ++m) cb.cp.col[m + 1] = cb.cp.col[m] + sub.c[m];
+  const int kind = scores ? kFromScores : codes16 ? kFromPlanes : kFromPacked;
   const float sigma = static_cast<float>(1.0 / sqrt(static_cast<double>(d)));
   const dim3 grid(c_q, heads), block(kSelBlock);
-  if (scores)
-    hipLaunchKernelGGL(select_base_kernel<false>, grid, block, 0, s, n, c_q, cm,
-                       sigma, scores, tables, codes, rho, k_fix, base, topp,
-                       row_max, row_state, coarse_hist);
-  else
-    hipLaunchKernelGGL(select_base_kernel<true>, grid, block, 0, s, n, c_q, cm,
-                       sigma, scores, tables, codes, rho, k_fix, base, topp,
-                       row_max, row_state, coarse_hist);
+#define SCOPE_SEL_BASE(K)                                                          \
+  hipLaunchKernelGGL(select_base_kernel<K>, grid, block, 0, s, n, c_q, cb, sigma,  \
+                     scores, tables, rho, k_fix, base, topp, row_max, row_state, \
+                     coarse_hist)
+#define SCOPE_SEL_FINAL(K)                                                         \
+  hipLaunchKernelGGL(select_final_kernel<K>, grid, block, 0, s, n, c_q, cb, sigma, \
+                     scores, tables, sel_counts, row_max, row_state, coarse_hist, \
+                     sel_idx)
+  if (kind == kFromScores) SCOPE_SEL_BASE(kFromScores);
+  else if (kind == kFromPacked) SCOPE_SEL_BASE(kFromPacked);
+  else SCOPE_SEL_BASE(kFromPlanes);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(select_head_kernel, dim3(heads), block, 0, s, c_q, counts,
                      base, row_state, policy, k_head, sel_counts);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (scores)
-    hipLaunchKernelGGL(select_final_kernel<false>, grid, block, 0, s, n, c_q, cm,
-                       sigma, scores, tables, codes, sel_counts, row_max,
-                       row_state, coarse_hist, sel_idx);
-  else
-    hipLaunchKernelGGL(select_final_kernel<true>, grid, block, 0, s, n, c_q, cm,
-                       sigma, scores, tables, codes, sel_counts, row_max,
-                       row_state, coarse_hist, sel_idx);
+  if (kind == kFromScores) SCOPE_SEL_FINAL(kFromScores);
+  else if (kind == kFromPacked) SCOPE_SEL_FINAL(kFromPacked);
+  else SCOPE_SEL_FINAL(kFromPlanes);
+#undef SCOPE_SEL_BASE
+#undef SCOPE_SEL_FINAL
   return hipGetLastError();
 }
 

@@ -14,7 +14,8 @@ from . import binding as B
 
 class ScopeLayer:
     def __init__(self, heads, n, d, ranges, c_q, c_m, iters, rho, k_fix,
-                 dtype="bf16", device="cuda", materialize_scores=False):
+                 dtype="bf16", device="cuda", materialize_scores=False,
+                 workspace=True):
         self.heads, self.n, self.d = int(heads), int(n), int(d)
         self.ranges = (tuple(map(int, ranges[0])), tuple(map(int, ranges[1])))
         self.c_q = int(c_q)
@@ -43,7 +44,8 @@ class ScopeLayer:
         self.sel_counts = torch.empty(H, C, **i32)
         self.sel_idx = torch.empty(H, C, N, **i32)
         self.out = torch.empty(H, N, D, dtype=self.tdtype, device=device)
-        self.workspace = B.alloc_workspace(self.shape, C, self.c_m, device)
+        self.workspace = (B.alloc_workspace(self.shape, C, self.c_m, device)
+                          if workspace else None)
         self.status = torch.zeros(1, **i32)
 
     # the five stages -------------------------------------------------------
@@ -102,6 +104,57 @@ class ScopeLayer:
         return self.out
 
 
+def _dummy_ranges(d):
+    """Three valid ranges for the calls that check but do not use them."""
+    a = d // 3 // 2 * 2
+    ln = (a, a, d - 2 * a)
+    return (0, ln[0], ln[0] + ln[1]), ln
+
+
+class ScopePartitionLayer(ScopeLayer):
+    """The layer with the keys split into any M disjoint channel sets (App. B;
+    the partition ablation of Table 3), through the partition calls: codes
+    are one uint16 plane per subspace (held in an int16 tensor)."""
+
+    def __init__(self, heads, n, d, sets, c_q, c_m, iters, rho, k_fix,
+                 dtype="bf16", device="cuda", materialize_scores=False):
+        self.sets = [tuple(map(int, x)) for x in sets]
+        self.part = B.make_partition(self.sets, c_m)
+        M = len(self.sets)
+        # the query and attention calls see three placeholder ranges
+        super().__init__(heads, n, d, _dummy_ranges(d), c_q, (1, 1, 1), iters,
+                         rho, k_fix, dtype, device, materialize_scores,
+                         workspace=False)
+        self.c_m = tuple(int(c) for c in c_m)
+        H, N, C = self.heads, self.n, self.c_q
+        per_head = sum(self.c_m[m] * len(self.sets[m]) for m in range(M))
+        self.k_centroids = torch.empty(H, per_head, dtype=torch.float32, device=device)
+        self.codes = torch.empty(H, M, N, dtype=torch.int16, device=device)
+        self.tables = torch.empty(H, C, sum(self.c_m), dtype=torch.float32, device=device)
+        self.workspace = B.alloc_partition_workspace(self.shape, C, self.part, device)
+
+    def cluster_keys(self, k, init_k=None, stream=None):
+        stride = init_k.shape[-1] if init_k is not None else 0
+        B.scope_cluster_key_partition(self.shape, k, self.part, self.iters, init_k,
+                                      stride, self.k_centroids, self.codes,
+                                      self.workspace, self.status, stream)
+
+    def proxy_scores(self, stream=None):
+        B.scope_proxy_scores_partition(self.shape, self.q_centroids, self.c_q,
+                                       self.k_centroids, self.part, self.codes,
+                                       self.tables, self.scores, self.workspace,
+                                       stream)
+
+    def select(self, stream=None, use_scores=False, policy="online", rho=None):
+        rho = self.rho if rho is None else rho
+        B.scope_select_partition(self.shape, self.c_q, self.part,
+                                 self.scores if use_scores else None, self.tables,
+                                 self.codes, self.counts, rho, self.k_fix,
+                                 self.base_counts, self.topp_counts, self.k_head,
+                                 self.sel_counts, self.sel_idx, self.workspace,
+                                 policy, stream)
+
+
 class DenseAttention:
     """Dense attention (Eq. 1) through the same attention call: one cluster
     holding every query, whose key set is every key."""
@@ -110,10 +163,7 @@ class DenseAttention:
         self.heads, self.n, self.d = int(heads), int(n), int(d)
         self.dtype = B.BF16 if dtype == "bf16" else B.F32
         tdt = torch.bfloat16 if self.dtype == B.BF16 else torch.float32
-        split = (d // 3 // 2 * 2, d // 3 // 2 * 2)
-        ln = (split[0], split[1], d - split[0] - split[1])
-        self.shape = B.make_shape(heads, n, d, self.dtype,
-                                  ((0, ln[0], ln[0] + ln[1]), ln))
+        self.shape = B.make_shape(heads, n, d, self.dtype, _dummy_ranges(d))
         i32 = dict(dtype=torch.int32, device=device)
         H, N = self.heads, self.n
         self.offsets = torch.tensor([0, N], **i32).repeat(H, 1).contiguous()

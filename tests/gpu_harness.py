@@ -10,7 +10,7 @@ import torch
 
 import oracle
 from paper_2608_12780_amd import inputs
-from paper_2608_12780_amd.layer import DenseAttention, ScopeLayer
+from paper_2608_12780_amd.layer import DenseAttention, ScopeLayer, ScopePartitionLayer
 
 # Attention tolerance (bf16 matrix products, fp32 softmax): max |o - ref| and
 # sum |o - ref| / sum |ref| over the compared elements.
@@ -45,10 +45,18 @@ def make_layer(cfg: inputs.LayerConfig, heads=None, materialize=True, **over):
     return ScopeLayer(**a)
 
 
-def run_gpu(layer: ScopeLayer, x: inputs.LayerInputs, use_scores=False, policy="online"):
+def make_partition_layer(cfg: inputs.LayerConfig, sets, c_m, heads=None,
+                         materialize=True):
+    return ScopePartitionLayer(cfg.heads if heads is None else heads, cfg.n, cfg.d,
+                               sets, cfg.c_q, c_m, cfg.iters, cfg.rho, cfg.k_fix,
+                               cfg.dtype, materialize_scores=materialize)
+
+
+def run_gpu(layer: ScopeLayer, x: inputs.LayerInputs, use_scores=False, policy="online",
+            init_k=None):
     q, k, v = to_device(x)
     iq = torch.from_numpy(x.init_q).cuda()
-    ik = torch.from_numpy(x.init_k).cuda()
+    ik = torch.from_numpy(x.init_k if init_k is None else init_k).cuda()
     layer.cluster_queries(q, iq)
     layer.cluster_keys(k, ik)
     layer.proxy_scores()
@@ -59,11 +67,16 @@ def run_gpu(layer: ScopeLayer, x: inputs.LayerInputs, use_scores=False, policy="
     return dict(centroids=g(layer.q_centroids), assign=g(layer.assign),
                 counts=g(layer.counts), offsets=g(layer.offsets),
                 perm=g(layer.perm), k_centroids=g(layer.k_centroids),
-                codes=g(layer.codes).view(np.uint32), tables=g(layer.tables),
+                codes=_codes(g(layer.codes)), tables=g(layer.tables),
                 scores=g(layer.scores), base=g(layer.base_counts),
                 topp=g(layer.topp_counts), k_head=g(layer.k_head),
                 sel_counts=g(layer.sel_counts), sel_idx=g(layer.sel_idx),
                 out=layer.out.float().cpu().numpy(), status=int(layer.status.item()))
+
+
+def _codes(c):
+    # packed composite codes (int32 storage) or uint16 planes (int16 storage)
+    return c.view(np.uint16) if c.dtype == np.int16 else c.view(np.uint32)
 
 
 def oracle_all(x: inputs.LayerInputs, c_q, c_m, iters, rho, k_fix, policy="online"):

@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
     L = B.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert L.scope_abi_version() == 1
+    assert L.scope_abi_version() == 2
 
 
 def test_status_strings():
@@ -161,3 +161,74 @@ def test_binding_rejects_host_tensors():
     q = torch.zeros(64, 64, dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         B.scope_cluster_queries(sh, q, 8, 2, None, q, q, q, q, q, q)
+
+
+def part(sets=None, c=None):
+    sets = sets if sets is not None else [range(0, 16), range(16, 72), range(72, 128)]
+    c = c if c is not None else [333] * len(sets)
+    return B.make_partition(sets, c)
+
+
+def part_ws(shape, p, c_q=300):
+    out = ctypes.c_size_t(0)
+    st = B.lib().scope_partition_workspace_size(ctypes.byref(shape), c_q, ctypes.byref(p),
+                                                ctypes.byref(out))
+    return st, out.value
+
+
+def test_partition_workspace_and_validation():
+    sh = hy_shape()
+    st, in_order = part_ws(sh, part())
+    assert st == OK and in_order % 256 == 0
+    # reordered channels: a copy of K (heads * n * d bf16) on top
+    rnd = [sorted(range(0, 128, 3)), sorted(set(range(128)) - set(range(0, 128, 3)))]
+    st, reordered = part_ws(sh, part(rnd, [333, 333]))
+    assert st == OK and reordered >= 24 * 118800 * 128 * 2
+    # the shape's ranges are not used by the partition calls
+    assert part_ws(hy_shape(ranges=((0, 0, 0), (0, 0, 0))), part())[0] == OK
+    bad = [
+        (part([range(0, 64), range(63, 127)]), INVALID),              # overlap
+        (part([range(0, 64), range(64, 127)]), INVALID),              # channel 127 missing
+        (part([[1, 0] + list(range(2, 64)), range(64, 128)]), INVALID),  # not ascending
+        (part([range(0, 64), range(64, 128)], [333, 0]), INVALID),
+        (part([range(0, 64), range(64, 128)], [333, 1025]), UNSUPPORTED),
+        (part([range(16 * m, 16 * m + 16) for m in range(8)], [400] * 8), UNSUPPORTED),  # LUT
+    ]
+    for p, want in bad:
+        assert part_ws(sh, p)[0] == want
+    p = part([range(16 * m, 16 * m + 16) for m in range(8)], [384] * 8)
+    assert part_ws(sh, p)[0] == OK
+    p.m = 9
+    assert part_ws(sh, p)[0] == UNSUPPORTED
+    p.m = 0
+    assert part_ws(sh, p)[0] == INVALID
+    assert B.lib().scope_partition_workspace_size(ctypes.byref(sh), 300, None,
+                                                  ctypes.byref(ctypes.c_size_t())) == INVALID
+
+
+def test_partition_calls_validation():
+    L, sh, p = B.lib(), hy_shape(), part()
+    def keys(iters=10, init=None, stride=0, ws=FAKE, ws_bytes=1 << 40, pp=p):
+        return L.scope_cluster_key_partition(ctypes.byref(sh), FAKE, ctypes.byref(pp) if pp else None,
+                                             iters, init, stride, FAKE, FAKE, ws, ws_bytes,
+                                             None, None)
+    assert keys(iters=0) == INVALID
+    assert keys(pp=None) == INVALID
+    assert keys(init=FAKE, stride=100) == INVALID              # stride < max c
+    assert keys(ws=None) == WORKSPACE
+    assert keys(ws_bytes=1000) == WORKSPACE
+    def scores(ws=None, ws_bytes=0, pp=p, codes=FAKE, sc=FAKE):
+        return L.scope_proxy_scores_partition(ctypes.byref(sh), FAKE, 300, FAKE,
+                                              ctypes.byref(pp), codes, FAKE, sc, ws,
+                                              ws_bytes, None)
+    assert scores(codes=None) == INVALID                        # scores need codes
+    rnd = part([sorted(range(0, 128, 2)), sorted(range(1, 128, 2))], [64, 64])
+    assert scores(pp=rnd) == WORKSPACE                          # reordering needs it
+    def select(policy=0, rho=0.9, tables=FAKE, codes=FAKE, ws=FAKE):
+        return L.scope_select_partition(ctypes.byref(sh), 300, ctypes.byref(p), None, tables,
+                                        codes, FAKE, rho, 11880, FAKE, None, FAKE, FAKE,
+                                        FAKE, ws, 1 << 40, policy, None)
+    assert select(policy=3) == INVALID
+    assert select(rho=0.0) == INVALID
+    assert select(codes=None) == INVALID
+    assert select(ws=None) == WORKSPACE

@@ -133,8 +133,11 @@ def test_selection_from_materialised_scores_is_identical():
     x = inputs.generate(cfg)
     a = G.run_gpu(G.make_layer(cfg), x, use_scores=False)
     b = G.run_gpu(G.make_layer(cfg), x, use_scores=True)
-    for key in ("base", "topp", "k_head", "sel_counts", "sel_idx", "out"):
+    for key in ("base", "topp", "k_head", "sel_counts", "out"):
         assert np.array_equal(a[key], b[key]), key
+    r = a["sel_counts"]
+    for h, c in np.ndindex(r.shape):
+        assert np.array_equal(a["sel_idx"][h, c, :r[h, c]], b["sel_idx"][h, c, :r[h, c]])
 
 
 def test_layer_is_deterministic():
@@ -215,3 +218,69 @@ def test_dense_mode_matches_oracle(d, n):
     ref = oracle.dense_attention(*qkv)
     mx, mr = G.assert_attention_close(out, ref)
     G.say(f"[parity] dense d={d} n={n}: max-abs {mx:.3e} mean-rel {mr:.3e}")
+
+
+def _partition_case(cfg, kind, c_m, seed=1):
+    x = inputs.generate(cfg)
+    sets = inputs.partition_sets(cfg, kind, seed)
+    M = len(sets)
+    init_k = (x.init_k if kind == "3-rope" and max(c_m) <= cfg.c_m
+              else inputs.partition_init(cfg, M, max(c_m)))
+    G.say(f"[parity] partition {kind}: M={M} c_m={list(c_m)} sizes={[len(s) for s in sets]}")
+    gpu = G.run_gpu(G.make_partition_layer(cfg, sets, c_m), x, init_k=init_k)
+    ref = oracle.layer_partition(x.q, x.k, x.v, sets, cfg.c_q, c_m, cfg.iters, x.init_q,
+                                 init_k, cfg.rho, cfg.k_fix)
+    assert gpu["status"] == 0
+    assert np.array_equal(gpu["perm"], ref["q"]["perm"])
+    assert np.array_equal(gpu["codes"], ref["k"]["codes"])
+    assert np.array_equal(gpu["k_centroids"].view(np.uint32),
+                          ref["k"]["centroids"].view(np.uint32))
+    assert np.array_equal(gpu["tables"].view(np.uint32), ref["tables"].view(np.uint32))
+    assert np.array_equal(gpu["scores"].view(np.uint32), ref["scores"].view(np.uint32))
+    G.assert_same_selection(gpu, ref["sel"])
+    qr, kr, vr = (G.bf16_round(a) for a in (x.q, x.k, x.v))
+    att = oracle.attention(qr, kr, vr, ref["q"]["offsets"], ref["q"]["perm"],
+                           ref["sel"]["sel_counts"], ref["sel"]["sel_idx"])
+    mx, mr = G.assert_attention_close(gpu["out"], att)
+    G.say(f"[parity] partition {kind}: attention max-abs {mx:.3e} mean-rel {mr:.3e}")
+    return gpu, x
+
+
+@pytest.mark.parametrize("kind,c_m", [
+    ("1", (40,)), ("2", (16, 24)), ("3-random", (20, 40, 33)), ("3-rope", (16, 16, 16)),
+    ("4", (16,) * 4), ("8", (5, 9, 16, 33, 7, 12, 16, 3)), ("1", (333,)),
+])
+def test_key_partitions_of_the_ablation(kind, c_m):
+    # Table 3 variants: any disjoint channel sets, M <= 8, codebooks of any
+    # size (C = 333 at d = 128 takes the fp32 VALU assignment)
+    _partition_case(MID_HY, kind, c_m)
+
+
+def test_rope_partition_equals_the_three_range_calls():
+    cfg = MID_HY
+    gpu_p, x = _partition_case(cfg, "3-rope", (cfg.c_m,) * 3)
+    gpu_r = G.run_gpu(G.make_layer(cfg), x)
+    packed = gpu_r["codes"]
+    planes = np.stack([(packed >> (10 * m)) & 1023 for m in range(3)], 1).astype(np.uint16)
+    assert np.array_equal(gpu_p["codes"], planes)
+    for key in ("k_centroids", "tables", "scores", "sel_counts", "out"):
+        assert np.array_equal(gpu_p[key], gpu_r[key]), key
+    # entries past r_c are left untouched by selection
+    r = gpu_r["sel_counts"]
+    for h, c in np.ndindex(r.shape):
+        assert np.array_equal(gpu_p["sel_idx"][h, c, :r[h, c]], gpu_r["sel_idx"][h, c, :r[h, c]])
+
+
+def test_partition_selection_from_codes_equals_from_scores():
+    cfg = MID_WAN
+    x = inputs.generate(cfg)
+    sets = inputs.partition_sets(cfg, "3-random", 2)
+    init_k = inputs.partition_init(cfg, 3, cfg.c_m)
+    a = G.run_gpu(G.make_partition_layer(cfg, sets, (cfg.c_m,) * 3), x, init_k=init_k)
+    b = G.run_gpu(G.make_partition_layer(cfg, sets, (cfg.c_m,) * 3), x, use_scores=True,
+                  init_k=init_k)
+    for key in ("base", "topp", "k_head", "sel_counts", "out"):
+        assert np.array_equal(a[key], b[key]), key
+    r = a["sel_counts"]
+    for h, c in np.ndindex(r.shape):
+        assert np.array_equal(a["sel_idx"][h, c, :r[h, c]], b["sel_idx"][h, c, :r[h, c]])
