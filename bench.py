@@ -299,6 +299,90 @@ def policy_study(config_name="hy720", heads=4):
             "heads": heads, "n": cfg.n, "target_density": round(target, 5), "rows": rows}
 
 
+def partition_study(config_name="hy720", heads=4, c_q=300, c_m=333, reps=2,
+                    sample=256):
+    """The key-partition ablation (Table 3) on synthetic inputs: every
+    partition (full-dimensional, 2, random 3-way, RoPE 3-way, 4 and 8 equal
+    ranges) at the paper's C_q = 300 and C_m = 333 per subspace, the same
+    rho and k_fix.  Per partition: stage and layer latency (HIP events), the
+    realised density, the share of the exact softmax mass each sampled query
+    keeps (attention recall), and the output's relative L2 error against
+    dense attention on the same heads."""
+    import torch
+    from paper_2608_12780_amd import inputs
+    from paper_2608_12780_amd.layer import DenseAttention, ScopeLayer, ScopePartitionLayer
+    cfg = inputs.CONFIGS[config_name].with_(c_q=c_q, c_m=c_m)
+    x = inputs.generate(cfg.with_(heads=heads))
+    dev = torch.device("cuda", 0)
+    up = lambda b: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
+    q, k, v = up(x.q_bits), up(x.k_bits), up(x.v_bits)
+    iq = torch.from_numpy(x.init_q).to(dev)
+    dense = DenseAttention(heads, cfg.n, cfg.d, cfg.dtype, dev)
+    ref = dense.forward(q, k, v).float()
+    torch.cuda.synchronize()
+    del dense
+    rng = np.random.default_rng(cfg.seed)
+    rows_q = torch.from_numpy(rng.choice(cfg.n, size=(heads, sample), replace=False)).to(dev)
+    scale = 1.0 / math.sqrt(cfg.d)
+    stream = torch.cuda.current_stream()
+    names = ["cluster_queries", "cluster_keys", "proxy_scores", "select", "sparse_attention"]
+
+    def measure(layer, init_k, label, M):
+        layer.forward(q, k, v, iq, init_k)
+        torch.cuda.synchronize()
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(reps)]
+        for i in range(reps):
+            layer.forward(q, k, v, iq, init_k, marks=lambda j, i=i: ev[i][j].record(stream))
+        torch.cuda.synchronize()
+        st = {n_: float(np.mean([ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(reps)]))
+              for j, n_ in enumerate(names)}
+        total = float(np.mean([ev[i][0].elapsed_time(ev[i][5]) for i in range(reps)]))
+        counts = layer.counts.double()
+        dens = float((counts * layer.sel_counts.double()).sum()) / (heads * float(cfg.n) ** 2)
+        err = layer.out.float() - ref
+        # attention recall: softmax mass of each sampled query on its key set
+        rec = []
+        cl = layer.assign.long()
+        for h in range(heads):
+            qi = rows_q[h]
+            p_ = torch.softmax((q[h, qi].float() @ k[h].float().T) * scale, dim=1)
+            c_ = cl[h, qi]
+            r_ = layer.sel_counts[h, c_].long()
+            idx = layer.sel_idx[h, c_].long()
+            keep = torch.arange(cfg.n, device=dev)[None, :] < r_[:, None]
+            mass = torch.gather(p_, 1, idx.clamp(0, cfg.n - 1)) * keep
+            rec.append(mass.sum(1))
+        rec = torch.cat(rec)
+        row = {"partition": label, "M": M, "layer_ms": round(total, 3),
+               "stages_ms": {n_: round(t_, 3) for n_, t_ in st.items()},
+               "density": round(dens, 5), "k_head_mean": float(layer.k_head.double().mean()),
+               "attention_recall_mean": round(float(rec.mean()), 5),
+               "attention_recall_p5": round(float(torch.quantile(rec, 0.05)), 5),
+               "rel_l2_vs_dense": float(err.norm() / ref.norm())}
+        log(f"[partition] {row}")
+        return row
+
+    rows = []
+    for kind in inputs.PARTITIONS:
+        sets = inputs.partition_sets(cfg, kind)
+        M = len(sets)
+        init_k = torch.from_numpy(inputs.partition_init(cfg, M, c_m, heads)).to(dev)
+        layer = ScopePartitionLayer(heads, cfg.n, cfg.d, sets, c_q, (c_m,) * M, cfg.iters,
+                                    cfg.rho, cfg.k_fix, dtype=cfg.dtype, device=dev)
+        rows.append(measure(layer, init_k, kind, M))
+        del layer
+        torch.cuda.empty_cache()
+    # the same RoPE partition through the three-range calls (packed codes)
+    init3 = torch.from_numpy(inputs.partition_init(cfg, 3, c_m, heads)).to(dev)
+    layer = ScopeLayer(heads, cfg.n, cfg.d, cfg.ranges, c_q, (c_m,) * 3, cfg.iters, cfg.rho,
+                       cfg.k_fix, dtype=cfg.dtype, device=dev)
+    rows.append(measure(layer, init3, "3-rope (range calls)", 3))
+    return {"study": "key partitions (Table 3 analogue)",
+            "workload": WORKLOAD_NAMES.get(cfg.name), "heads": heads, "n": cfg.n,
+            "c_q": c_q, "c_m": c_m, "rho": cfg.rho, "k_fix": cfg.k_fix,
+            "sampled_queries_per_head": sample, "rows": rows}
+
+
 def cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -414,6 +498,9 @@ def main():
         return
     if len(sys.argv) >= 2 and sys.argv[1] == "--traffic-probe":
         traffic_probe()
+        return
+    if len(sys.argv) >= 2 and sys.argv[1] == "--partition-study":
+        print(json.dumps(partition_study()), flush=True)
         return
     if len(sys.argv) >= 2 and sys.argv[1] == "--policy-study":
         print(json.dumps(policy_study()), flush=True)

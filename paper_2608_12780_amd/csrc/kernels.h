@@ -35,7 +35,7 @@ struct KmProblem {
 };
 
 // Whether the matrix-core assignment applies: bf16 rows at even offsets and
-// a bf16 codebook that fits the kernel's LDS.
+// at most 1024 centroids (codebooks beyond the LDS are streamed in chunks).
 bool km_mfma_ok(bool bf16, int ld, int col0, int dx, int C);
 int km_cpad(int C);
 int km_dxp(int dx);

@@ -284,3 +284,41 @@ def test_partition_selection_from_codes_equals_from_scores():
     r = a["sel_counts"]
     for h, c in np.ndindex(r.shape):
         assert np.array_equal(a["sel_idx"][h, c, :r[h, c]], b["sel_idx"][h, c, :r[h, c]])
+
+
+def _queries_case(cfg, x):
+    layer = G.make_layer(cfg)
+    q, _, _ = G.to_device(x)
+    layer.cluster_queries(q, torch.from_numpy(x.init_q).cuda())
+    torch.cuda.synchronize()
+    ref = oracle.cluster_queries(x.q, cfg.c_q, cfg.iters, x.init_q)
+    assert int(layer.status.item()) == 0
+    assert np.array_equal(layer.assign.cpu().numpy(), ref["assign"])
+    assert np.array_equal(layer.perm.cpu().numpy(), ref["perm"])
+    assert np.array_equal(layer.q_centroids.cpu().numpy().view(np.uint32),
+                          ref["centroids"].view(np.uint32))
+    return ref
+
+
+@pytest.mark.parametrize("d,c_q", [(128, 300), (64, 600), (128, 1000)])
+def test_codebooks_streamed_through_lds_in_chunks(d, c_q):
+    # bf16 codebooks beyond the assignment kernel's LDS: 300 x 128 (two
+    # chunks), 600 x 64 (a ragged last chunk), 1000 x 128 (four chunks)
+    split = (16, 56, 56) if d == 128 else (16, 24, 24)
+    cfg = MID_HY.with_(name=f"chunked_{d}_{c_q}", d=d, split=split, c_q=c_q, heads=2,
+                       iters=4, seed=13)
+    G.say(f"[parity] chunked codebook d={d} c_q={c_q} n={cfg.n}")
+    _queries_case(cfg, inputs.generate(cfg))
+
+
+def test_chunked_codebook_with_tied_centroids():
+    # six distinct query rows repeated: hundreds of equal centroids, so
+    # points have four or more tied candidates and scan every centroid
+    cfg = MID_HY.with_(name="chunked_ties", c_q=300, heads=1, iters=3, seed=17)
+    x = inputs.generate(cfg)
+    rng = np.random.default_rng(5)
+    proto = x.q[0, rng.choice(cfg.n, 6, replace=False)]
+    x.q[0] = proto[rng.integers(0, 6, cfg.n)]
+    x.q_bits[0] = inputs.bf16_bits(x.q[0])
+    ref = _queries_case(cfg, x)
+    assert (ref["counts"] == 0).sum() >= 290
