@@ -383,6 +383,111 @@ def partition_study(config_name="hy720", heads=4, c_q=300, c_m=333, reps=2,
             "sampled_queries_per_head": sample, "rows": rows}
 
 
+def matched_retention(exact, proxy, top_frac=0.1, target=0.958):
+    """App. C protocol, per row (one query): the oracle set is the top
+    ceil(top_frac N) keys by exact score (ties to the lower index); keys
+    are taken in proxy-score order, whole groups of equal proxy score at a
+    time, until `target` of the oracle set is held.  Returns the retained
+    fraction of all keys and the oracle recall reached, per row."""
+    import torch
+    Q, N = exact.shape
+    kt = math.ceil(top_frac * N)
+    need = math.ceil(target * kt)
+    order_e = torch.argsort(exact, dim=1, descending=True, stable=True)
+    oracle = torch.zeros(exact.shape, dtype=torch.bool, device=exact.device)
+    oracle.scatter_(1, order_e[:, :kt], True)
+    order_p = torch.argsort(proxy, dim=1, descending=True, stable=True)
+    hits = torch.gather(oracle, 1, order_p).to(torch.int32).cumsum(1)
+    pos = (hits >= need).to(torch.int8).argmax(1)          # first position reaching it
+    s_star = torch.gather(torch.gather(proxy, 1, order_p), 1, pos[:, None])
+    kept = proxy >= s_star                                   # the whole tie group
+    recall = (kept & oracle).sum(1).double() / kt
+    return kept.sum(1).double() / N, recall
+
+
+def recall_at_density(p_exact, proxy, density):
+    """Softmax mass of the exact attention row held by the top
+    round(density N) keys in proxy order (ties to the lower index)."""
+    import torch
+    N = proxy.shape[1]
+    k = max(1, int(round(density * N)))
+    top = torch.argsort(proxy, dim=1, descending=True, stable=True)[:, :k]
+    return torch.gather(p_exact, 1, top).sum(1)
+
+
+def recall_study(config_name="hy720", heads=4, c_q=300, c_m=333, block=64, sample=256,
+                 densities=(0.05, 0.1, 0.2, 0.3, 0.5)):
+    """Matched-recall retention (App. C, Fig. 9) and attention recall against
+    density (Fig. 2) of three key-side proxies that all score a query by its
+    cluster centroid: SCOPE's subspace lookup sum (RoPE t/h/w, C_m per
+    subspace), full-dimensional key clusters (C_m centroids) and block means
+    of `block` consecutive tokens.  Exact scores of sampled queries come
+    from their own rows of Q K^T."""
+    import torch
+    from paper_2608_12780_amd import inputs
+    from paper_2608_12780_amd.layer import ScopeLayer, ScopePartitionLayer
+    cfg = inputs.CONFIGS[config_name].with_(c_q=c_q, c_m=c_m)
+    x = inputs.generate(cfg.with_(heads=heads))
+    dev = torch.device("cuda", 0)
+    up = lambda b: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
+    q, k, v = up(x.q_bits), up(x.k_bits), up(x.v_bits)
+    iq = torch.from_numpy(x.init_q).to(dev)
+    sig = 1.0 / math.sqrt(cfg.d)
+    # SCOPE proxy (materialised logits of the three-range calls)
+    scope = ScopeLayer(heads, cfg.n, cfg.d, cfg.ranges, c_q, (c_m,) * 3, cfg.iters,
+                       cfg.rho, cfg.k_fix, dtype=cfg.dtype, device=dev,
+                       materialize_scores=True)
+    scope.cluster_queries(q, iq)
+    scope.cluster_keys(k, torch.from_numpy(inputs.partition_init(cfg, 3, c_m, heads)).to(dev))
+    scope.proxy_scores()
+    # full-dimensional key clusters: the one-set partition
+    full = ScopePartitionLayer(heads, cfg.n, cfg.d, inputs.partition_sets(cfg, "1"), c_q,
+                               (c_m,), cfg.iters, cfg.rho, cfg.k_fix, dtype=cfg.dtype,
+                               device=dev, materialize_scores=True)
+    full.cluster_queries(q, iq)
+    full.cluster_keys(k, torch.from_numpy(inputs.partition_init(cfg, 1, c_m, heads)).to(dev))
+    full.proxy_scores()
+    torch.cuda.synchronize()
+    assert torch.equal(scope.assign, full.assign)   # same query clusters
+    rng = np.random.default_rng(cfg.seed + 7)
+    rows = {"scope_subspaces": [], "full_dim_clusters": [], "blocks": []}
+    dens = {name: {str(dd): [] for dd in densities} for name in rows}
+    nb = (cfg.n + block - 1) // block
+    for h in range(heads):
+        kf = k[h].float()
+        pad = torch.zeros(nb * block - cfg.n, cfg.d, device=dev)
+        cnt = torch.full((nb,), float(block), device=dev)
+        cnt[-1] = block - (nb * block - cfg.n)
+        kbar = torch.cat([kf, pad]).reshape(nb, block, cfg.d).sum(1) / cnt[:, None]
+        qi = torch.from_numpy(rng.choice(cfg.n, sample, replace=False)).to(dev)
+        c_ = scope.assign[h, qi].long()
+        exact = (q[h, qi].float() @ kf.T) * sig
+        p_exact = torch.softmax(exact, dim=1)
+        qbar = scope.q_centroids[h, c_]
+        prox = {"scope_subspaces": scope.scores[h, c_],
+                "full_dim_clusters": full.scores[h, c_],
+                "blocks": ((qbar @ kbar.T) * sig).repeat_interleave(block, dim=1)[:, :cfg.n]}
+        for name, pr in prox.items():
+            ret, rec = matched_retention(exact, pr)
+            rows[name].append(torch.stack([ret, rec], 1))
+            for dd in densities:
+                dens[name][str(dd)].append(recall_at_density(p_exact, pr, dd))
+    out = []
+    for name in rows:
+        r = torch.cat(rows[name])
+        row = {"proxy": name, "retention_mean": round(float(r[:, 0].mean()), 4),
+               "retention_median": round(float(r[:, 0].median()), 4),
+               "oracle_recall_mean": round(float(r[:, 1].mean()), 4),
+               "attention_recall_at_density": {dd: round(float(torch.cat(v_).mean()), 4)
+                                               for dd, v_ in dens[name].items()}}
+        log(f"[recall] {row}")
+        out.append(row)
+    return {"study": "matched oracle recall and attention recall vs density (App. C, Fig. 2)",
+            "workload": WORKLOAD_NAMES.get(cfg.name), "heads": heads, "n": cfg.n,
+            "c_q": c_q, "c_m": c_m, "block_tokens": block, "oracle_top_fraction": 0.1,
+            "target_oracle_recall": 0.958, "sampled_queries_per_head": sample, "rows": out}
+
+
 def cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -498,6 +603,9 @@ def main():
         return
     if len(sys.argv) >= 2 and sys.argv[1] == "--traffic-probe":
         traffic_probe()
+        return
+    if len(sys.argv) >= 2 and sys.argv[1] == "--recall-study":
+        print(json.dumps(recall_study()), flush=True)
         return
     if len(sys.argv) >= 2 and sys.argv[1] == "--partition-study":
         print(json.dumps(partition_study()), flush=True)
