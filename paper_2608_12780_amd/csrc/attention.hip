@@ -75,7 +75,12 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel(
     const int32_t *__restrict__ perm, const int32_t *__restrict__ sel_idx,
     const int4 *__restrict__ items, float scale_log2) {
   constexpr int NT = kNW * 64;
-  constexpr int KS = D + 8;       // K and V tile row stride (bf16 elements)
+  // LDS row strides (bf16 elements): K rows are read 16 bytes per lane, 16
+  // consecutive rows at a time, so 16 bytes of padding keep them on distinct
+  // banks; the transposing V reads take 64 bytes from each of four rows per
+  // 32 lanes, so V rows are padded by 64 bytes (stride = 64 mod 256 bytes)
+  constexpr int KS = D + 8;
+  constexpr int KSV = D + 32;
   constexpr int C8 = D / 8;       // 16-byte chunks per row
   // staging: the first half of the block stages V (4 consecutive keys of one
   // 8-channel column per thread), the second half K (RK consecutive rows of
@@ -85,7 +90,7 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel(
   static_assert(kBN * C8 % HALF == 0 && RK >= 1 && RK <= 4, "tile/threads mismatch");
   constexpr int NR = 4;                     // rows fetched per thread per tile
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kBN * KS];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][kBN * KS];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][kBN * KSV];
 
   const int item = blockIdx.x;
   if (item >= total_items) return;
@@ -145,7 +150,7 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel(
   // transposing reads of V (ds_read_b64_tr_b16): source lane s supplies
   // row 4*(s/32) + (s%16)/4 and channels 16*((s/16)%2) + 4*(s%4) .. +3 of a
   // 16-key step; lane L then holds 4 consecutive keys of channel L%32
-  const int tr_off = (4 * (lane >> 5) + ((lane & 15) >> 2)) * KS + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const int tr_off = (4 * (lane >> 5) + ((lane & 15) >> 2)) * KSV + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
   const void *src = is_v ? vv : kv;
   // bf16 inputs are gathered through buffer resources: out-of-range offsets
   // (index slots past the key set, any bad row) read as zero in hardware,
@@ -189,7 +194,7 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel(
     uint16_t *dst = is_v ? Vs[buf] : Ks[buf];
 #pragma unroll
     for (int i = 0; i < RK; ++i)
-      *reinterpret_cast<uint4 *>(&dst[(key0 + i) * KS + 8 * c8]) = dx[i];
+      *reinterpret_cast<uint4 *>(&dst[(key0 + i) * (is_v ? KSV : KS) + 8 * c8]) = dx[i];
   };
 
   auto compute = [&](int tile, int buf) {
@@ -282,9 +287,9 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel(
       for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
-          const uint16_t *vt = &Vs[buf][(kb * 32 + 16 * s2) * KS + db * 32 + tr_off];
+          const uint16_t *vt = &Vs[buf][(kb * 32 + 16 * s2) * KSV + db * 32 + tr_off];
           const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(vt));
-          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(vt + 8 * KS));
+          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(vt + 8 * KSV));
           const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
           const bf16x8 a = as_bf16x8(make_uint4(l2.x, l2.y, h2.x, h2.y));
           oacc[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
