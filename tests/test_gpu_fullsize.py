@@ -93,3 +93,68 @@ def check_head(cfg, x, head, gpu, name):
     mx, mr = G.assert_attention_close(gpu["out"][0, rows], ref[0, rows])
     G.say(f"[fullsize] {name}: head {head} attention on {len(rows)} rows max-abs {mx:.3e} "
           f"mean-rel {mr:.3e}")
+
+
+def test_full_size_paper_operating_point():
+    # C_q = 300 and C_m = 333 at the HunyuanVideo-720p-like shape: the query
+    # codebook is streamed through LDS in chunks
+    cfg = inputs.CONFIGS["hy720"].with_(c_q=300, c_m=333, heads=3)
+    G.say(f"[fullsize] paper point: heads={cfg.heads} n={cfg.n} c_q=300 c_m=333")
+    x = inputs.generate(cfg)
+    layer = ScopeLayer(cfg.heads, cfg.n, cfg.d, cfg.ranges, cfg.c_q, (cfg.c_m,) * 3,
+                       cfg.iters, cfg.rho, cfg.k_fix, dtype=cfg.dtype)
+    q, k, v = G.to_device(x)
+    layer.forward(q, k, v, torch.from_numpy(x.init_q).cuda(),
+                  torch.from_numpy(x.init_k).cuda())
+    torch.cuda.synchronize()
+    assert int(layer.status.item()) == 0
+    head = 1
+    g = lambda t: t[head:head + 1].cpu().numpy()
+    gpu = dict(assign=g(layer.assign), counts=g(layer.counts), offsets=g(layer.offsets),
+               perm=g(layer.perm), centroids=g(layer.q_centroids),
+               k_centroids=g(layer.k_centroids), codes=g(layer.codes).view(np.uint32),
+               tables=g(layer.tables), base=g(layer.base_counts), topp=g(layer.topp_counts),
+               k_head=g(layer.k_head), sel_counts=g(layer.sel_counts), sel_idx=g(layer.sel_idx),
+               out=layer.out[head:head + 1].float().cpu().numpy())
+    del layer, q, k, v
+    torch.cuda.empty_cache()
+    check_head(cfg, x, head, gpu, "paper point")
+
+
+def test_full_size_random_partition():
+    # a random three-way channel split (the gather path) with 333 centroids
+    # per subspace, full HunyuanVideo-720p-like size, two heads
+    from paper_2608_12780_amd.layer import ScopePartitionLayer
+    cfg = inputs.CONFIGS["hy720"].with_(c_q=300, c_m=333, heads=2)
+    sets = inputs.partition_sets(cfg, "3-random")
+    init_k = inputs.partition_init(cfg, 3, 333)
+    G.say(f"[fullsize] random partition: sizes {[len(s) for s in sets]}")
+    x = inputs.generate(cfg)
+    layer = ScopePartitionLayer(cfg.heads, cfg.n, cfg.d, sets, cfg.c_q, (333,) * 3,
+                                cfg.iters, cfg.rho, cfg.k_fix, dtype=cfg.dtype)
+    q, k, v = G.to_device(x)
+    layer.forward(q, k, v, torch.from_numpy(x.init_q).cuda(), torch.from_numpy(init_k).cuda())
+    torch.cuda.synchronize()
+    assert int(layer.status.item()) == 0
+    head = 0
+    g = lambda t: t[head:head + 1].cpu().numpy()
+    codes, kcen, tables = g(layer.codes).view(np.uint16), g(layer.k_centroids), g(layer.tables)
+    counts, qcen = g(layer.counts), g(layer.q_centroids)
+    gsel = dict(base=g(layer.base_counts), topp=g(layer.topp_counts), k_head=g(layer.k_head),
+                sel_counts=g(layer.sel_counts), sel_idx=g(layer.sel_idx))
+    del layer, q, k, v
+    torch.cuda.empty_cache()
+    hk = x.k[head:head + 1]
+    qr = oracle.cluster_queries(x.q[head:head + 1], cfg.c_q, cfg.iters, x.init_q[head:head + 1])
+    assert np.array_equal(counts, qr["counts"])
+    assert np.array_equal(qcen.view(np.uint32), qr["centroids"].view(np.uint32))
+    kr = oracle.cluster_key_partition(hk, sets, (333,) * 3, cfg.iters, init_k[head:head + 1])
+    assert np.array_equal(codes, kr["codes"])
+    assert np.array_equal(kcen.view(np.uint32), kr["centroids"].view(np.uint32))
+    P = oracle.tables_partition(qr["centroids"], kr["centroids"], sets, (333,) * 3)
+    assert np.array_equal(tables.view(np.uint32), P.view(np.uint32))
+    S = oracle.proxy_scores_partition(P, kr["codes"], cfg.d, (333,) * 3)
+    sel = oracle.select(S, qr["counts"], cfg.rho, cfg.k_fix)
+    del S
+    G.assert_same_selection(gsel, sel)
+    G.say(f"[fullsize] random partition: head {head} bit-exact, k_head {int(gsel['k_head'][0])}")
