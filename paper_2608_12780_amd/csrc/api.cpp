@@ -113,8 +113,15 @@ struct QueryWs {
   long long *slab;
   int32_t *cslab;
   uint16_t *ubf;
-  float *nu, *bnd;
+  float *nu, *bnd, *split;
 };
+
+// part/pnx of a chunked codebook inside one split buffer
+void set_split(KmProblem &p, float *split) {
+  p.part = split;
+  p.pnx = split ? split + static_cast<size_t>(p.heads) * p.n * 4 * scope::km_parts(p.C, p.dx)
+                : nullptr;
+}
 size_t query_ws(const scope_shape *s, int c_q, void *base, QueryWs *w) {
   Carver cv(base);
   const int nch = scope::km_nchunks(s->n);
@@ -128,6 +135,7 @@ size_t query_ws(const scope_shape *s, int c_q, void *base, QueryWs *w) {
   q.ubf = cv.take<uint16_t>(static_cast<size_t>(s->heads) * cpad * 2 * scope::km_dxp(s->d));
   q.nu = cv.take<float>(static_cast<size_t>(s->heads) * cpad);
   q.bnd = cv.take<float>(static_cast<size_t>(s->heads) * cpad * 2);
+  q.split = cv.take<float>(scope::km_split_floats(c_q, s->d, s->heads, s->n));
   if (w) *w = q;
   return cv.used;
 }
@@ -138,6 +146,7 @@ struct KeyWs {
   int32_t *cslab;
   uint16_t *ubf[3];
   float *nu[3], *bnd[3];
+  float *split;  // shared by the subspaces, whose assignments run in turn
 };
 size_t key_ws(const scope_shape *s, const int32_t *c_m, void *base, KeyWs *w) {
   Carver cv(base);
@@ -154,6 +163,12 @@ size_t key_ws(const scope_shape *s, const int32_t *c_m, void *base, KeyWs *w) {
     k.nu[m] = cv.take<float>(H * cpad);
     k.bnd[m] = cv.take<float>(H * cpad * 2);
   }
+  size_t split = 0;
+  for (int m = 0; m < 3; ++m) {
+    const size_t f = scope::km_split_floats(c_m[m], s->range_len[m], s->heads, s->n);
+    split = f > split ? f : split;
+  }
+  k.split = cv.take<float>(split);
   if (w) *w = k;
   return cv.used;
 }
@@ -254,6 +269,7 @@ struct PartKeyWs {
   int32_t *cslab;
   uint16_t *ubf[scope::kMaxSub];
   float *nu[scope::kMaxSub], *bnd[scope::kMaxSub];
+  float *split;
 };
 size_t part_key_ws(const scope_shape *s, const scope_partition *p, void *base,
                    PartKeyWs *w) {
@@ -276,6 +292,12 @@ size_t part_key_ws(const scope_shape *s, const scope_partition *p, void *base,
     k.nu[m] = cv.take<float>(H * cpad);
     k.bnd[m] = cv.take<float>(H * cpad * 2);
   }
+  size_t split = 0;
+  for (int m = 0; m < g.M; ++m) {
+    const size_t f = scope::km_split_floats(g.C[m], g.len[m], s->heads, s->n);
+    split = f > split ? f : split;
+  }
+  k.split = cv.take<float>(split);
   if (w) *w = k;
   return cv.used;
 }
@@ -376,6 +398,7 @@ int32_t scope_cluster_queries(const scope_shape *shape, const void *q,
   p.ubf = w.ubf;
   p.nu = w.nu;
   p.bnd = w.bnd;
+  set_split(p, w.split);
   const scope::AccPlan plan = query_plan(shape, c_q);
   SCOPE_TRY(scope::km_init(p, init_idx, c_q, dev_status, s));
   // the returned grouping is that of the last assignment, taken before the
@@ -443,6 +466,7 @@ int32_t scope_cluster_key_subspaces(const scope_shape *shape, const void *k,
     pm.ubf = w.ubf[m];
     pm.nu = w.nu[m];
     pm.bnd = w.bnd[m];
+    set_split(pm, w.split);
     ucol += static_cast<size_t>(c_m[m]) * pm.dx;
     const int32_t *init = init_idx ? init_idx + static_cast<size_t>(m) * init_stride : nullptr;
     // init rows of head h, subspace m live at init_idx[(h*3 + m)*init_stride]
@@ -606,6 +630,7 @@ int32_t scope_cluster_key_partition(const scope_shape *shape, const void *k,
     pm.ubf = w.ubf[m];
     pm.nu = w.nu[m];
     pm.bnd = w.bnd[m];
+    set_split(pm, w.split);
     ucol += static_cast<size_t>(g.C[m]) * pm.dx;
     // rows of head h, subspace m at init_idx[(h*M + m)*init_stride]
     const int32_t *init = init_idx ? init_idx + static_cast<size_t>(m) * init_stride : nullptr;

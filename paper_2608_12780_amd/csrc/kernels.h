@@ -32,11 +32,17 @@ struct KmProblem {
   uint16_t *ubf;          // [heads][cpad][2 * dxp]: bf16 hi then lo terms
   float *nu;              // [heads][cpad]
   float *bnd;             // [heads][cpad][2]: per-row bound parts
+  // codebooks beyond the LDS: per chunk and point the four smallest packed
+  // scores ([parts][heads][n][4]) and the point's norm bound ([heads][n])
+  float *part, *pnx;
 };
 
 // Whether the matrix-core assignment applies: bf16 rows at even offsets and
 // at most 1024 centroids (codebooks beyond the LDS are streamed in chunks).
 bool km_mfma_ok(bool bf16, int ld, int col0, int dx, int C);
+int km_parts(int C, int dx);
+// floats of KmProblem::part and ::pnx together (0 when the codebook fits)
+size_t km_split_floats(int C, int dx, int heads, int n);
 int km_cpad(int C);
 int km_dxp(int dx);
 
@@ -54,8 +60,8 @@ hipError_t km_group(const KmProblem &p, hipStream_t s);
 // clusters, centroids [C[m]][dx[m]] at float offset ucol[m] of a head) are
 // updated together; their channels are cut into windows whose int64 sums
 // fit one block's LDS.
-constexpr int kAccLds = 16384;           // int64 sums per block
-constexpr int kAccCnt = 3072;            // int32 cluster counts per block
+constexpr int kAccLds = 19200;           // int64 sums per block (150 KB of LDS)
+constexpr int kAccCnt = 1024;            // int32 cluster counts per block
 constexpr int kAccMaxPieces = 4;
 constexpr int kAccMaxWindows = 16;
 constexpr int kMaxSub = 8;               // subspaces of a key partition

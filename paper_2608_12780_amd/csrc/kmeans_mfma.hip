@@ -344,34 +344,28 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
   }
 }
 
-// Codebooks larger than the LDS holds (e.g. 300 centroids at d = 128): the
-// block walks its slices in rounds of one slice per wave and streams the
-// codebook through LDS chunk by chunk in every round.  Each point keeps its
-// four smallest packed scores over all chunks; with the same margin as
-// above, a point whose second score is clear takes the smallest, one whose
-// fourth score is clear has at most three candidates, re-scored
-// canonically, and only a point with four or more candidates scans every
-// centroid canonically.
+// Codebooks larger than the LDS holds (e.g. 300 centroids at d = 128) are
+// cut into chunks of at most CR rows, and every chunk gets its own
+// persistent blocks, which keep the chunk in LDS for their whole range of
+// slices (waves run independently, as above).  Per point, each chunk yields
+// its four smallest packed scores (indices over the whole codebook), and
+// chunk 0 also the point's norm bound.  The decision kernel below merges the
+// lists, one point per thread.
 template <int DXP>
-__global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_chunked_kernel(
+__global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_part_kernel(
     const uint16_t *__restrict__ X, size_t x_hs, int ld, int col0, int dx,
-    int n, int heads, const float *__restrict__ U, size_t u_hs,
-    const uint16_t *__restrict__ ubf, const float *__restrict__ nu,
-    const float *__restrict__ bnd, int C, int cpad, int32_t *assign,
-    size_t a_hs, int32_t *chunk_hist, int nchunks) {
-  constexpr int US = 2 * DXP + 8;
-  constexpr int KS = DXP / 16;
-  constexpr int CR = kUbfLds / US / 32 * 32;  // codebook rows per chunk
+    int n, int heads, const uint16_t *__restrict__ ubf, const float *__restrict__ nu,
+    int cpad, int crows, float *part, float *pnx) {
+  constexpr int US = 2 * DXP + 8;  // LDS row stride of the two-term codebook
+  constexpr int KS = DXP / 16;     // MFMA k-steps per term
   __shared__ __attribute__((aligned(16))) uint16_t Us[kUbfLds];
   __shared__ float nus[kMaxCpad];
-  __shared__ float red[3][kWavesPerBlock];
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6, l32 = lane & 31, hf = lane >> 5;
-
-  const float kappa = 8.0f * DXP * 0x1p-24f;
+  const int chunk = blockIdx.y, r0 = chunk * crows;
+  const int rows = cpad - r0 < crows ? cpad - r0 : crows;  // a multiple of 32
   const int ib = 32 - __clz(cpad - 1);
   const uint32_t imask = (1u << ib) - 1u;
-  const float dpack = __uint_as_float(static_cast<uint32_t>(127 + ib - 23) << 23);
   const int nslices = (n + 31) / 32;
 
   const long long total = static_cast<long long>(heads) * nslices;
@@ -382,46 +376,21 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_chunked_ke
     const int h = static_cast<int>(beg / nslices);
     const long long seg_end = end < static_cast<long long>(h + 1) * nslices
                                   ? end : static_cast<long long>(h + 1) * nslices;
+    // stage this head's chunk (rows r0 .. r0+rows) and its norms
     __syncthreads();
-    float e_max = 0.0f, n_max = 0.0f, nu_max = 0.0f;
-    for (int r = t; r < cpad; r += 64 * kWavesPerBlock) {
-      const size_t row = static_cast<size_t>(h) * cpad + r;
-      const float v = nu[row];
-      nus[r] = v;
-      if (r < C) {
-        e_max = fmaxf(e_max, bnd[2 * row + 0]);
-        n_max = fmaxf(n_max, bnd[2 * row + 1]);
-        nu_max = fmaxf(nu_max, fabsf(v));
-      }
+    const uint16_t *ub = ubf + (static_cast<size_t>(h) * cpad + r0) * (2 * DXP);
+    for (int e = t; e < rows * (DXP / 4); e += 64 * kWavesPerBlock) {
+      const int r = e / (DXP / 4), q = e % (DXP / 4);
+      *reinterpret_cast<uint4 *>(&Us[r * US + 8 * q]) =
+          *reinterpret_cast<const uint4 *>(ub + static_cast<size_t>(r) * (2 * DXP) + 8 * q);
     }
-    e_max = wave_max(e_max);
-    n_max = wave_max(n_max);
-    nu_max = wave_max(nu_max);
-    if (lane == 0) {
-      red[0][w] = e_max;
-      red[1][w] = n_max;
-      red[2][w] = nu_max;
-    }
+    for (int r = t; r < rows; r += 64 * kWavesPerBlock)
+      nus[r] = nu[static_cast<size_t>(h) * cpad + r0 + r];
     __syncthreads();
-    float E = 0.0f, Nmax = 0.0f, numax = 0.0f;
-#pragma unroll
-    for (int i = 0; i < kWavesPerBlock; ++i) {
-      E = fmaxf(E, red[0][i]);
-      Nmax = fmaxf(Nmax, red[1][i]);
-      numax = fmaxf(numax, red[2][i]);
-    }
-    E = E * 1.001f + 1e-30f;
-    Nmax *= 1.001f;
-    numax *= 1.001f;
-    const float *Uh = U + h * u_hs;
-    const uint16_t *ub = ubf + static_cast<size_t>(h) * cpad * (2 * DXP);
-    // rounds: every wave of the block takes the next slice (or idles)
-    for (long long g0 = beg; g0 < seg_end; g0 += kWavesPerBlock) {
-      const long long g = g0 + w;
-      const bool act = g < seg_end;
-      const int sl = static_cast<int>((act ? g : g0) - static_cast<long long>(h) * nslices);
+    for (long long g = beg + w; g < seg_end; g += kWavesPerBlock) {
+      const int sl = static_cast<int>(g - static_cast<long long>(h) * nslices);
       const int i = sl * 32 + l32;
-      const bool valid = act && i < n;
+      const bool valid = i < n;
       const uint16_t *xrow = X + h * x_hs + static_cast<size_t>(valid ? i : 0) * ld + col0;
       bf16x8 xf[KS];
       float ss = 0.0f;
@@ -441,11 +410,8 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_chunked_ke
         xf[s] = __builtin_bit_cast(bf16x8, make_uint4(wv[0], wv[1], wv[2], wv[3]));
       }
       ss += __shfl_xor(ss, 32);
-      const float nx = sqrtf(ss) * 1.0001f + 1e-30f;
-      const float beta = (2.0f * nx * (E + kappa * Nmax) +
-                          0x1p-23f * (numax + 2.02f * nx * Nmax)) * 1.01f + 1e-25f;
 
-      auto chain = [&](int rb) {  // rb: row within the staged chunk
+      auto chain = [&](int rb) {  // rb: row within the chunk
         f32x16 acc;
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
@@ -467,34 +433,21 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_chunked_ke
         m2 = __builtin_amdgcn_fmed3f(m1, m2, sp);
         m1 = fminf(m1, sp);
       };
-      auto fold = [&](const f32x16 &acc, int r0) {  // r0: codebook row of the block
+      auto fold = [&](const f32x16 &acc, int rb) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const uint32_t r = static_cast<uint32_t>(r0 + 8 * (e >> 2) + 4 * hf + (e & 3));
-          const float sc = fmaf(-2.0f, acc[e], nus[r]);
-          insert(__uint_as_float((__float_as_uint(sc) & ~imask) | r));
+          const int rl = rb + 8 * (e >> 2) + 4 * hf + (e & 3);
+          const float sc = fmaf(-2.0f, acc[e], nus[rl]);
+          insert(__uint_as_float((__float_as_uint(sc) & ~imask) | static_cast<uint32_t>(r0 + rl)));
         }
       };
-      for (int c0 = 0; c0 < cpad; c0 += CR) {
-        const int rows = cpad - c0 < CR ? cpad - c0 : CR;
-        __syncthreads();  // every wave is done with the previous chunk
-        for (int e = t; e < rows * (DXP / 4); e += 64 * kWavesPerBlock) {
-          const int r = e / (DXP / 4), q = e % (DXP / 4);
-          *reinterpret_cast<uint4 *>(&Us[r * US + 8 * q]) = *reinterpret_cast<const uint4 *>(
-              ub + static_cast<size_t>(c0 + r) * (2 * DXP) + 8 * q);
-        }
-        __syncthreads();
-        if (act) {
-          f32x16 prev = chain(0);
-          for (int rb = 32; rb < rows; rb += 32) {
-            const f32x16 cur = chain(rb);
-            fold(prev, c0 + rb - 32);
-            prev = cur;
-          }
-          fold(prev, c0 + rows - 32);
-        }
+      f32x16 prev = chain(0);
+      for (int rb = 32; rb < rows; rb += 32) {
+        const f32x16 cur = chain(rb);
+        fold(prev, rb - 32);
+        prev = cur;
       }
-      if (!act) continue;
+      fold(prev, rows - 32);
       {  // the two half-waves saw disjoint centroids of the same points
         const float o1 = __shfl_xor(m1, 32), o2 = __shfl_xor(m2, 32);
         const float o3 = __shfl_xor(m3, 32), o4 = __shfl_xor(m4, 32);
@@ -503,42 +456,104 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_chunked_ke
         insert(o3);
         insert(o4);
       }
-      const float slack = (2.0f * beta + 2.0f * dpack * fabsf(m1)) * 1.001f;
-      const float lim = m1 + slack;
-      const float thr = lim + fabsf(lim) * 2e-6f + 1e-30f;
-      int arg = static_cast<int>(__float_as_uint(m1) & imask);
-      if (valid && hf == 0 && !(m2 > thr)) {
-        const uint16_t *xr = X + h * x_hs + static_cast<size_t>(i) * ld + col0;
-        unsigned long long b = ~0ull;
-        auto rescore = [&](int r) {
-          r = min(r, C - 1);
-          const float *u = Uh + static_cast<size_t>(r) * dx;
-          float dot = 0.0f;
-          for (int c = 0; c < dx; ++c) dot = fmaf(bf16_to_f32(xr[c]), u[c], dot);
-          const float sc = fmaf(-2.0f, dot, nus[r]) + 0.0f;
-          const unsigned long long key =
-              (static_cast<unsigned long long>(asc_key(sc)) << 32) | static_cast<unsigned>(r);
-          b = key < b ? key : b;
-        };
-        if (m4 > thr) {
-          // every candidate is among the three smallest
-          rescore(arg);
-          rescore(static_cast<int>(__float_as_uint(m2) & imask));
-          if (m3 <= thr) rescore(static_cast<int>(__float_as_uint(m3) & imask));
-        } else {
-          for (int r = 0; r < C; ++r) rescore(r);
-        }
-        arg = static_cast<int>(b & 0xFFFFFFFFu);
-      }
       if (valid && hf == 0) {
-        arg = min(max(arg, 0), C - 1);
-        assign[h * a_hs + i] = arg;
-        if (chunk_hist)
-          atomicAdd(&chunk_hist[(static_cast<size_t>(h) * nchunks + (i / kAssignBlock)) * C + arg], 1);
+        *reinterpret_cast<float4 *>(part + ((static_cast<size_t>(chunk) * heads + h) * n + i) * 4) =
+            make_float4(m1, m2, m3, m4);
+        if (chunk == 0) pnx[static_cast<size_t>(h) * n + i] = sqrtf(ss) * 1.0001f + 1e-30f;
       }
     }
     beg = seg_end;
   }
+}
+
+// The decision for chunked codebooks, one point per thread: the chunks'
+// lists merged into the four smallest packed scores, then the margin of the
+// kernel above; with a runner-up inside it, the fourth score bounds the
+// candidates to at most three, re-scored canonically, and only four or more
+// candidates scan every centroid canonically.
+__global__ __launch_bounds__(256) void km_assign_decide_kernel(
+    const uint16_t *__restrict__ X, size_t x_hs, int ld, int col0, int dx, int n,
+    int heads, const float *__restrict__ U, size_t u_hs, const float *__restrict__ nu,
+    const float *__restrict__ bnd, int C, int cpad, int nparts,
+    const float *__restrict__ part, const float *__restrict__ pnx, float kappa,
+    int32_t *assign, size_t a_hs, int32_t *chunk_hist, int nchunks) {
+  __shared__ float red[3][4];
+  const int h = blockIdx.y, t = threadIdx.x, lane = t & 63, w = t >> 6;
+  // the head's bound constants, as in the assignment kernel
+  float e_max = 0.0f, n_max = 0.0f, nu_max = 0.0f;
+  for (int r = t; r < C; r += 256) {
+    const size_t row = static_cast<size_t>(h) * cpad + r;
+    e_max = fmaxf(e_max, bnd[2 * row + 0]);
+    n_max = fmaxf(n_max, bnd[2 * row + 1]);
+    nu_max = fmaxf(nu_max, fabsf(nu[row]));
+  }
+  e_max = wave_max(e_max);
+  n_max = wave_max(n_max);
+  nu_max = wave_max(nu_max);
+  if (lane == 0) {
+    red[0][w] = e_max;
+    red[1][w] = n_max;
+    red[2][w] = nu_max;
+  }
+  __syncthreads();
+  const float E = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3])) * 1.001f + 1e-30f;
+  const float Nmax = fmaxf(fmaxf(red[1][0], red[1][1]), fmaxf(red[1][2], red[1][3])) * 1.001f;
+  const float numax = fmaxf(fmaxf(red[2][0], red[2][1]), fmaxf(red[2][2], red[2][3])) * 1.001f;
+  const int i = blockIdx.x * 256 + t;
+  if (i >= n) return;
+  const int ib = 32 - __clz(cpad - 1);
+  const uint32_t imask = (1u << ib) - 1u;
+  const float dpack = __uint_as_float(static_cast<uint32_t>(127 + ib - 23) << 23);
+  float m1 = 0x1.1p127f, m2 = 0x1.1p127f, m3 = 0x1.1p127f, m4 = 0x1.1p127f;
+  auto insert = [&](float sp) {
+    m4 = __builtin_amdgcn_fmed3f(m3, m4, sp);
+    m3 = __builtin_amdgcn_fmed3f(m2, m3, sp);
+    m2 = __builtin_amdgcn_fmed3f(m1, m2, sp);
+    m1 = fminf(m1, sp);
+  };
+  for (int k = 0; k < nparts; ++k) {
+    const float4 v = *reinterpret_cast<const float4 *>(
+        part + ((static_cast<size_t>(k) * heads + h) * n + i) * 4);
+    insert(v.x);
+    insert(v.y);
+    insert(v.z);
+    insert(v.w);
+  }
+  const float nx = pnx[static_cast<size_t>(h) * n + i];
+  const float beta = (2.0f * nx * (E + kappa * Nmax) +
+                      0x1p-23f * (numax + 2.02f * nx * Nmax)) * 1.01f + 1e-25f;
+  const float slack = (2.0f * beta + 2.0f * dpack * fabsf(m1)) * 1.001f;
+  const float lim = m1 + slack;
+  const float thr = lim + fabsf(lim) * 2e-6f + 1e-30f;
+  int arg = static_cast<int>(__float_as_uint(m1) & imask);
+  if (!(m2 > thr)) {
+    const uint16_t *xr = X + h * x_hs + static_cast<size_t>(i) * ld + col0;
+    const float *Uh = U + h * u_hs;
+    unsigned long long b = ~0ull;
+    auto rescore = [&](int r) {
+      r = min(r, C - 1);
+      const float *u = Uh + static_cast<size_t>(r) * dx;
+      float dot = 0.0f;
+      for (int c = 0; c < dx; ++c) dot = fmaf(bf16_to_f32(xr[c]), u[c], dot);
+      const float sc = fmaf(-2.0f, dot, nu[static_cast<size_t>(h) * cpad + r]) + 0.0f;
+      const unsigned long long key =
+          (static_cast<unsigned long long>(asc_key(sc)) << 32) | static_cast<unsigned>(r);
+      b = key < b ? key : b;
+    };
+    if (m4 > thr) {
+      // every candidate is among the three smallest
+      rescore(arg);
+      rescore(static_cast<int>(__float_as_uint(m2) & imask));
+      if (m3 <= thr) rescore(static_cast<int>(__float_as_uint(m3) & imask));
+    } else {
+      for (int r = 0; r < C; ++r) rescore(r);
+    }
+    arg = static_cast<int>(b & 0xFFFFFFFFu);
+  }
+  arg = min(max(arg, 0), C - 1);
+  assign[h * a_hs + i] = arg;
+  if (chunk_hist)
+    atomicAdd(&chunk_hist[(static_cast<size_t>(h) * nchunks + (i / kAssignBlock)) * C + arg], 1);
 }
 
 __global__ void km_zero_kernel(int32_t *p, size_t count) {
@@ -570,12 +585,29 @@ hipError_t launch_mfma(const KmProblem &p, bool with_hist, hipStream_t s) {
     cus = 256;
   const int blocks = static_cast<int>(slices < static_cast<long long>(cus) * kWavesPerBlock
                                           ? (slices + kWavesPerBlock - 1) / kWavesPerBlock : cus);
-  auto kernel = p.cpad * (2 * DXP + 8) <= kUbfLds ? km_assign_mfma_kernel<DXP>
-                                                  : km_assign_mfma_chunked_kernel<DXP>;
-  hipLaunchKernelGGL(kernel, dim3(blocks), dim3(64 * kWavesPerBlock), 0, s,
-                     static_cast<const uint16_t *>(p.x), p.x_head_stride, p.ld,
-                     p.col0, p.dx, p.n, p.heads, p.u, p.u_head_stride, p.ubf, p.nu, p.bnd,
-                     p.C, p.cpad, p.assign, p.a_head_stride,
+  const uint16_t *x = static_cast<const uint16_t *>(p.x);
+  if (p.cpad * (2 * DXP + 8) <= kUbfLds) {
+    hipLaunchKernelGGL(km_assign_mfma_kernel<DXP>, dim3(blocks), dim3(64 * kWavesPerBlock), 0, s,
+                       x, p.x_head_stride, p.ld, p.col0, p.dx, p.n, p.heads, p.u,
+                       p.u_head_stride, p.ubf, p.nu, p.bnd, p.C, p.cpad, p.assign,
+                       p.a_head_stride, with_hist ? p.chunk_hist : nullptr, nch);
+    return hipGetLastError();
+  }
+  // chunked codebook: balanced chunks, the CUs shared among them
+  const int nparts = km_parts(p.C, p.dx);
+  const int crows = (p.cpad / 32 + nparts - 1) / nparts * 32;
+  const int per_part = cus / nparts > 1 ? cus / nparts : 1;
+  const long long need = (slices + kWavesPerBlock - 1) / kWavesPerBlock;
+  const int bpp = static_cast<int>(need < per_part ? need : per_part);
+  hipLaunchKernelGGL(km_assign_mfma_part_kernel<DXP>, dim3(bpp, nparts),
+                     dim3(64 * kWavesPerBlock), 0, s, x, p.x_head_stride, p.ld, p.col0, p.dx,
+                     p.n, p.heads, p.ubf, p.nu, p.cpad, crows, p.part, p.pnx);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(km_assign_decide_kernel, dim3((p.n + 255) / 256, p.heads), dim3(256), 0,
+                     s, x, p.x_head_stride, p.ld, p.col0, p.dx, p.n, p.heads, p.u,
+                     p.u_head_stride, p.nu, p.bnd, p.C, p.cpad, nparts, p.part, p.pnx,
+                     8.0f * DXP * 0x1p-24f, p.assign, p.a_head_stride,
                      with_hist ? p.chunk_hist : nullptr, nch);
   return hipGetLastError();
 }
@@ -585,7 +617,19 @@ hipError_t launch_mfma(const KmProblem &p, bool with_hist, hipStream_t s) {
 int km_cpad(int C) { return (C + 31) / 32 * 32; }
 int km_dxp(int dx) { return dx <= 16 ? 16 : dx <= 32 ? 32 : dx <= 48 ? 48 : dx <= 64 ? 64 : 128; }
 
-// Codebooks beyond the LDS take the chunked kernel.
+// Chunks of a codebook beyond the LDS (1 when it fits).
+int km_parts(int C, int dx) {
+  const int rows_max = kUbfLds / (2 * km_dxp(dx) + 8) / 32 * 32;
+  return (km_cpad(C) + rows_max - 1) / rows_max;
+}
+
+size_t km_split_floats(int C, int dx, int heads, int n) {
+  const int parts = km_parts(C, dx);
+  if (parts <= 1) return 0;
+  return static_cast<size_t>(heads) * n * (4 * static_cast<size_t>(parts) + 1);
+}
+
+// Codebooks beyond the LDS are split in chunks across blocks.
 bool km_mfma_ok(bool bf16, int ld, int col0, int dx, int C) {
   if (!bf16 || (ld & 1) || (col0 & 1) || (dx & 1) || dx > 128) return false;
   return km_cpad(C) <= kMaxCpad;

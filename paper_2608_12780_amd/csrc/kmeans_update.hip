@@ -242,7 +242,10 @@ bool km_accum_plan(int nsub, const int *col0, const int *dx, const int *C,
       int w = dx[m] - done;
       if (w > room_lds) w = room_lds;
       if (w > room_lanes) w = room_lanes;
-      if (w < dx[m] - done) w &= ~1;
+      // cuts fall on multiples of 64 channels where the room allows (whole
+      // 128-byte lines of bf16 rows), else of 32, else of 4 (8-byte loads);
+      // a window with less room than that is closed
+      if (w < dx[m] - done) w &= w >= 64 ? ~63 : w >= 32 ? ~31 : ~3;
       if (w < 1 || cur.npieces == kAccMaxPieces || !cnt_fits) {
         if (cur.npieces == 0) return false;
         if (!flush()) return false;
@@ -257,7 +260,9 @@ bool km_accum_plan(int nsub, const int *col0, const int *dx, const int *C,
       cur.elems += C[m] * w;
       if (counts_here) cur.cnt_elems += C[m];
       cur.lanes += (w + 1) / 2;
+      const bool cut = w < dx[m] - done;
       done += w;
+      if (cut && !flush()) return false;  // a cut closes its window
     }
   }
   if (!flush()) return false;
