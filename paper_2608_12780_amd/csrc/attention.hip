@@ -161,9 +161,10 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel(
       const_cast<uint16_t *>(static_cast<const uint16_t *>(src) + hoff), static_cast<short>(0),
       static_cast<int>(static_cast<uint32_t>(n) * (D * 2)), 0x00020000);
 
-  // Software pipeline, two tiles deep: the row indices of tile T+1 are
-  // requested before the rows of tile T, so waiting for indices never waits
-  // for rows in flight (vector loads complete in order).  Every load is
+  // Software pipeline, two tiles deep: step T requests the row indices of
+  // tile T+3 first and the rows of tile T+2 after its compute, so waiting for
+  // indices never waits for rows in flight (vector loads complete in order)
+  // and the rows have a whole step to arrive.  Every load is
   // unconditional with clamped indices, so the pipeline has no branches;
   // rows past the key set are fetched but masked (or never read).
   int selA[NR], selB[NR];
@@ -298,12 +299,14 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel(
   };
 
   // one pipeline step: compute tile T from LDS while tile T+1 (already in
-  // registers `cur`) lands in the other LDS buffer and tile T+2 is requested
+  // registers `cur`) lands in the other LDS buffer; the rows of tile T+2
+  // are requested after the compute (they have until the end of the next
+  // step), so the MFMAs of this step never wait for them
   auto step = [&](int tile, int (&sel_next)[NR], uint4 (&cur)[NR],
                   int (&sel_far)[NR], uint4 (&far)[NR]) {
     load_sel(tile + 3, sel_next);
-    load_rows(sel_far, far);
     compute(tile, tile & 1);
+    load_rows(sel_far, far);
     store_rows((tile + 1) & 1, cur);
     __syncthreads();
   };
