@@ -285,15 +285,35 @@ __global__ __launch_bounds__(kSelBlock) void select_base_kernel(
       hm[b] = 0;
     }
     __syncthreads();
+    // four consecutive keys per thread: a run of keys in one bin costs one
+    // pair of LDS atomics (integer sums, so the order does not matter)
     uint64_t tloc = 0;
-    for (int j = threadIdx.x; j < n; j += kSelBlock) {
-      const float y = src(j) - M;
-      const int bin = coarse_bin(y);
-      const uint64_t e = fixexp(y);
-      atomicAdd(&hc[bin], 1u);
-      if (e) atomicAdd(reinterpret_cast<unsigned long long *>(&hm[bin]),
-                       static_cast<unsigned long long>(e));
-      tloc += e;
+    for (int j0 = 4 * threadIdx.x; j0 < n; j0 += 4 * kSelBlock) {
+      int cb = -1;
+      uint32_t cc = 0;
+      uint64_t cm = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (j0 + i < n) {
+          const float y = src(j0 + i) - M;
+          const int bin = coarse_bin(y);
+          const uint64_t e = fixexp(y);
+          tloc += e;
+          if (bin != cb) {
+            if (cc) atomicAdd(&hc[cb], cc);
+            if (cm) atomicAdd(reinterpret_cast<unsigned long long *>(&hm[cb]),
+                              static_cast<unsigned long long>(cm));
+            cb = bin;
+            cc = 0;
+            cm = 0;
+          }
+          cc += 1;
+          cm += e;
+        }
+      }
+      if (cc) atomicAdd(&hc[cb], cc);
+      if (cm) atomicAdd(reinterpret_cast<unsigned long long *>(&hm[cb]),
+                        static_cast<unsigned long long>(cm));
     }
     const uint64_t tot = block_sum<uint64_t>(tloc);
     __syncthreads();
