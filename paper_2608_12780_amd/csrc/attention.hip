@@ -15,7 +15,10 @@
 // (ds_read_b64_tr_b16).  K/V tiles are double buffered: the next tiles'
 // gathers are in flight during the MFMAs.  bf16 gathers go through buffer
 // resources, whose range checks turn every out-of-range index into a zero
-// read instead of a fault.
+// read instead of a fault.  At d = 128 with bf16 inputs (attn_kernel_dma)
+// the buffer unit writes the gathered rows straight into LDS; fp32 inputs
+// (rounded to bf16 on the way) and d = 64 stage rows through registers
+// (attn_kernel).
 #include <math.h>
 
 #include "common.h"
@@ -352,6 +355,229 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel(
   }
 }
 
+// bf16 inputs at d = 128: the same computation with the K/V rows gathered
+// straight into LDS by the buffer unit (one 1 KB load per 4 rows, no
+// staging registers).  Rows land unpadded, so 16-byte slots are
+// XOR-swizzled: slot = chunk ^ (row mod 16) in K tiles (16-row b128 reads)
+// and chunk ^ 4 (row mod 4) in V tiles (4-row transposing reads).  The four
+// tile buffers are distinct LDS objects, so the compiler's waits for the
+// loads into one never hold up reads of another.
+__global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
+    int n, int c_q, int items_per_head, int total_items,
+    const void *__restrict__ qv, const void *__restrict__ kv,
+    const void *__restrict__ vv, void *ov, const int32_t *__restrict__ offsets,
+    const int32_t *__restrict__ perm, const int32_t *__restrict__ sel_idx,
+    const int4 *__restrict__ items, float scale_log2) {
+  constexpr int D = 128;
+  __shared__ __attribute__((aligned(16))) uint16_t K0[kBN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t K1[kBN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t V0[kBN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t V1[kBN * D];
+
+  const int item = blockIdx.x;
+  if (item >= total_items) return;
+  const int h = item / items_per_head;
+  const int4 it = items[item];
+  const int c = it.x, row0 = it.y, rows = it.z, r = it.w;
+  if (rows <= 0) return;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int l32 = lane & 31, hf = lane >> 5;
+  const size_t hoff = static_cast<size_t>(h) * n * D;
+
+  // queries: wave w owns rows 32w + l32 of the chunk
+  const int ql = w * 32 + l32;
+  const bool qvalid = ql < rows;
+  int qi = 0;
+  if (qvalid) {
+    const int pb = offsets[static_cast<size_t>(h) * (c_q + 1) + c] + row0 + ql;
+    qi = min(max(perm[static_cast<size_t>(h) * n + min(max(pb, 0), n - 1)], 0), n - 1);
+  }
+  bf16x8 qf[D / 16];
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s)
+    qf[s] = as_bf16x8(qvalid ? load8<true>(qv, hoff + static_cast<size_t>(qi) * D + 16 * s + 8 * hf)
+                             : make_uint4(0, 0, 0, 0));
+  const bool wave_active = w * 32 < rows;
+
+  f32x16 oacc[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) oacc[db][e] = 0.0f;
+  float m_run = -INFINITY, l_run = 0.0f;
+
+  const int32_t *sel = sel_idx + (static_cast<size_t>(h) * c_q + c) * n;
+  const int ntiles = (r + kBN - 1) / kBN;
+  const __amdgpu_buffer_rsrc_t rsel = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int32_t *>(sel), static_cast<short>(0), r * 4, 0x00020000);
+  const int nbytes = static_cast<int>(static_cast<uint32_t>(n) * (D * 2));
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t *>(static_cast<const uint16_t *>(kv) + hoff), static_cast<short>(0), nbytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t *>(static_cast<const uint16_t *>(vv) + hoff), static_cast<short>(0), nbytes, 0x00020000);
+
+  // gathers: wave w brings rows 8w .. 8w+7 of each tile, four rows (1 KB)
+  // per load; lane L covers row 8w + 4i + L/16, slot L%16, and fetches the
+  // chunk that the swizzle puts there
+  auto load_idx = [&](int tile, int (&ix)[2]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      ix[i] = __builtin_amdgcn_raw_buffer_load_b32(rsel, (tile * kBN + 8 * w + 4 * i + (lane >> 4)) * 4, 0, 0);
+  };
+  auto gather = [&](uint16_t *kbuf, uint16_t *vbuf, const int (&ix)[2]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int row = 8 * w + 4 * i + (lane >> 4), s = lane & 15;
+      const int ck = s ^ (row & 15), cv = s ^ (4 * (row & 3));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, kbuf + (8 * w + 4 * i) * D, 16, ix[i] * (D * 2) + 16 * ck, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, vbuf + (8 * w + 4 * i) * D, 16, ix[i] * (D * 2) + 16 * cv, 0, 0, 0);
+    }
+  };
+
+  // transposing V reads: lane L supplies row rl = 4(L/32) + (L%16)/4 of a
+  // 16-key step, chunk 4db + 2((L/16)%2) + (L%4)/2, half L%2
+  const int rl = 4 * (lane >> 5) + ((lane & 15) >> 2);
+  const int vch = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
+  const int vsw = 4 * (rl & 3);
+  const int vhalf = 4 * (lane & 1);   // elements
+
+  auto compute = [&](int tile, const uint16_t *kt, const uint16_t *vt0) {
+    if (!wave_active) return;
+    f32x16 sacc[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sacc[kb][e] = 0.0f;
+    const int krow = l32;  // + 32 kb; the swizzle sees row mod 16 only
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const int slot = (2 * s + hf) ^ (krow & 15);
+        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4 *>(
+            &kt[(kb * 32 + krow) * D + 8 * slot]));
+        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], sacc[kb], 0, 0, 0);
+      }
+    const int kbase = tile * kBN;
+    if (kbase + kBN > r) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (kbase + 32 * kb + 8 * (e >> 2) + 4 * hf + (e & 3) >= r) sacc[kb][e] = -INFINITY;
+    }
+    float mx0 = fmaxf(sacc[0][0], sacc[0][1]), mx1 = fmaxf(sacc[1][0], sacc[1][1]);
+#pragma unroll
+    for (int e = 2; e < 16; e += 2) {
+      mx0 = fmaxf(fmaxf(mx0, sacc[0][e]), sacc[0][e + 1]);
+      mx1 = fmaxf(fmaxf(mx1, sacc[1][e]), sacc[1][e + 1]);
+    }
+    float mx = fmaxf(mx0, mx1);
+    {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+    }
+    const float mt = mx * scale_log2;
+    const bool behind = mt > m_run + kRescale;
+    if (__ballot(behind)) {
+      const float m_new = behind ? fmaxf(m_run, mt) : m_run;
+      const float alpha = behind ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) oacc[db][e] *= alpha;
+      m_run = m_new;
+    }
+    const float neg_m = -m_run;
+    uint4 pk[2][2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      float p[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) p[e] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][e], scale_log2, neg_m));
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2)
+        pk[kb][s2] = make_uint4(pack_bf16(p[8 * s2 + 0], p[8 * s2 + 1]),
+                                pack_bf16(p[8 * s2 + 2], p[8 * s2 + 3]),
+                                pack_bf16(p[8 * s2 + 4], p[8 * s2 + 5]),
+                                pack_bf16(p[8 * s2 + 6], p[8 * s2 + 7]));
+    }
+    {
+      const bf16x2 one = __builtin_bit_cast(bf16x2, 0x3F803F80u);
+      float ps[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+          const uint4 w4 = pk[kb][s2];
+          ps[0] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4.x), one, ps[0], false);
+          ps[1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4.y), one, ps[1], false);
+          ps[2] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4.z), one, ps[2], false);
+          ps[3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w4.w), one, ps[3], false);
+        }
+      l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
+    }
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+          const int vrow = kb * 32 + 16 * s2 + rl;  // hi: vrow + 8, same swizzle
+          const int slot = (4 * db + vch) ^ vsw;
+          const uint16_t *p0 = &vt0[vrow * D + 8 * slot + vhalf];
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(p0));
+          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(p0 + 8 * D));
+          const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+          const bf16x8 a = as_bf16x8(make_uint4(l2.x, l2.y, h2.x, h2.y));
+          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, as_bf16x8(pk[kb][s2]), oacc[db], 0, 0, 0);
+        }
+  };
+
+  // one step: indices of tile T+2 requested, tile T+1 gathered into the free
+  // buffers, tile T computed; every wave's gathers land before the barrier
+  int cidx[2], nidx[2];
+  auto step = [&](int tile, const uint16_t *kc, const uint16_t *vc, uint16_t *kn, uint16_t *vn) {
+    load_idx(tile + 2, nidx);
+    gather(kn, vn, cidx);
+    compute(tile, kc, vc);
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's gathers are in LDS
+    __syncthreads();
+    cidx[0] = nidx[0];
+    cidx[1] = nidx[1];
+  };
+
+  if (ntiles > 0) {
+    int ix0[2];
+    load_idx(0, ix0);
+    load_idx(1, cidx);
+    gather(K0, V0, ix0);
+  }
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  __syncthreads();
+  for (int tile = 0; tile < ntiles; tile += 2) {
+    step(tile, K0, V0, K1, V1);
+    if (tile + 1 < ntiles) step(tile + 1, K1, V1, K0, V0);
+  }
+
+  // lanes l and l^32 hold the two halves of one query's row sum
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (!qvalid) return;
+  const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int dim = db * 32 + 8 * i + 4 * hf;
+      const size_t at = hoff + static_cast<size_t>(qi) * D + dim;
+      const float o0 = oacc[db][4 * i + 0] * inv, o1 = oacc[db][4 * i + 1] * inv;
+      const float o2 = oacc[db][4 * i + 2] * inv, o3 = oacc[db][4 * i + 3] * inv;
+      *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(ov) + at) =
+          make_uint2(pack_bf16(o0, o1), pack_bf16(o2, o3));
+    }
+}
+
 // Work list of one head: every cluster's queries cut into chunks of kBM rows,
 // clusters in order; unused slots get rows = 0.
 __global__ __launch_bounds__(1024) void attn_items_kernel(
@@ -399,7 +625,11 @@ hipError_t launch_attn(int heads, int n, bool bf16, const void *q,
                        float scale_log2, hipStream_t s) {
   const int total = iph * heads;
   const dim3 grid(total), block(kNW * 64);
-  if (bf16)
+  if (bf16 && D == 128)
+    hipLaunchKernelGGL(attn_kernel_dma, grid, block, 0, s, n, c_q, iph,
+                       total, q, k, v, o, offsets, perm, sel_idx, items,
+                       scale_log2);
+  else if (bf16)
     hipLaunchKernelGGL((attn_kernel<D, true>), grid, block, 0, s, n, c_q, iph,
                        total, q, k, v, o, offsets, perm, sel_idx, items,
                        scale_log2);
