@@ -424,13 +424,18 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
     for (int i = 0; i < 2; ++i)
       ix[i] = __builtin_amdgcn_raw_buffer_load_b32(rsel, (tile * kBN + 8 * w + 4 * i + (lane >> 4)) * 4, 0, 0);
   };
-  auto gather = [&](uint16_t *kbuf, uint16_t *vbuf, const int (&ix)[2]) {
+  auto gather_k = [&](uint16_t *kbuf, const int (&ix)[2]) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int row = 8 * w + 4 * i + (lane >> 4), s = lane & 15;
-      const int ck = s ^ (row & 15), cv = s ^ (4 * (row & 3));
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, kbuf + (8 * w + 4 * i) * D, 16, ix[i] * (D * 2) + 16 * ck, 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, vbuf + (8 * w + 4 * i) * D, 16, ix[i] * (D * 2) + 16 * cv, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, kbuf + (8 * w + 4 * i) * D, 16, ix[i] * (D * 2) + 16 * (s ^ (row & 15)), 0, 0, 0);
+    }
+  };
+  auto gather_v = [&](uint16_t *vbuf, const int (&ix)[2]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int row = 8 * w + 4 * i + (lane >> 4), s = lane & 15;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, vbuf + (8 * w + 4 * i) * D, 16, ix[i] * (D * 2) + 16 * (s ^ (4 * (row & 3))), 0, 0, 0);
     }
   };
 
@@ -441,8 +446,15 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
   const int vsw = 4 * (rl & 3);
   const int vhalf = 4 * (lane & 1);   // elements
 
-  auto compute = [&](int tile, const uint16_t *kt, const uint16_t *vt0) {
-    if (!wave_active) return;
+  // tile T from kt/vt0; the gathers of the next tile into kn/vn are issued
+  // between the phases: K rows after the S MFMAs, V rows before the PV MFMAs
+  auto compute = [&](int tile, const uint16_t *kt, const uint16_t *vt0, uint16_t *kn,
+                     uint16_t *vn, const int (&ix)[2]) {
+    if (!wave_active) {
+      gather_k(kn, ix);
+      gather_v(vn, ix);
+      return;
+    }
     f32x16 sacc[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -458,6 +470,15 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
             &kt[(kb * 32 + krow) * D + 8 * slot]));
         sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[s], sacc[kb], 0, 0, 0);
       }
+    // each K operand is read from LDS two MFMAs ahead of its use
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+    for (int i = 0; i < 14; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    gather_k(kn, ix);
     const int kbase = tile * kBN;
     if (kbase + kBN > r) {
 #pragma unroll
@@ -518,6 +539,7 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
         }
       l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
     }
+    gather_v(vn, ix);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -535,13 +557,13 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
         }
   };
 
-  // one step: indices of tile T+2 requested, tile T+1 gathered into the free
-  // buffers, tile T computed; every wave's gathers land before the barrier
+  // one step: indices of tile T+2 requested, tile T computed while tile T+1
+  // is gathered into the free buffers; every wave's gathers land before the
+  // barrier
   int cidx[2], nidx[2];
   auto step = [&](int tile, const uint16_t *kc, const uint16_t *vc, uint16_t *kn, uint16_t *vn) {
     load_idx(tile + 2, nidx);
-    gather(kn, vn, cidx);
-    compute(tile, kc, vc);
+    compute(tile, kc, vc, kn, vn, cidx);
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's gathers are in LDS
     __syncthreads();
     cidx[0] = nidx[0];
@@ -552,7 +574,8 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
     int ix0[2];
     load_idx(0, ix0);
     load_idx(1, cidx);
-    gather(K0, V0, ix0);
+    gather_k(K0, ix0);
+    gather_v(V0, ix0);
   }
   __builtin_amdgcn_s_waitcnt(0x0F70);
   __syncthreads();
