@@ -262,6 +262,15 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
         const f32x16 cur = chain(rb);
         fold(prev, rb - 32);
         prev = cur;
+        // each MFMA of this block is followed by an LDS read and a share
+        // of the previous block's fold
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+        for (int k = 0; k < 2 * KS; ++k) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+        }
       }
       fold(prev, cpad - 32);
       {

@@ -18,22 +18,41 @@ struct TableGeom {
 };
 
 // P[h][c][col] = <qbar_c[I_m], u_r^m>, fp32 fma chain in channel order.
-__global__ void tables_kernel(int d, int c_q, int per_head, TableGeom g,
-                              const float *__restrict__ qc,
-                              const float *__restrict__ kc, float *tables) {
-  const int col = blockIdx.x * blockDim.x + threadIdx.x;
-  const int c = blockIdx.y, h = blockIdx.z;
+// A block takes kTabC clusters of one head: their centroid rows are staged
+// in LDS, and each thread runs the kTabC independent chains of one table
+// column (one codebook row read once for all of them).
+constexpr int kTabC = 8;
+constexpr int kTabMaxD = 128;
+__global__ __launch_bounds__(256) void tables_kernel(int d, int c_q, int per_head, TableGeom g,
+                                                     const float *__restrict__ qc,
+                                                     const float *__restrict__ kc, float *tables) {
+  __shared__ float qs[kTabC][kTabMaxD];
+  const int c0 = blockIdx.x * kTabC, h = blockIdx.y;
   const int cs = g.col[g.M];
-  if (col >= cs) return;
-  int m = 0;
-  while (m + 1 < g.M && col >= g.col[m + 1]) ++m;
-  const int r = col - g.col[m];
-  const float *q = qc + (static_cast<size_t>(h) * c_q + c) * d + g.off[m];
-  const float *u = kc + static_cast<size_t>(h) * per_head + g.ucol[m] +
-                   static_cast<size_t>(r) * g.len[m];
-  float acc = 0.0f;
-  for (int ch = 0; ch < g.len[m]; ++ch) acc = fmaf(q[ch], u[ch], acc);
-  tables[(static_cast<size_t>(h) * c_q + c) * cs + col] = acc;
+  const int nc = c_q - c0 < kTabC ? c_q - c0 : kTabC;
+  for (int e = threadIdx.x; e < kTabC * d; e += blockDim.x) {
+    const int k = e / d, ch = e % d;
+    qs[k][ch] = k < nc ? qc[(static_cast<size_t>(h) * c_q + c0 + k) * d + ch] : 0.0f;
+  }
+  __syncthreads();
+  for (int col = threadIdx.x; col < cs; col += blockDim.x) {
+    int m = 0;
+    while (m + 1 < g.M && col >= g.col[m + 1]) ++m;
+    const int r = col - g.col[m], len = g.len[m], off = g.off[m];
+    const float *u = kc + static_cast<size_t>(h) * per_head + g.ucol[m] +
+                     static_cast<size_t>(r) * len;
+    float acc[kTabC];
+#pragma unroll
+    for (int k = 0; k < kTabC; ++k) acc[k] = 0.0f;
+    for (int ch = 0; ch < len; ++ch) {
+      const float uv = u[ch];
+#pragma unroll
+      for (int k = 0; k < kTabC; ++k) acc[k] = fmaf(qs[k][off + ch], uv, acc[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < kTabC; ++k)
+      if (k < nc) tables[(static_cast<size_t>(h) * c_q + c0 + k) * cs + col] = acc[k];
+  }
 }
 
 __global__ void logits_kernel(int n, int c_q, int cs, int cT, int cTH,
@@ -79,8 +98,9 @@ hipError_t score_tables(int heads, int d, const int *off, const int *len,
     ucol += sub.c[m] * len[m];
   }
   g.col[sub.M] = col;
-  hipLaunchKernelGGL(tables_kernel, dim3((col + 127) / 128, c_q, heads),
-                     dim3(128), 0, s, d, c_q, ucol, g, qc, kc, tables);
+  if (d > kTabMaxD) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(tables_kernel, dim3((c_q + kTabC - 1) / kTabC, heads),
+                     dim3(256), 0, s, d, c_q, ucol, g, qc, kc, tables);
   return hipGetLastError();
 }
 
