@@ -177,6 +177,7 @@ struct SelectWs {
   float *row_max;
   uint32_t *row_state;
   uint32_t *coarse_hist;
+  uint32_t *dedup;
 };
 size_t select_ws(const scope_shape *s, int c_q, void *base, SelectWs *w) {
   Carver cv(base);
@@ -184,6 +185,7 @@ size_t select_ws(const scope_shape *s, int c_q, void *base, SelectWs *w) {
   sw.row_max = cv.take<float>(static_cast<size_t>(s->heads) * c_q);
   sw.row_state = cv.take<uint32_t>(static_cast<size_t>(s->heads) * c_q * 4);
   sw.coarse_hist = cv.take<uint32_t>(static_cast<size_t>(s->heads) * c_q * scope::kSelCoarseBins);
+  sw.dedup = cv.take<uint32_t>(scope::select_dedup_words(s->heads, s->n));
   if (w) *w = sw;
   return cv.used;
 }
@@ -534,7 +536,7 @@ int32_t scope_select_policy(const scope_shape *shape, int32_t c_q,
                               shape->d, scores, tables, codes, nullptr, counts,
                               rho, k_fix,
                               base_counts, topp_counts, k_head, sel_counts,
-                              sel_idx, w.row_max, w.row_state, w.coarse_hist, policy,
+                              sel_idx, w.row_max, w.row_state, w.coarse_hist, w.dedup, policy,
                               static_cast<hipStream_t>(stream)));
   return SCOPE_OK;
 }
@@ -711,7 +713,7 @@ int32_t scope_select_partition(const scope_shape *shape, int32_t c_q,
   SCOPE_TRY(scope::select_run(shape->heads, shape->n, c_q, part_subspaces(part_geom(part)),
                               shape->d, scores, tables, nullptr, codes, counts, rho,
                               k_fix, base_counts, topp_counts, k_head, sel_counts,
-                              sel_idx, w.row_max, w.row_state, w.coarse_hist, policy,
+                              sel_idx, w.row_max, w.row_state, w.coarse_hist, w.dedup, policy,
                               static_cast<hipStream_t>(stream)));
   return SCOPE_OK;
 }

@@ -131,8 +131,10 @@ hipError_t select_run(int heads, int n, int c_q, const Subspaces &sub, int d,
                       const int32_t *counts, float rho,
                       int k_fix, int32_t *base, int32_t *topp, int32_t *k_head,
                       int32_t *sel_counts, int32_t *sel_idx, float *row_max,
-                      uint32_t *row_state, uint32_t *coarse_hist, int policy,
-                      hipStream_t s);
+                      uint32_t *row_state, uint32_t *coarse_hist, uint32_t *dedup,
+                      int policy, hipStream_t s);
+// 32-bit words of the distinct-code scratch of select_run
+size_t select_dedup_words(int heads, int n);
 constexpr int kSelCoarseBins = 2048;  // coarse histogram bins per cluster row
 hipError_t debug_fixexp(const float *y, uint64_t *out, int64_t count,
                         hipStream_t s);

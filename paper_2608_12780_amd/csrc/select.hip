@@ -13,6 +13,12 @@
 //   t = (#keys above) + ceil((T - mass above) / E*) (Eq. 7);
 //   b = max(t, k_fix) (Eq. 8).  The coarse count histogram is kept for the
 //   final kernel.
+// Logits depend on a key only through its composite code (Eq. 6), so with
+// packed codes the passes that only need per-logit counts and masses (max,
+// coarse histogram, crossing-bin gathers and digit rounds) run over the
+// head's distinct codes, each weighted by how many keys carry it (built once
+// per call by hashing the codes into per-part LDS tables).  Only the final
+// compaction, which emits key indices, visits every key.
 // head kernel: k_head = ceil(sum n_c b_c / sum n_c) in integers (Eq. 9),
 //   r_c = max(b_c, k_head) (Eq. 10), or for the Fig. 6 variants r_c = b_c
 //   (fixed floor) or r_c = t_c (pure Top-p).
@@ -118,27 +124,37 @@ __device__ Crossing find_crossing(const uint32_t *hc, const uint64_t *hm,
 // Where a cluster row's logits come from: the materialised scores, or the
 // table row (staged in LDS) and the key codes, packed (three subspaces) or
 // one uint16 plane per subspace.
-constexpr int kFromScores = 0, kFromPacked = 1, kFromPlanes = 2;
+constexpr int kFromScores = 0, kFromPacked = 1, kFromPlanes = 2, kFromUnique = 3;
 
 struct CodeBooks {
   const uint32_t *packed;  // [heads][n], KIND == kFromPacked
   const uint16_t *planes;  // [heads][M][n], KIND == kFromPlanes
+  const uint32_t *ucodes;  // [heads][n]: distinct packed codes, KIND == kFromUnique
+  const uint32_t *umult;   // [heads][n]: keys carrying each of them
+  const int *ucount;       // [heads]: number of distinct codes
   CodePlanes cp;           // M and the table columns of each subspace
 };
 
+// Entry j of a row: its logit and how many keys it stands for (1 except
+// for distinct codes); count is the number of entries.
 template <int KIND>
 struct LogitSource {
   const float *P;          // LDS table row or global score row
-  const uint32_t *packed;  // codes of this head
+  const uint32_t *packed;  // codes of this head (or its distinct codes)
+  const uint32_t *mult;
   const uint16_t *planes;
   CodePlanes cp;
   size_t n;
+  int count;
   float sigma;
   __device__ __forceinline__ float operator()(int j) const {
     if (KIND == kFromScores) return P[j];
-    if (KIND == kFromPacked)
+    if (KIND == kFromPacked || KIND == kFromUnique)
       return proxy_logit(P, cp.col[1], cp.col[2], cp.col[3], packed[j], sigma);
     return proxy_logit_planes(P, cp, planes, n, j, sigma);
+  }
+  __device__ __forceinline__ uint32_t weight(int j) const {
+    return KIND == kFromUnique ? mult[j] : 1u;
   }
 };
 
@@ -150,7 +166,15 @@ __device__ LogitSource<KIND> make_source(float *lut, int h, int c, int n, int c_
   src.cp = cb.cp;
   src.n = static_cast<size_t>(n);
   src.sigma = sigma;
-  src.packed = cb.packed ? cb.packed + static_cast<size_t>(h) * n : nullptr;
+  src.count = n;
+  src.mult = nullptr;
+  if (KIND == kFromUnique) {
+    src.packed = cb.ucodes + static_cast<size_t>(h) * n;
+    src.mult = cb.umult + static_cast<size_t>(h) * n;
+    src.count = min(max(cb.ucount[h], 0), n);
+  } else {
+    src.packed = cb.packed ? cb.packed + static_cast<size_t>(h) * n : nullptr;
+  }
   src.planes = cb.planes ? cb.planes + static_cast<size_t>(h) * cb.cp.M * n : nullptr;
   if (KIND != kFromScores) {
     const int cs = cb.cp.col[cb.cp.M];
@@ -182,13 +206,13 @@ __device__ void refine(Visit visit, float M, uint64_t target, uint32_t *hc,
       if (BY_MASS) hm[b] = 0;
     }
     __syncthreads();
-    visit([&](float s) {
+    visit([&](float s, uint32_t wt) {
       const uint32_t key = desc_key(s);
       if ((key & pmask) != prefix) return;
       const int dig = (key >> sh) & (nb - 1);
-      atomicAdd(&hc[dig], 1u);
+      atomicAdd(&hc[dig], wt);
       if (BY_MASS) {
-        const uint64_t e = fixexp(s - M);
+        const uint64_t e = fixexp(s - M) * wt;
         if (e) atomicAdd(reinterpret_cast<unsigned long long *>(&hm[dig]),
                          static_cast<unsigned long long>(e));
       }
@@ -208,11 +232,12 @@ __device__ void refine(Visit visit, float M, uint64_t target, uint32_t *hc,
 // reserved per wave); returns how many there are (more than kCand: the
 // list is incomplete and the caller visits all keys instead).
 template <int KIND>
-__device__ int gather_bin(const LogitSource<KIND> &src, int n, float M, int cbin,
-                          float *cand, int *ncand) {
+__device__ int gather_bin(const LogitSource<KIND> &src, float M, int cbin,
+                          float *cand, uint32_t *candw, int *ncand) {
   if (threadIdx.x == 0) *ncand = 0;
   __syncthreads();
   const int lane = threadIdx.x & 63;
+  const int n = src.count;
   for (int j0 = 0; j0 < n; j0 += kSelBlock) {
     const int j = j0 + threadIdx.x;
     float s = 0.0f;
@@ -229,7 +254,10 @@ __device__ int gather_bin(const LogitSource<KIND> &src, int n, float M, int cbin
       first = __shfl(first, __ffsll(static_cast<long long>(mask)) - 1);
       const int slot = first + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
           static_cast<uint32_t>(mask >> 32), __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u)));
-      if (in && slot < kCand) cand[slot] = s;
+      if (in && slot < kCand) {
+        cand[slot] = s;
+        candw[slot] = src.weight(j);
+      }
     }
   }
   __syncthreads();
@@ -241,20 +269,20 @@ __device__ int gather_bin(const LogitSource<KIND> &src, int n, float M, int cbin
 // Exact crossing key inside coarse bin `cbin`: over the gathered list when
 // it is complete, else over all keys.
 template <int KIND, bool BY_MASS>
-__device__ void refine_bin(const LogitSource<KIND> &src, int n, float M, int cbin,
+__device__ void refine_bin(const LogitSource<KIND> &src, float M, int cbin,
                            uint64_t target, uint32_t *hc, uint64_t *hm, float *cand,
-                           int *ncand, uint32_t *key_out, uint32_t *cnt_above,
-                           uint64_t *mass_above) {
-  const int cnt = gather_bin<KIND>(src, n, M, cbin, cand, ncand);
+                           uint32_t *candw, int *ncand, uint32_t *key_out,
+                           uint32_t *cnt_above, uint64_t *mass_above) {
+  const int cnt = gather_bin<KIND>(src, M, cbin, cand, candw, ncand);
   if (cnt <= kCand) {
     refine<BY_MASS>([&](auto f) {
-      for (int k = threadIdx.x; k < cnt; k += kSelBlock) f(cand[k]);
+      for (int k = threadIdx.x; k < cnt; k += kSelBlock) f(cand[k], candw[k]);
     }, M, target, hc, hm, key_out, cnt_above, mass_above);
   } else {
     refine<BY_MASS>([&](auto f) {
-      for (int j = threadIdx.x; j < n; j += kSelBlock) {
+      for (int j = threadIdx.x; j < src.count; j += kSelBlock) {
         const float s = src(j);
-        if (coarse_bin(s - M) == cbin) f(s);
+        if (coarse_bin(s - M) == cbin) f(s, src.weight(j));
       }
     }, M, target, hc, hm, key_out, cnt_above, mass_above);
   }
@@ -269,13 +297,15 @@ __global__ __launch_bounds__(kSelBlock) void select_base_kernel(
   __shared__ uint32_t hc[kCoarseBins];
   __shared__ uint64_t hm[kCoarseBins];
   __shared__ float cand[kCand];
+  __shared__ uint32_t candw[kCand];
   __shared__ int ncand;
   const int c = blockIdx.x, h = blockIdx.y;
   const size_t row = static_cast<size_t>(h) * c_q + c;
   const LogitSource<KIND> src =
       make_source<KIND>(lut, h, c, n, c_q, cb, sigma, scores, tables);
+  const int ne = src.count;
   float mloc = -INFINITY;
-  for (int j = threadIdx.x; j < n; j += kSelBlock) mloc = fmaxf(mloc, src(j));
+  for (int j = threadIdx.x; j < ne; j += kSelBlock) mloc = fmaxf(mloc, src(j));
   const float M = block_max(mloc);
   int t_p = n;
   uint32_t key_star = 0, above_star = 0;
@@ -285,19 +315,20 @@ __global__ __launch_bounds__(kSelBlock) void select_base_kernel(
       hm[b] = 0;
     }
     __syncthreads();
-    // four consecutive keys per thread: a run of keys in one bin costs one
-    // pair of LDS atomics (integer sums, so the order does not matter)
+    // four consecutive entries per thread: a run of them in one bin costs
+    // one pair of LDS atomics (integer sums, so the order does not matter)
     uint64_t tloc = 0;
-    for (int j0 = 4 * threadIdx.x; j0 < n; j0 += 4 * kSelBlock) {
+    for (int j0 = 4 * threadIdx.x; j0 < ne; j0 += 4 * kSelBlock) {
       int cb = -1;
       uint32_t cc = 0;
       uint64_t cm = 0;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        if (j0 + i < n) {
+        if (j0 + i < ne) {
           const float y = src(j0 + i) - M;
+          const uint32_t wt = src.weight(j0 + i);
           const int bin = coarse_bin(y);
-          const uint64_t e = fixexp(y);
+          const uint64_t e = fixexp(y) * wt;
           tloc += e;
           if (bin != cb) {
             if (cc) atomicAdd(&hc[cb], cc);
@@ -307,7 +338,7 @@ __global__ __launch_bounds__(kSelBlock) void select_base_kernel(
             cc = 0;
             cm = 0;
           }
-          cc += 1;
+          cc += wt;
           cm += e;
         }
       }
@@ -324,7 +355,7 @@ __global__ __launch_bounds__(kSelBlock) void select_base_kernel(
     const Crossing x = find_crossing<true>(hc, hm, kCoarseBins, 0, T);
     uint32_t cnt_above = x.cnt_before;
     uint64_t mass_above = x.mass_before;
-    refine_bin<KIND, true>(src, n, M, x.bin, T, hc, hm, cand, &ncand, &key_star,
+    refine_bin<KIND, true>(src, M, x.bin, T, hc, hm, cand, candw, &ncand, &key_star,
                             &cnt_above, &mass_above);
     const float s_star = desc_key_value(key_star);
     const uint64_t e_star = fixexp(s_star - M);
@@ -367,7 +398,7 @@ __global__ __launch_bounds__(kSelBlock) void select_head_kernel(
   }
 }
 
-template <int KIND>
+template <int KIND, int RKIND>
 __global__ __launch_bounds__(kSelBlock) void select_final_kernel(
     int n, int c_q, CodeBooks cb, float sigma, const float *__restrict__ scores,
     const float *__restrict__ tables, const int32_t *__restrict__ sel_counts, const float *__restrict__ row_max,
@@ -376,6 +407,7 @@ __global__ __launch_bounds__(kSelBlock) void select_final_kernel(
   __shared__ float lut[kMaxTable];
   __shared__ uint32_t hc[kCoarseBins];
   __shared__ float cand[kCand];
+  __shared__ uint32_t candw[kCand];
   __shared__ int ncand;
   const int c = blockIdx.x, h = blockIdx.y;
   const size_t row = static_cast<size_t>(h) * c_q + c;
@@ -402,8 +434,23 @@ __global__ __launch_bounds__(kSelBlock) void select_final_kernel(
                                             static_cast<uint64_t>(r));
     above = x.cnt_before;
     uint64_t unused = 0;
-    refine_bin<KIND, false>(src, n, M, x.bin, static_cast<uint64_t>(r), hc, nullptr,
-                             cand, &ncand, &key_r, &above, &unused);
+    LogitSource<RKIND> rsrc;
+    rsrc.P = src.P;
+    rsrc.packed = src.packed;
+    rsrc.mult = src.mult;
+    rsrc.planes = src.planes;
+    rsrc.cp = src.cp;
+    rsrc.n = src.n;
+    rsrc.count = src.count;
+    rsrc.sigma = src.sigma;
+    if (RKIND != KIND) {
+      // the same table row (already in LDS), over the distinct codes
+      rsrc.packed = cb.ucodes + static_cast<size_t>(h) * n;
+      rsrc.mult = cb.umult + static_cast<size_t>(h) * n;
+      rsrc.count = min(max(cb.ucount[h], 0), n);
+    }
+    refine_bin<RKIND, false>(rsrc, M, x.bin, static_cast<uint64_t>(r), hc, nullptr,
+                             cand, candw, &ncand, &key_r, &above, &unused);
   }
   // ordered compaction, four consecutive keys per thread: keys above key_r
   // and the first `need` ties in index order
@@ -439,6 +486,113 @@ __global__ __launch_bounds__(kSelBlock) void select_final_kernel(
   }
 }
 
+// Distinct packed codes of every head.  Only the low 30 bits of a code (its
+// three 10-bit fields) reach a logit, so they are the key; 0xFFFFFFFF marks
+// a free slot.  The code space is hashed into P parts of a head; block
+// (part, head) reads all of the head's codes and counts the ones of its
+// part in an LDS table with open addressing, then stores the part's
+// (code, count) pairs.  P is chosen so that the tables are at most half
+// full even if every key has its own code; should a skewed part still fill
+// its table, the head falls back to one entry per key (count 1), which the
+// selection treats exactly like the keys themselves.
+constexpr uint32_t kFreeSlot = 0xFFFFFFFFu;
+constexpr int kPartSlots = 16384;   // LDS table of one part: 128 KB
+
+__device__ __forceinline__ uint32_t code_hash(uint32_t code) { return code * 0x9E3779B1u; }
+
+__global__ void code_parts_clear_kernel(int *overflow, int heads) {
+  for (int h = blockIdx.x * blockDim.x + threadIdx.x; h < heads; h += gridDim.x * blockDim.x)
+    overflow[h] = 0;
+}
+
+__global__ __launch_bounds__(kSelBlock) void code_parts_kernel(
+    const uint32_t *__restrict__ codes, int n, int parts, uint32_t *stage_codes,
+    uint32_t *stage_mult, int *part_count, int *overflow) {
+  __shared__ uint32_t lk[kPartSlots];
+  __shared__ uint32_t lc[kPartSlots];
+  __shared__ int full;
+  const int p = blockIdx.x, h = blockIdx.y;
+  for (int i = threadIdx.x; i < kPartSlots; i += kSelBlock) {
+    lk[i] = kFreeSlot;
+    lc[i] = 0;
+  }
+  if (threadIdx.x == 0) full = 0;
+  __syncthreads();
+  const uint32_t *hc = codes + static_cast<size_t>(h) * n;
+  for (int j = threadIdx.x; j < n; j += kSelBlock) {
+    const uint32_t code = hc[j] & 0x3FFFFFFFu;
+    const uint32_t hv = code_hash(code);
+    if (static_cast<int>((static_cast<uint64_t>(hv) * parts) >> 32) != p) continue;
+    uint32_t slot = hv & (kPartSlots - 1);
+    bool done = false;
+    for (int probe = 0; probe < kPartSlots; ++probe) {
+      const uint32_t prev = atomicCAS(&lk[slot], kFreeSlot, code);
+      if (prev == kFreeSlot || prev == code) {
+        atomicAdd(&lc[slot], 1u);
+        done = true;
+        break;
+      }
+      slot = (slot + 1u) & (kPartSlots - 1);
+    }
+    if (!done) full = 1;
+  }
+  __syncthreads();
+  if (full) {
+    if (threadIdx.x == 0) atomicOr(&overflow[h], 1);
+    return;
+  }
+  // the part's pairs, in slot order
+  constexpr int per = kPartSlots / kSelBlock;
+  uint32_t mine = 0;
+#pragma unroll
+  for (int k = 0; k < per; ++k) mine += lk[threadIdx.x * per + k] != kFreeSlot;
+  uint32_t total;
+  uint32_t at = block_excl_scan<uint32_t>(mine, &total);
+  const size_t base = (static_cast<size_t>(h) * parts + p) * kPartSlots;
+#pragma unroll
+  for (int k = 0; k < per; ++k) {
+    const int i = threadIdx.x * per + k;
+    if (lk[i] != kFreeSlot) {
+      stage_codes[base + at] = lk[i];
+      stage_mult[base + at] = lc[i];
+      ++at;
+    }
+  }
+  if (threadIdx.x == 0) part_count[static_cast<size_t>(h) * parts + p] = static_cast<int>(total);
+}
+
+// One block per head: the parts' pairs concatenated into the head's list,
+// or one entry per key after an overflow.
+__global__ __launch_bounds__(kSelBlock) void code_parts_gather_kernel(
+    const uint32_t *__restrict__ codes, int n, int parts, const uint32_t *__restrict__ stage_codes,
+    const uint32_t *__restrict__ stage_mult, const int *__restrict__ part_count,
+    const int *__restrict__ overflow, uint32_t *ucodes, uint32_t *umult, int *ucount) {
+  const int h = blockIdx.x;
+  uint32_t *uc = ucodes + static_cast<size_t>(h) * n;
+  uint32_t *um = umult + static_cast<size_t>(h) * n;
+  if (overflow[h]) {
+    for (int j = threadIdx.x; j < n; j += kSelBlock) {
+      uc[j] = codes[static_cast<size_t>(h) * n + j] & 0x3FFFFFFFu;
+      um[j] = 1u;
+    }
+    if (threadIdx.x == 0) ucount[h] = n;
+    return;
+  }
+  int off = 0;
+  for (int p = 0; p < parts; ++p) {
+    const int cnt = part_count[static_cast<size_t>(h) * parts + p];
+    const size_t base = (static_cast<size_t>(h) * parts + p) * kPartSlots;
+    for (int i = threadIdx.x; i < cnt; i += kSelBlock) {
+      if (off + i < n) {
+        uc[off + i] = stage_codes[base + i];
+        um[off + i] = stage_mult[base + i];
+      }
+    }
+    off += cnt;
+  }
+  if (threadIdx.x == 0) ucount[h] = off < n ? off : n;
+}
+
 __global__ void fixexp_kernel(const float *y, uint64_t *out, int64_t count) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i < count) out[i] = fixexp(y[i]);
@@ -446,13 +600,24 @@ __global__ void fixexp_kernel(const float *y, uint64_t *out, int64_t count) {
 
 }  // namespace
 
+int code_parts(int n) {
+  const long long p = (2LL * n + kPartSlots - 1) / kPartSlots;
+  return p < 1 ? 1 : static_cast<int>(p);
+}
+
+size_t select_dedup_words(int heads, int n) {
+  const size_t parts = static_cast<size_t>(code_parts(n));
+  return static_cast<size_t>(heads) *
+         (2 * parts * kPartSlots + parts + 2 * static_cast<size_t>(n) + 2);
+}
+
 hipError_t select_run(int heads, int n, int c_q, const Subspaces &sub, int d,
                       const float *scores, const float *tables,
                       const uint32_t *codes32, const uint16_t *codes16,
                       const int32_t *counts, float rho, int k_fix, int32_t *base,
                       int32_t *topp, int32_t *k_head, int32_t *sel_counts,
                       int32_t *sel_idx, float *row_max, uint32_t *row_state,
-                      uint32_t *coarse_hist, int policy, hipStream_t s) {
+                      uint32_t *coarse_hist, uint32_t *dedup, int policy, hipStream_t s) {
   CodeBooks cb{};
   cb.packed = codes32;
   cb.planes = codes16;
@@ -461,26 +626,51 @@ hipError_t select_run(int heads, int n, int c_q, const Subspaces &sub, int d,
   const int kind = scores ? kFromScores : codes16 ? kFromPlanes : kFromPacked;
   const float sigma = static_cast<float>(1.0 / sqrt(static_cast<double>(d)));
   const dim3 grid(c_q, heads), block(kSelBlock);
+  hipError_t e = hipSuccess;
+  if (kind == kFromPacked) {
+    // the head's distinct codes and their multiplicities
+    const int parts = code_parts(n);
+    const size_t stage = static_cast<size_t>(heads) * parts * kPartSlots;
+    uint32_t *stage_codes = dedup;
+    uint32_t *stage_mult = stage_codes + stage;
+    uint32_t *ucodes = stage_mult + stage;
+    uint32_t *umult = ucodes + static_cast<size_t>(heads) * n;
+    int *part_count = reinterpret_cast<int *>(umult + static_cast<size_t>(heads) * n);
+    int *ucount = part_count + static_cast<size_t>(heads) * parts;
+    int *overflow = ucount + heads;
+    hipLaunchKernelGGL(code_parts_clear_kernel, dim3((heads + 255) / 256), dim3(256), 0, s,
+                       overflow, heads);
+    hipLaunchKernelGGL(code_parts_kernel, dim3(parts, heads), dim3(kSelBlock), 0, s, codes32, n,
+                       parts, stage_codes, stage_mult, part_count, overflow);
+    hipLaunchKernelGGL(code_parts_gather_kernel, dim3(heads), dim3(kSelBlock), 0, s, codes32, n,
+                       parts, stage_codes, stage_mult, part_count, overflow, ucodes, umult,
+                       ucount);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    cb.ucodes = ucodes;
+    cb.umult = umult;
+    cb.ucount = ucount;
+  }
 #define SCOPE_SEL_BASE(K)                                                          \
   hipLaunchKernelGGL(select_base_kernel<K>, grid, block, 0, s, n, c_q, cb, sigma,  \
                      scores, tables, rho, k_fix, base, topp, row_max, row_state, \
                      coarse_hist)
-#define SCOPE_SEL_FINAL(K)                                                         \
-  hipLaunchKernelGGL(select_final_kernel<K>, grid, block, 0, s, n, c_q, cb, sigma, \
-                     scores, tables, sel_counts, row_max, row_state, coarse_hist, \
-                     sel_idx)
+#define SCOPE_SEL_FINAL(K, R)                                                      \
+  hipLaunchKernelGGL((select_final_kernel<K, R>), grid, block, 0, s, n, c_q, cb,   \
+                     sigma, scores, tables, sel_counts, row_max, row_state,       \
+                     coarse_hist, sel_idx)
   if (kind == kFromScores) SCOPE_SEL_BASE(kFromScores);
-  else if (kind == kFromPacked) SCOPE_SEL_BASE(kFromPacked);
+  else if (kind == kFromPacked) SCOPE_SEL_BASE(kFromUnique);
   else SCOPE_SEL_BASE(kFromPlanes);
-  hipError_t e = hipGetLastError();
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(select_head_kernel, dim3(heads), block, 0, s, c_q, counts,
                      base, row_state, policy, k_head, sel_counts);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (kind == kFromScores) SCOPE_SEL_FINAL(kFromScores);
-  else if (kind == kFromPacked) SCOPE_SEL_FINAL(kFromPacked);
-  else SCOPE_SEL_FINAL(kFromPlanes);
+  if (kind == kFromScores) SCOPE_SEL_FINAL(kFromScores, kFromScores);
+  else if (kind == kFromPacked) SCOPE_SEL_FINAL(kFromPacked, kFromUnique);
+  else SCOPE_SEL_FINAL(kFromPlanes, kFromPlanes);
 #undef SCOPE_SEL_BASE
 #undef SCOPE_SEL_FINAL
   return hipGetLastError();

@@ -322,3 +322,63 @@ def test_chunked_codebook_with_tied_centroids():
     x.q_bits[0] = inputs.bf16_bits(x.q[0])
     ref = _queries_case(cfg, x)
     assert (ref["counts"] == 0).sum() >= 290
+
+
+def _select_from_codes(tables_np, codes_np, counts_np, d, c_m, rho, k_fix):
+    """scope_select on given tables and packed codes (logits fused from the
+    LUT), against the oracle's selection on the oracle's proxy logits."""
+    H, C, _ = tables_np.shape
+    n = codes_np.shape[1]
+    shape = B.make_shape(H, n, d, B.BF16, ((0, d // 4, d // 2), (d // 4, d // 4, d // 2)))
+    dev = "cuda"
+    tables = torch.from_numpy(tables_np).to(dev)
+    codes = torch.from_numpy(codes_np.view(np.int32)).to(dev)
+    counts = torch.from_numpy(counts_np).to(dev)
+    i32 = dict(dtype=torch.int32, device=dev)
+    base = torch.empty(H, C, **i32)
+    topp = torch.empty(H, C, **i32)
+    kh = torch.empty(H, **i32)
+    sc = torch.empty(H, C, **i32)
+    idx = torch.empty(H, C, n, **i32)
+    ws = B.alloc_workspace(shape, C, c_m, dev)
+    B.scope_select(shape, C, c_m, None, tables, codes, counts, rho, k_fix, base, topp,
+                   kh, sc, idx, ws)
+    torch.cuda.synchronize()
+    gpu = dict(base=base.cpu().numpy(), topp=topp.cpu().numpy(), k_head=kh.cpu().numpy(),
+               sel_counts=sc.cpu().numpy(), sel_idx=idx.cpu().numpy())
+    ref = oracle.select(oracle.proxy_scores(tables_np, codes_np, d, c_m), counts_np, rho, k_fix)
+    G.assert_same_selection(gpu, ref)
+    return gpu
+
+
+def test_selection_with_heavily_shared_codes():
+    """The passes over distinct codes weight each by its key count: 20000 keys
+    sharing 300 codes give the oracle's sets exactly."""
+    rng = np.random.default_rng(21)
+    H, C, n, d, c_m = 2, 6, 20000, 64, (32, 32, 64)
+    tables = rng.standard_normal((H, C, sum(c_m))).astype(np.float32) * 4
+    pool = (rng.integers(0, c_m[0], 300) | (rng.integers(0, c_m[1], 300) << 10)
+            | (rng.integers(0, c_m[2], 300) << 20)).astype(np.uint32)
+    codes = pool[rng.integers(0, 300, (H, n))]
+    counts = rng.multinomial(n, np.ones(C) / C, size=H).astype(np.int32)
+    _select_from_codes(tables, codes, counts, d, c_m, 0.9, (n + 9) // 10)
+
+
+def test_selection_when_one_dedup_part_overflows():
+    """Head 0's 40000 distinct codes all hash to the same part of the
+    distinct-code build (more than its table holds): that head falls back to
+    one entry per key; head 1 (ordinary codes) keeps the distinct list.  Both
+    must give the oracle's sets."""
+    rng = np.random.default_rng(22)
+    H, C, n, d, c_m = 2, 4, 40000, 64, (1024, 1024, 1024)
+    parts = (2 * n + 16383) // 16384
+    cand = np.arange(0, 1 << 22, dtype=np.uint64)
+    hv = (cand * np.uint64(0x9E3779B1)) & np.uint64(0xFFFFFFFF)
+    same_part = cand[((hv * np.uint64(parts)) >> np.uint64(32)) == 0][:n].astype(np.uint32)
+    assert same_part.size == n
+    codes = np.empty((H, n), np.uint32)
+    codes[0] = rng.permutation(same_part)
+    codes[1] = rng.integers(0, 1 << 30, n, dtype=np.uint32) & np.uint32(0x000FFFFF)
+    tables = rng.standard_normal((H, C, sum(c_m))).astype(np.float32) * 3
+    counts = rng.multinomial(n, np.ones(C) / C, size=H).astype(np.int32)
+    _select_from_codes(tables, codes, counts, d, c_m, 0.7, (n + 9) // 10)
