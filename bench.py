@@ -9,6 +9,9 @@ rho = 0.9, k_fix = ceil(0.1 N)).
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 
+Summaries of saved JSON lines (any machine):
+  python3 bench.py --lines-summary workloads|rho "<command>" line1.json line2.json ...
+
 Traffic measurement (two counter passes, then a summary on any machine):
   rocprofv3 --pmc FETCH_SIZE --kernel-include-regex 'attn_kernel|copy' -d F -o run \
       --output-format csv -- python3 bench.py --traffic-probe
@@ -597,7 +600,53 @@ def traffic_probe():
     log("[probe] attention done")
 
 
+def lines_summary(kind, paths, cmd):
+    """Table of bench.py JSON lines (one per file): kind "workloads" (one
+    line per workload) or "rho" (one line per rho of a workload)."""
+    recs = []
+    for p in paths:
+        line = [l for l in open(p).read().splitlines() if l.startswith("{")][-1]
+        recs.append(json.loads(line))
+    out = [f"command: {cmd}", ""]
+    if kind == "workloads":
+        out += ["the whole layer (5 calls, every head) per workload, HIP-event time;",
+                "SDPA = torch scaled_dot_product_attention (flash backend) on the same Q/K/V, same GPU", "",
+                f"{'workload':>26} {'heads':>5} {'N':>7} {'layer ms':>9} {'eff TFLOP/s':>11} "
+                f"{'q-kmeans':>8} {'k-kmeans':>8} {'select':>7} {'attn ms':>8} {'attn MFMA':>9} "
+                f"{'kept':>6} {'SDPA ms':>8} {'speedup':>7}"]
+        for r in recs:
+            c, st = r["config"], r["stages_ms"]
+            sd = r.get("sdpa_ms")
+            sp = r.get("speedup_vs_sdpa")
+            out.append(f"{c['workload']:>26} {c['heads']:>5} {c['n']:>7} {r['ms_per_step']:>9.2f} "
+                       f"{r['value']:>11.1f} {st['cluster_queries']:>8.2f} "
+                       f"{st['cluster_key_subspaces']:>8.2f} {st['select']:>7.2f} "
+                       f"{st['sparse_attention']:>8.2f} {100 * r['roofline']['frac']:>8.1f}% "
+                       f"{r['retained_fraction']:>6.3f} "
+                       f"{(f'{sd:8.1f}' if sd is not None else f'{chr(45):>8}')} "
+                       f"{(f'{sp:6.2f}x' if sp is not None else f'{chr(45):>7}')}")
+    else:
+        c = recs[0]["config"]
+        out += [f"workload: {c['workload']} ({c['heads']} heads, N = {c['n']}, d = {c['d']}); "
+                "event timings in ms", "",
+                f"{'rho':>5} {'layer':>8} {'q-kmeans':>9} {'k-kmeans':>9} {'tables':>7} {'select':>7} "
+                f"{'attention':>10} {'attn TF/s':>10} {'retained':>9} {'k_head':>8} {'floor binds':>12}"]
+        for r in sorted(recs, key=lambda r: r["config"]["rho"]):
+            st = r["stages_ms"]
+            out.append(f"{r['config']['rho']:>5} {r['ms_per_step']:>8.2f} {st['cluster_queries']:>9.2f} "
+                       f"{st['cluster_key_subspaces']:>9.2f} {st['proxy_scores']:>7.2f} {st['select']:>7.2f} "
+                       f"{st['sparse_attention']:>10.2f} {r['roofline']['achieved']:>10.1f} "
+                       f"{r['retained_fraction']:>9.3f} {r['k_head_mean']:>8.0f} "
+                       f"{r['floor_bound_fraction']:>12.3f}")
+    out += ["", "JSON lines:"] + [json.dumps(r) for r in recs]
+    return "\n".join(out) + "\n"
+
+
 def main():
+    if len(sys.argv) >= 2 and sys.argv[1] == "--lines-summary":
+        # --lines-summary workloads|rho "COMMAND" FILE...
+        sys.stdout.write(lines_summary(sys.argv[2], sys.argv[4:], sys.argv[3]))
+        return
     if len(sys.argv) >= 2 and sys.argv[1] == "--traffic-summary":
         sys.stdout.write(traffic_summary(sys.argv[2], sys.argv[3]))
         return
