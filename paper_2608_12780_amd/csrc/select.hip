@@ -605,7 +605,13 @@ int code_parts(int n) {
   return p < 1 ? 1 : static_cast<int>(p);
 }
 
+// Every part reads all of a head's codes, so the build costs parts x n
+// reads; beyond kMaxParts parts (n > 262144) the passes visit every key.
+constexpr int kMaxParts = 32;
+bool use_distinct_codes(int n) { return code_parts(n) <= kMaxParts; }
+
 size_t select_dedup_words(int heads, int n) {
+  if (!use_distinct_codes(n)) return 0;
   const size_t parts = static_cast<size_t>(code_parts(n));
   return static_cast<size_t>(heads) *
          (2 * parts * kPartSlots + parts + 2 * static_cast<size_t>(n) + 2);
@@ -627,7 +633,8 @@ hipError_t select_run(int heads, int n, int c_q, const Subspaces &sub, int d,
   const float sigma = static_cast<float>(1.0 / sqrt(static_cast<double>(d)));
   const dim3 grid(c_q, heads), block(kSelBlock);
   hipError_t e = hipSuccess;
-  if (kind == kFromPacked) {
+  const bool distinct = kind == kFromPacked && use_distinct_codes(n);
+  if (distinct) {
     // the head's distinct codes and their multiplicities
     const int parts = code_parts(n);
     const size_t stage = static_cast<size_t>(heads) * parts * kPartSlots;
@@ -660,7 +667,8 @@ hipError_t select_run(int heads, int n, int c_q, const Subspaces &sub, int d,
                      sigma, scores, tables, sel_counts, row_max, row_state,       \
                      coarse_hist, sel_idx)
   if (kind == kFromScores) SCOPE_SEL_BASE(kFromScores);
-  else if (kind == kFromPacked) SCOPE_SEL_BASE(kFromUnique);
+  else if (distinct) SCOPE_SEL_BASE(kFromUnique);
+  else if (kind == kFromPacked) SCOPE_SEL_BASE(kFromPacked);
   else SCOPE_SEL_BASE(kFromPlanes);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -669,7 +677,8 @@ hipError_t select_run(int heads, int n, int c_q, const Subspaces &sub, int d,
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (kind == kFromScores) SCOPE_SEL_FINAL(kFromScores, kFromScores);
-  else if (kind == kFromPacked) SCOPE_SEL_FINAL(kFromPacked, kFromUnique);
+  else if (distinct) SCOPE_SEL_FINAL(kFromPacked, kFromUnique);
+  else if (kind == kFromPacked) SCOPE_SEL_FINAL(kFromPacked, kFromPacked);
   else SCOPE_SEL_FINAL(kFromPlanes, kFromPlanes);
 #undef SCOPE_SEL_BASE
 #undef SCOPE_SEL_FINAL

@@ -382,3 +382,15 @@ def test_selection_when_one_dedup_part_overflows():
     tables = rng.standard_normal((H, C, sum(c_m))).astype(np.float32) * 3
     counts = rng.multinomial(n, np.ones(C) / C, size=H).astype(np.int32)
     _select_from_codes(tables, codes, counts, d, c_m, 0.7, (n + 9) // 10)
+
+
+def test_selection_beyond_the_distinct_code_limit():
+    """Above 262144 keys the selection passes visit every key instead of the
+    distinct codes: 270000 keys, codes from a small pool, against the oracle."""
+    rng = np.random.default_rng(23)
+    H, C, n, d, c_m = 1, 4, 270000, 64, (16, 16, 32)
+    tables = rng.standard_normal((H, C, sum(c_m))).astype(np.float32) * 2
+    codes = (rng.integers(0, c_m[0], (H, n)) | (rng.integers(0, c_m[1], (H, n)) << 10)
+             | (rng.integers(0, c_m[2], (H, n)) << 20)).astype(np.uint32)
+    counts = rng.multinomial(n, np.ones(C) / C, size=H).astype(np.int32)
+    _select_from_codes(tables, codes, counts, d, c_m, 0.8, (n + 9) // 10)
