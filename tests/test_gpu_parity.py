@@ -394,3 +394,39 @@ def test_selection_beyond_the_distinct_code_limit():
              | (rng.integers(0, c_m[2], (H, n)) << 20)).astype(np.uint32)
     counts = rng.multinomial(n, np.ones(C) / C, size=H).astype(np.int32)
     _select_from_codes(tables, codes, counts, d, c_m, 0.8, (n + 9) // 10)
+
+
+def test_points_at_exactly_zero_score():
+    """A point whose score against its best centroid is exactly zero (centroid
+    u = (2, 0, ...), point x = (1, 5, 0, ...): |u|^2 - 2<x, u> = 0) packs its
+    index into a zero, i.e. a denormal.  The matrix-core assignment must still
+    return that index (regression: scaling the packed value by -2 shifted a
+    denormal's mantissa and doubled the index)."""
+    cfg = MID_WAN.with_(name="zero_score", c_q=16, c_m=8, iters=2, seed=31)
+    x = inputs.generate(cfg)
+    (t_off, h_off, w_off), (t_len, h_len, w_len) = cfg.ranges
+
+    def plant(a, bits, lo, ln):
+        # row 0 -> (2, 0, ...) and row 1 -> (1, 5, 0, ...) on channels [lo, lo + ln)
+        a[0, 0, lo:lo + ln] = 0.0
+        a[0, 1, lo:lo + ln] = 0.0
+        a[0, 0, lo] = 2.0
+        a[0, 1, lo] = 1.0
+        a[0, 1, lo + 1] = 5.0
+        bits[0] = inputs.bf16_bits(a[0])
+
+    plant(x.q, x.q_bits, 0, cfg.d)
+    for lo, ln in ((t_off, t_len), (h_off, h_len), (w_off, w_len)):
+        plant(x.k, x.k_bits, lo, ln)
+    # centroid 1 starts at row 0; no other start row is 0 or 1
+    def starts(row, c):
+        others = [r for r in row.tolist() if r not in (0, 1)]
+        extra = [r for r in range(2, cfg.n) if r not in others]
+        out = [others.pop(0) if others else extra.pop(0) for _ in range(c)]
+        out[1] = 0
+        return np.asarray(out, np.int32)
+    x.init_q[0] = starts(x.init_q[0], cfg.c_q)
+    for m in range(3):
+        x.init_k[0, m] = starts(x.init_k[0, m], cfg.c_m)
+    gpu, ref = check_layer_inputs(cfg, x)
+    assert ref["q"]["assign"][0, 1] == 1 or ref["q"]["counts"][0, 1] > 0
