@@ -158,3 +158,38 @@ def test_full_size_random_partition():
     del S
     G.assert_same_selection(gsel, sel)
     G.say(f"[fullsize] random partition: head {head} bit-exact, k_head {int(gsel['k_head'][0])}")
+
+
+@pytest.mark.parametrize("name", ["hy720", "wan720"])
+def test_full_size_every_head_matrix_core_assignment_is_canonical(name):
+    """Every head at full size: the bf16 clustering (matrix-core assignment,
+    exact by its filter and canonical re-score) against the same clustering
+    of the bf16 values widened to fp32, which takes the plain canonical
+    fp32 assignment kernel.  Query assignments, centroids, permutation and
+    key codes and centroids must be identical on all heads."""
+    cfg = inputs.CONFIGS[name]
+    G.say(f"[fullsize] {name}: every head, matrix-core vs canonical assignment")
+    x = inputs.generate(cfg)
+    iq = torch.from_numpy(x.init_q).cuda()
+    ik = torch.from_numpy(x.init_k).cuda()
+    res = {}
+    for dtype in ("bf16", "f32"):
+        layer = ScopeLayer(cfg.heads, cfg.n, cfg.d, cfg.ranges, cfg.c_q, (cfg.c_m,) * 3,
+                           cfg.iters, cfg.rho, cfg.k_fix, dtype=dtype)
+        if dtype == "bf16":
+            q, k, _ = G.to_device(x)
+        else:
+            q, k = torch.from_numpy(x.q).cuda(), torch.from_numpy(x.k).cuda()
+        layer.cluster_queries(q, iq)
+        layer.cluster_keys(k, ik)
+        torch.cuda.synchronize()
+        assert int(layer.status.item()) == 0
+        res[dtype] = {key: getattr(layer, key).cpu().numpy() for key in
+                      ("assign", "counts", "perm", "q_centroids", "codes", "k_centroids")}
+        del layer, q, k
+        torch.cuda.empty_cache()
+        G.say(f"[fullsize] {name}: {dtype} clustering done")
+    for key in res["bf16"]:
+        a, b = res["bf16"][key], res["f32"][key]
+        bad = np.flatnonzero((a.view(np.uint32) != b.view(np.uint32)).reshape(cfg.heads, -1).any(1))
+        assert bad.size == 0, (key, bad.tolist())
