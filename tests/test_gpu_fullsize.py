@@ -193,3 +193,34 @@ def test_full_size_every_head_matrix_core_assignment_is_canonical(name):
         a, b = res["bf16"][key], res["f32"][key]
         bad = np.flatnonzero((a.view(np.uint32) != b.view(np.uint32)).reshape(cfg.heads, -1).any(1))
         assert bad.size == 0, (key, bad.tolist())
+
+
+def test_full_size_every_head_selection_from_codes_equals_from_scores():
+    """Every head of the HunyuanVideo-720p-like layer: the selection fused
+    from the tables and codes (passes over each head's distinct codes)
+    against the selection from the materialised logits (passes over every
+    key).  Counts, k_head and every key set must be identical."""
+    cfg = inputs.CONFIGS["hy720"]
+    x = inputs.generate(cfg)
+    layer = ScopeLayer(cfg.heads, cfg.n, cfg.d, cfg.ranges, cfg.c_q, (cfg.c_m,) * 3,
+                       cfg.iters, cfg.rho, cfg.k_fix, dtype=cfg.dtype, materialize_scores=True)
+    q, k, _ = G.to_device(x)
+    layer.cluster_queries(q, torch.from_numpy(x.init_q).cuda())
+    layer.cluster_keys(k, torch.from_numpy(x.init_k).cuda())
+    layer.proxy_scores()
+    res = []
+    for use_scores in (False, True):
+        layer.select(use_scores=use_scores)
+        torch.cuda.synchronize()
+        res.append({key: getattr(layer, key).clone() for key in
+                    ("base_counts", "topp_counts", "k_head", "sel_counts")})
+        res[-1]["sel_idx"] = layer.sel_idx.clone()
+        G.say(f"[fullsize] hy720 selection from {'scores' if use_scores else 'codes'} done")
+    a, b = res
+    for key in ("base_counts", "topp_counts", "k_head", "sel_counts"):
+        assert torch.equal(a[key], b[key]), key
+    # compare the valid prefix of every key set on the GPU
+    r = a["sel_counts"]
+    pos = torch.arange(cfg.n, device=r.device).view(1, 1, -1)
+    valid = pos < r.unsqueeze(-1)
+    assert torch.equal(torch.where(valid, a["sel_idx"], -1), torch.where(valid, b["sel_idx"], -1))
