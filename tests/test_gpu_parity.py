@@ -430,3 +430,19 @@ def test_points_at_exactly_zero_score():
         x.init_k[0, m] = starts(x.init_k[0, m], cfg.c_m)
     gpu, ref = check_layer_inputs(cfg, x)
     assert ref["q"]["assign"][0, 1] == 1 or ref["q"]["counts"][0, 1] > 0
+
+
+@pytest.mark.parametrize("grid,d,split,c_q,c_m,k_fix,dtype", [
+    ((1, 1, 7), 64, (16, 24, 24), 3, 2, 2, "bf16"),       # fewer keys than a wave slice
+    ((1, 3, 5), 64, (16, 24, 24), 1, 1, 1, "bf16"),       # one query cluster, one centroid per subspace
+    ((1, 2, 9), 128, (16, 56, 56), 18, 18, 18, "bf16"),   # as many clusters as tokens, k_fix = N
+    ((2, 3, 11), 64, (16, 24, 24), 5, 4, 66, "f32"),      # k_fix = N keeps every key
+    ((3, 7, 13), 128, (44, 42, 42), 7, 5, 1, "bf16"),     # k_fix = 1, ragged tiles everywhere
+])
+def test_extreme_small_shapes(grid, d, split, c_q, c_m, k_fix, dtype):
+    n = grid[0] * grid[1] * grid[2]
+    cfg = inputs.LayerConfig(f"edge_{n}_{c_q}_{c_m}", 2, grid, d, split, c_q, c_m, 2, 0.9,
+                             k_fix, dtype, 2, 40 + n)
+    gpu, ref = check_layer(cfg)
+    if k_fix == n:
+        assert (gpu["sel_counts"] == n).all()
