@@ -51,6 +51,26 @@ __device__ __forceinline__ uint16_t to_bf16(float f) {
   return static_cast<uint16_t>(__builtin_bit_cast(uint32_t, r) & 0xFFFFu);
 }
 
+// Channels c0 .. c0+7 of one bf16 row as four packed pairs, zero from dx on
+// and for invalid rows.  A whole group is one 16-byte load when the rows are
+// 16-byte aligned (vec), else four 4-byte loads (rows, ld, col0 and dx are
+// even, so no pair straddles dx).
+__device__ __forceinline__ uint4 load_group8(const uint16_t *xrow, int c0, int dx, bool valid, bool vec) {
+  uint4 v = make_uint4(0, 0, 0, 0);
+  if (vec && c0 + 8 <= dx) {
+    if (valid) v = *reinterpret_cast<const uint4 *>(xrow + c0);
+  } else {
+    uint32_t w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int c = c0 + 2 * q;
+      w[q] = valid && c < dx ? *reinterpret_cast<const uint32_t *>(xrow + c) : 0u;
+    }
+    v = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+  return v;
+}
+
 // ascending-order key of a float score
 __device__ __forceinline__ uint32_t asc_key(float f) {
   const uint32_t u = __float_as_uint(f);
@@ -148,6 +168,8 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
   const uint32_t imask = (1u << ib) - 1u;
   const float dpack = __uint_as_float(static_cast<uint32_t>(127 + ib - 23) << 23);  // 2^(ib-23)
   const int nslices = (n + 31) / 32;
+  // every row's first channel is 16-byte aligned
+  const bool vec = ((reinterpret_cast<uintptr_t>(X + col0) & 15) | ((x_hs | static_cast<size_t>(ld)) & 7)) == 0;
 
   // this block's contiguous range of (head, slice) pairs
   const long long total = static_cast<long long>(heads) * nslices;
@@ -208,18 +230,15 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
       float ss = 0.0f;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
-        uint32_t wv[4];
+        const uint4 v4 = load_group8(xrow, 16 * s + 8 * hf, dx, valid, vec);
+        const uint32_t wv[4] = {v4.x, v4.y, v4.z, v4.w};
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int c = 16 * s + 8 * hf + 2 * q;
-          uint32_t v = 0;
-          if (valid && c < dx) v = *reinterpret_cast<const uint32_t *>(xrow + c);
-          wv[q] = v;
-          const float a = __uint_as_float(v << 16), b = __uint_as_float(v & 0xFFFF0000u);
+          const float a = __uint_as_float(wv[q] << 16), b = __uint_as_float(wv[q] & 0xFFFF0000u);
           ss = fmaf(a, a, ss);
           ss = fmaf(b, b, ss);
         }
-        xf[s] = __builtin_bit_cast(bf16x8, make_uint4(wv[0], wv[1], wv[2], wv[3]));
+        xf[s] = __builtin_bit_cast(bf16x8, v4);
       }
       ss += __shfl_xor(ss, 32);
       const float nx = sqrtf(ss) * 1.0001f + 1e-30f;
@@ -376,6 +395,8 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_part_kerne
   const int ib = 32 - __clz(cpad - 1);
   const uint32_t imask = (1u << ib) - 1u;
   const int nslices = (n + 31) / 32;
+  // every row's first channel is 16-byte aligned
+  const bool vec = ((reinterpret_cast<uintptr_t>(X + col0) & 15) | ((x_hs | static_cast<size_t>(ld)) & 7)) == 0;
 
   const long long total = static_cast<long long>(heads) * nslices;
   const long long per = (total + gridDim.x - 1) / gridDim.x;
@@ -405,18 +426,15 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_part_kerne
       float ss = 0.0f;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
-        uint32_t wv[4];
+        const uint4 v4 = load_group8(xrow, 16 * s + 8 * hf, dx, valid, vec);
+        const uint32_t wv[4] = {v4.x, v4.y, v4.z, v4.w};
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int c = 16 * s + 8 * hf + 2 * q;
-          uint32_t v = 0;
-          if (valid && c < dx) v = *reinterpret_cast<const uint32_t *>(xrow + c);
-          wv[q] = v;
-          const float a = __uint_as_float(v << 16), b = __uint_as_float(v & 0xFFFF0000u);
+          const float a = __uint_as_float(wv[q] << 16), b = __uint_as_float(wv[q] & 0xFFFF0000u);
           ss = fmaf(a, a, ss);
           ss = fmaf(b, b, ss);
         }
-        xf[s] = __builtin_bit_cast(bf16x8, make_uint4(wv[0], wv[1], wv[2], wv[3]));
+        xf[s] = __builtin_bit_cast(bf16x8, v4);
       }
       ss += __shfl_xor(ss, 32);
 
