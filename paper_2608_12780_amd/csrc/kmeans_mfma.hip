@@ -73,7 +73,8 @@ __device__ __forceinline__ uint4 load_group8(const uint16_t *xrow, int c0, int d
 
 // Canonical <x, u>: one fp32 fma per channel in ascending channel order, x
 // in bf16 and u in fp32.  Both rows 16-byte aligned: eight channels per load
-// step (the same chain), with the loads of four steps issued together.
+// step (the same chain), with the loads of four steps issued together; x
+// 4-byte and u 8-byte aligned: two channels per step; then one at a time.
 __device__ __forceinline__ float canon_dot(const uint16_t *xr, const float *u, int dx) {
   float dot = 0.0f;
   int c = 0;
@@ -91,6 +92,15 @@ __device__ __forceinline__ float canon_dot(const uint16_t *xr, const float *u, i
       dot = fmaf(__uint_as_float(xv.z & 0xFFFF0000u), u1.y, dot);
       dot = fmaf(__uint_as_float(xv.w << 16), u1.z, dot);
       dot = fmaf(__uint_as_float(xv.w & 0xFFFF0000u), u1.w, dot);
+    }
+  }
+  if (((reinterpret_cast<uintptr_t>(xr) & 3) | (reinterpret_cast<uintptr_t>(u) & 7)) == 0) {
+#pragma unroll 4
+    for (; c + 2 <= dx; c += 2) {
+      const uint32_t xv = *reinterpret_cast<const uint32_t *>(xr + c);
+      const float2 uv = *reinterpret_cast<const float2 *>(u + c);
+      dot = fmaf(__uint_as_float(xv << 16), uv.x, dot);
+      dot = fmaf(__uint_as_float(xv & 0xFFFF0000u), uv.y, dot);
     }
   }
   for (; c < dx; ++c) dot = fmaf(bf16_to_f32(xr[c]), u[c], dot);
