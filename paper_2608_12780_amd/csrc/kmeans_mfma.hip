@@ -296,16 +296,17 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
         }
         return acc;
       };
-      // one pass: smallest and second-smallest packed score per point (med3
-      // keeps the two smallest of {m1, m2, sp}; the start value lies above
+      // one pass: the three smallest packed scores per point (each med3 keeps
+      // the smaller two of its inputs' upper pair; the start value lies above
       // every score of valid inputs)
-      float m1 = 0x1.1p127f, m2 = 0x1.1p127f;
+      float m1 = 0x1.1p127f, m2 = 0x1.1p127f, m3 = 0x1.1p127f;
       auto fold = [&](const f32x16 &acc, int rb) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const uint32_t r = static_cast<uint32_t>(rb + 8 * (e >> 2) + 4 * hf + (e & 3));
           const float sc = fmaf(-2.0f, acc[e], nus[r]);
           const float sp = __uint_as_float((__float_as_uint(sc) & ~imask) | r);
+          m3 = __builtin_amdgcn_fmed3f(m2, m3, sp);
           m2 = __builtin_amdgcn_fmed3f(m1, m2, sp);
           m1 = __builtin_amdgcn_fmed3f(m1, sp, -0x1.1p127f);
         }
@@ -329,18 +330,42 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
       }
       fold(prev, cpad - 32);
       {
-        const float o1 = __shfl_xor(m1, 32), o2 = __shfl_xor(m2, 32);
-        m2 = fminf(fmaxf(m1, o1), fminf(m2, o2));
-        m1 = fminf(m1, o1);
+        // the other half-wave's three into this one's (same multiset, same
+        // result in both halves)
+        const float o[3] = {__shfl_xor(m1, 32), __shfl_xor(m2, 32), __shfl_xor(m3, 32)};
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+          m3 = __builtin_amdgcn_fmed3f(m2, m3, o[q]);
+          m2 = __builtin_amdgcn_fmed3f(m1, m2, o[q]);
+          m1 = fminf(m1, o[q]);
+        }
       }
       const float slack = (2.0f * beta + 2.0f * dpack * fabsf(m1)) * 1.001f;
       const float lim = m1 + slack;
       const float thr = lim + fabsf(lim) * 2e-6f + 1e-30f;
       const bool needy = valid && !(m2 > thr);
+      // three or more candidates (very rare)
+      const bool wide = needy && !(m3 > thr);
       int arg = static_cast<int>(__float_as_uint(m1) & imask);
 
-      if (__ballot(needy)) {
-        // rare: every candidate of the needy points, re-scored canonically
+      if (__ballot(needy && !wide)) {
+        // exactly two candidates, the two smallest packed scores: the point's
+        // two half-wave lanes re-score one each canonically and exchange
+        unsigned long long key = ~0ull;
+        if (needy && !wide) {
+          const int r = min(static_cast<int>(__float_as_uint(hf ? m2 : m1) & imask), C - 1);
+          const uint16_t *xr = X + h * x_hs + static_cast<size_t>(i) * ld + col0;
+          const float dot = canon_dot(xr, Uh + static_cast<size_t>(r) * dx, dx);
+          const float sc = fmaf(-2.0f, dot, nus[r]) + 0.0f;
+          key = (static_cast<unsigned long long>(asc_key(sc)) << 32) | static_cast<unsigned>(r);
+        }
+        const uint32_t ok_lo = __shfl_xor(static_cast<uint32_t>(key), 32);
+        const uint32_t ok_hi = __shfl_xor(static_cast<uint32_t>(key >> 32), 32);
+        const unsigned long long other = (static_cast<unsigned long long>(ok_hi) << 32) | ok_lo;
+        if (needy && !wide) arg = static_cast<int>((key < other ? key : other) & 0xFFFFFFFFu);
+      }
+      if (__ballot(wide)) {
+        // every candidate of the wide points, re-scored canonically
         wave_sync();
         if (lane == 0) ncand[w] = 0;
         if (lane < 32) best[w][lane] = ~0ull;
@@ -348,7 +373,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
         bool over = false;
         for (int rb = 0; rb < cpad; rb += 32) {
           const f32x16 acc = chain(rb);
-          if (needy) {
+          if (wide) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
               const uint32_t r = static_cast<uint32_t>(rb + 8 * (e >> 2) + 4 * hf + (e & 3));
@@ -378,7 +403,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
           atomicMin(&best[w][q], (static_cast<unsigned long long>(asc_key(sc)) << 32) | static_cast<unsigned>(r));
         }
         wave_sync();
-        if (needy && hf == 0) {
+        if (wide && hf == 0) {
           unsigned long long b = best[w][l32];
           if (full) {
             const uint16_t *xr = X + h * x_hs + static_cast<size_t>(i) * ld + col0;
