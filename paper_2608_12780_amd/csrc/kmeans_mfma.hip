@@ -13,15 +13,16 @@
 // the final subtraction), inflated by 1%.  So the canonical argmin r*
 // satisfies s~_{r*} <= min_r s~_r + 2 beta.
 //
-// One pass keeps, per point, the smallest and second-smallest approximate
-// score with the centroid index packed into the low mantissa bits (IB bits;
-// this moves a score by less than delta = 2^(IB-23) |s|, added to the
-// margin).  If the second-smallest is more than 2 beta + 2 delta above the
-// smallest, the smallest's index is the only candidate and thus r*.  For the
-// few points where it is not, the wave recomputes the scores, lists every
-// candidate within the margin and re-scores them with the canonical
-// arithmetic (smallest (score, r) wins, so equal scores keep the lowest
-// index).
+// One pass keeps, per point, the three smallest approximate scores with the
+// centroid index packed into the low mantissa bits (IB bits; this moves a
+// score by less than delta = 2^(IB-23) |s|, added to the margin).  If the
+// second-smallest is more than 2 beta + 2 delta above the smallest, the
+// smallest's index is the only candidate and thus r*.  If only the third
+// is, r* is one of the two smallest, and the point's two half-wave lanes
+// re-score one each with the canonical arithmetic.  For the very few points
+// with three or more candidates, the wave recomputes the scores, lists every
+// candidate within the margin and re-scores them canonically.  In both
+// cases the smallest (score, r) wins, so equal scores keep the lowest index.
 //
 // Blocks are persistent per head: the two-term codebook is staged in LDS
 // once, then each wave independently takes 32-point slices; chunk

@@ -432,6 +432,46 @@ def test_points_at_exactly_zero_score():
     assert ref["q"]["assign"][0, 1] == 1 or ref["q"]["counts"][0, 1] > 0
 
 
+def test_exact_two_and_three_way_ties():
+    """Exact ties in the first assignment, in the query clustering and in every
+    key subspace.  Centroid 5 starts at e0, centroid 2 at e1 and centroid 7
+    at -e0 (unit vectors on the first two channels of the range).  The zero
+    point then scores exactly 1 against all three (three candidates within
+    the matrix-core margin: the full re-scoring path).  e0 + e1 scores
+    exactly -1 against centroids 5 and 2 (two candidates: the two half-wave
+    lanes re-score one each).  The canonical rule (lowest index: 2 both
+    times) must win; a wrong pick moves the centroids and fails the
+    bit-exact comparison."""
+    cfg = MID_WAN.with_(name="exact_ties", c_q=16, c_m=8, iters=2, seed=37)
+    x = inputs.generate(cfg)
+    (t_off, h_off, w_off), (t_len, h_len, w_len) = cfg.ranges
+
+    def plant(a, bits, lo, ln):
+        rows = {0: (1.0, 0.0), 1: (0.0, 1.0), 2: (-1.0, 0.0), 3: (0.0, 0.0), 4: (1.0, 1.0)}
+        for r, (v0, v1) in rows.items():
+            a[0, r, lo:lo + ln] = 0.0
+            a[0, r, lo] = v0
+            a[0, r, lo + 1] = v1
+        bits[0] = inputs.bf16_bits(a[0])
+
+    plant(x.q, x.q_bits, 0, cfg.d)
+    for lo, ln in ((t_off, t_len), (h_off, h_len), (w_off, w_len)):
+        plant(x.k, x.k_bits, lo, ln)
+
+    def starts(row, c):
+        # slots 5, 2, 7 start at rows 0, 1, 2; no other slot starts at rows 0-4
+        others = [r for r in row.tolist() if r > 4]
+        extra = [r for r in range(5, cfg.n) if r not in others]
+        out = [others.pop(0) if others else extra.pop(0) for _ in range(c)]
+        out[5], out[2], out[7] = 0, 1, 2
+        return np.asarray(out, np.int32)
+
+    x.init_q[0] = starts(x.init_q[0], cfg.c_q)
+    for m in range(3):
+        x.init_k[0, m] = starts(x.init_k[0, m], cfg.c_m)
+    check_layer_inputs(cfg, x)
+
+
 @pytest.mark.parametrize("grid,d,split,c_q,c_m,k_fix,dtype", [
     ((1, 1, 7), 64, (16, 24, 24), 3, 2, 2, "bf16"),       # fewer keys than a wave slice
     ((1, 3, 5), 64, (16, 24, 24), 1, 1, 1, "bf16"),       # one query cluster, one centroid per subspace
