@@ -40,6 +40,7 @@ constexpr int kSelBlock = 1024;
 constexpr int kCoarseBins = kSelCoarseBins;
 constexpr int kMaxTable = kSelMaxTable;
 constexpr int kCand = 8192;      // logits of the crossing coarse bin held in LDS
+constexpr int kCandFinal = 4096; // the same in the final kernel (two blocks per CU)
 
 __device__ __forceinline__ int coarse_bin(float y) {
   // y = s - M <= 0; monotone non-increasing in s
@@ -231,7 +232,7 @@ __device__ void refine(Visit visit, float M, uint64_t target, uint32_t *hc,
 // Gathers the logits of coarse bin `cbin` into cand (one LDS slot per key,
 // reserved per wave); returns how many there are (more than kCand: the
 // list is incomplete and the caller visits all keys instead).
-template <int KIND>
+template <int KIND, int CAP = kCand>
 __device__ int gather_bin(const LogitSource<KIND> &src, float M, int cbin,
                           float *cand, uint32_t *candw, int *ncand) {
   if (threadIdx.x == 0) *ncand = 0;
@@ -254,7 +255,7 @@ __device__ int gather_bin(const LogitSource<KIND> &src, float M, int cbin,
       first = __shfl(first, __ffsll(static_cast<long long>(mask)) - 1);
       const int slot = first + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
           static_cast<uint32_t>(mask >> 32), __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u)));
-      if (in && slot < kCand) {
+      if (in && slot < CAP) {
         cand[slot] = s;
         candw[slot] = src.weight(j);
       }
@@ -268,13 +269,13 @@ __device__ int gather_bin(const LogitSource<KIND> &src, float M, int cbin,
 
 // Exact crossing key inside coarse bin `cbin`: over the gathered list when
 // it is complete, else over all keys.
-template <int KIND, bool BY_MASS>
+template <int KIND, bool BY_MASS, int CAP = kCand>
 __device__ void refine_bin(const LogitSource<KIND> &src, float M, int cbin,
                            uint64_t target, uint32_t *hc, uint64_t *hm, float *cand,
                            uint32_t *candw, int *ncand, uint32_t *key_out,
                            uint32_t *cnt_above, uint64_t *mass_above) {
-  const int cnt = gather_bin<KIND>(src, M, cbin, cand, candw, ncand);
-  if (cnt <= kCand) {
+  const int cnt = gather_bin<KIND, CAP>(src, M, cbin, cand, candw, ncand);
+  if (cnt <= CAP) {
     refine<BY_MASS>([&](auto f) {
       for (int k = threadIdx.x; k < cnt; k += kSelBlock) f(cand[k], candw[k]);
     }, M, target, hc, hm, key_out, cnt_above, mass_above);
@@ -289,15 +290,15 @@ __device__ void refine_bin(const LogitSource<KIND> &src, float M, int cbin,
 }
 
 template <int KIND>
-__global__ __launch_bounds__(kSelBlock) void select_base_kernel(
+__global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) void select_base_kernel(
     int n, int c_q, CodeBooks cb, float sigma, const float *__restrict__ scores,
     const float *__restrict__ tables, float rho, int k_fix, int32_t *base_counts, int32_t *topp_counts,
     float *row_max, uint32_t *row_state, uint32_t *coarse_hist) {
   __shared__ float lut[kMaxTable];
   __shared__ uint32_t hc[kCoarseBins];
   __shared__ uint64_t hm[kCoarseBins];
-  __shared__ float cand[kCand];
-  __shared__ uint32_t candw[kCand];
+  __shared__ float cand[kCandFinal];
+  __shared__ uint32_t candw[kCandFinal];
   __shared__ int ncand;
   const int c = blockIdx.x, h = blockIdx.y;
   const size_t row = static_cast<size_t>(h) * c_q + c;
@@ -355,7 +356,7 @@ __global__ __launch_bounds__(kSelBlock) void select_base_kernel(
     const Crossing x = find_crossing<true>(hc, hm, kCoarseBins, 0, T);
     uint32_t cnt_above = x.cnt_before;
     uint64_t mass_above = x.mass_before;
-    refine_bin<KIND, true>(src, M, x.bin, T, hc, hm, cand, candw, &ncand, &key_star,
+    refine_bin<KIND, true, kCandFinal>(src, M, x.bin, T, hc, hm, cand, candw, &ncand, &key_star,
                             &cnt_above, &mass_above);
     const float s_star = desc_key_value(key_star);
     const uint64_t e_star = fixexp(s_star - M);
@@ -399,15 +400,15 @@ __global__ __launch_bounds__(kSelBlock) void select_head_kernel(
 }
 
 template <int KIND, int RKIND>
-__global__ __launch_bounds__(kSelBlock) void select_final_kernel(
+__global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) void select_final_kernel(
     int n, int c_q, CodeBooks cb, float sigma, const float *__restrict__ scores,
     const float *__restrict__ tables, const int32_t *__restrict__ sel_counts, const float *__restrict__ row_max,
     const uint32_t *__restrict__ row_state,
     const uint32_t *__restrict__ coarse_hist, int32_t *sel_idx) {
   __shared__ float lut[kMaxTable];
   __shared__ uint32_t hc[kCoarseBins];
-  __shared__ float cand[kCand];
-  __shared__ uint32_t candw[kCand];
+  __shared__ float cand[kCandFinal];
+  __shared__ uint32_t candw[kCandFinal];
   __shared__ int ncand;
   const int c = blockIdx.x, h = blockIdx.y;
   const size_t row = static_cast<size_t>(h) * c_q + c;
@@ -449,7 +450,7 @@ __global__ __launch_bounds__(kSelBlock) void select_final_kernel(
       rsrc.mult = cb.umult + static_cast<size_t>(h) * n;
       rsrc.count = min(max(cb.ucount[h], 0), n);
     }
-    refine_bin<RKIND, false>(rsrc, M, x.bin, static_cast<uint64_t>(r), hc, nullptr,
+    refine_bin<RKIND, false, kCandFinal>(rsrc, M, x.bin, static_cast<uint64_t>(r), hc, nullptr,
                              cand, candw, &ncand, &key_r, &above, &unused);
   }
   // ordered compaction, four consecutive keys per thread: keys above key_r
