@@ -34,9 +34,13 @@
  *    outside what the kernels implement) or SCOPE_ERR_WORKSPACE; nothing is
  *    enqueued then.  A failed kernel launch returns SCOPE_ERR_HIP.  Faults
  *    that depend on data are OR-ed into the optional device word
- *    `dev_status` (bit 0: non-finite input; bit 1: |x| >= 2^22, outside the
- *    fixed-point range of the k-means means; bit 2: an initial row index out
- *    of range, replaced by the default row).  Nothing aborts or prints.
+ *    `dev_status` (bit 0: non-finite input; bit 1: |x| >= 2^e with
+ *    e = min(22, 39 - ceil(log2 n)), outside the range in which the int64
+ *    fixed-point sums of the k-means means are exact (2^22 for n <= 2^17,
+ *    2^15 at n = 2^24), also set for non-finite input; bit 2: an initial
+ *    row index out of range, replaced by the default row).  The inputs are
+ *    checked in the first update pass of calls 1 and 2.  Nothing aborts or
+ *    prints.
  *  - Determinism: every output is bitwise reproducible run to run and
  *    independent of launch geometry; calls 1-4 are bit-exact with respect to
  *    the canonical arithmetic defined under each call.

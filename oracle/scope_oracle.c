@@ -93,19 +93,29 @@ static void km_assign(const float *X, long ldx, int n, int dx, const float *U,
   free(nu);
 }
 
-/* returns OR_ERR_RANGE if some |x| >= 2^22 (fixed-point range exceeded) */
+/* Largest magnitude the fixed-point sums of n rows hold exactly: every
+ * |rint(x 2^24)| is below 2^(e+24) for |x| < 2^e, and n <= 2^L such terms sum
+ * below 2^63 when e <= 39 - L; e is capped at 22 (2^22 for n <= 2^17).    */
+static float range_limit(int n) {
+  int L = 0;
+  while (L < 31 && (1L << L) < n) ++L;
+  return ldexpf(1.0f, 39 - L < 22 ? 39 - L : 22);
+}
+
+/* returns OR_ERR_RANGE if some |x| >= range_limit(n) or is not finite */
 static int km_update(const float *X, long ldx, int n, int dx, const int *a,
                      int C, float *U, int *cnt) {
   int64_t *S = (int64_t *)calloc((size_t)C * dx, sizeof(int64_t));
   if (!S) return OR_ERR_MEM;
   int status = OR_OK;
+  const float lim = range_limit(n);
   for (int r = 0; r < C; ++r) cnt[r] = 0;
   for (int i = 0; i < n; ++i) {
     const float *x = X + (size_t)i * ldx;
     int r = a[i];
     cnt[r] += 1;
     for (int c = 0; c < dx; ++c) {
-      if (!(fabsf(x[c]) < 4194304.0f)) status = OR_ERR_RANGE;
+      if (!(fabsf(x[c]) < lim)) status = OR_ERR_RANGE;
       S[(size_t)r * dx + c] += (int64_t)rintf(x[c] * 16777216.0f);
     }
   }

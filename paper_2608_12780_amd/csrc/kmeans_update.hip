@@ -40,8 +40,11 @@ __device__ __forceinline__ unsigned long long fixed24(float x) {
   return (static_cast<unsigned long long>(hi) << 32) | lo;
 }
 
-__device__ __forceinline__ void check_value(float x, int &bad) {
-  if (!(fabsf(x) < 0x1p22f))
+// The int64 sums stay exact while n terms of magnitude below 2^(e+24) cannot
+// reach 2^63: |x| < lim = 2^e with e = min(22, 39 - ceil(log2 n)).  Larger or
+// non-finite inputs are flagged.
+__device__ __forceinline__ void check_value(float x, float lim, int &bad) {
+  if (!(fabsf(x) < lim))
     bad |= isfinite(x) ? kStatusRange : (kStatusRange | kStatusNonFinite);
 }
 
@@ -83,7 +86,7 @@ template <typename T, int CPL, bool VEC, bool CHECK>
 __global__ __launch_bounds__(kAccThreads) void km_accum_kernel(
     const T *__restrict__ X, size_t x_hs, int ld, int n, const AccPlan plan,
     const int32_t *__restrict__ assign, size_t a_hs, size_t a_ss,
-    long long *slab, int32_t *cslab, int32_t *status) {
+    long long *slab, int32_t *cslab, int32_t *status, float lim) {
   // the last CPL sums are a sink for lanes that hold no channels
   __shared__ unsigned long long sums[kAccLds + 4];
   __shared__ int cnts[kAccCnt];
@@ -147,7 +150,7 @@ __global__ __launch_bounds__(kAccThreads) void km_accum_kernel(
 #pragma unroll
       for (int e = 0; e < CPL; ++e) {
         const float x = ok ? xv[u][e] : 0.0f;
-        if (CHECK && e < nvalid) check_value(x, bad);
+        if (CHECK && e < nvalid) check_value(x, lim, bad);
         if (VEC || e < nvalid) atomicAdd(&sums[idx + (active ? e * e_stride : e)], fixed24(x));
       }
       if (counter) atomicAdd(&cnts[p_cnt + a], ok ? 1 : 0);
@@ -289,6 +292,9 @@ hipError_t km_accum(const AccPlan &plan, const void *x, bool bf16, size_t x_hs,
                     float *U, size_t u_hs, int32_t *status, hipStream_t s) {
   const dim3 grid(plan.blocks, plan.nwin, heads);
   const bool check = status != nullptr;
+  int ce = 0;  // ceil(log2 n)
+  while (ce < 31 && (1LL << ce) < n) ++ce;
+  const float lim = ldexpf(1.0f, 39 - ce < 22 ? 39 - ce : 22);
   // vector loads need complete chunks starting on chunk boundaries
   auto aligned = [&](int cpl) {
     const size_t bytes = static_cast<size_t>(cpl) * (bf16 ? 2 : 4);
@@ -304,7 +310,7 @@ hipError_t km_accum(const AccPlan &plan, const void *x, bool bf16, size_t x_hs,
 #define SCOPE_ACCUM(T, CPL, V, K)                                                    \
   hipLaunchKernelGGL((km_accum_kernel<T, CPL, V, K>), grid, dim3(kAccThreads), 0, s, \
                      static_cast<const T *>(x), x_hs, ld, n, plan, assign, a_hs,      \
-                     a_ss, slab, cslab, status)
+                     a_ss, slab, cslab, status, lim)
 #define SCOPE_ACCUM_K(T, CPL, V)            \
   if (check) SCOPE_ACCUM(T, CPL, V, true);  \
   else SCOPE_ACCUM(T, CPL, V, false);

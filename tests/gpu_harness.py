@@ -9,6 +9,7 @@ import numpy as np
 import torch
 
 import oracle
+from paper_2608_12780_amd import binding as B
 from paper_2608_12780_amd import inputs
 from paper_2608_12780_amd.layer import DenseAttention, ScopeLayer, ScopePartitionLayer
 
@@ -105,3 +106,30 @@ def assert_attention_close(out, ref):
     mx, mr = attention_error(out, ref)
     assert mx <= MAX_ABS and mr <= MEAN_REL, (mx, mr)
     return mx, mr
+
+
+def select_from_codes(tables_np, codes_np, counts_np, d, c_m, rho, k_fix):
+    """scope_select on given tables and packed codes (logits fused from the
+    LUT), against the oracle's selection on the oracle's proxy logits."""
+    H, C, _ = tables_np.shape
+    n = codes_np.shape[1]
+    shape = B.make_shape(H, n, d, B.BF16, ((0, d // 4, d // 2), (d // 4, d // 4, d // 2)))
+    dev = "cuda"
+    tables = torch.from_numpy(tables_np).to(dev)
+    codes = torch.from_numpy(codes_np.view(np.int32)).to(dev)
+    counts = torch.from_numpy(counts_np).to(dev)
+    i32 = dict(dtype=torch.int32, device=dev)
+    base = torch.empty(H, C, **i32)
+    topp = torch.empty(H, C, **i32)
+    kh = torch.empty(H, **i32)
+    sc = torch.empty(H, C, **i32)
+    idx = torch.empty(H, C, n, **i32)
+    ws = B.alloc_workspace(shape, C, c_m, dev)
+    B.scope_select(shape, C, c_m, None, tables, codes, counts, rho, k_fix, base, topp,
+                   kh, sc, idx, ws)
+    torch.cuda.synchronize()
+    gpu = dict(base=base.cpu().numpy(), topp=topp.cpu().numpy(), k_head=kh.cpu().numpy(),
+               sel_counts=sc.cpu().numpy(), sel_idx=idx.cpu().numpy())
+    ref = oracle.select(oracle.proxy_scores(tables_np, codes_np, d, c_m), counts_np, rho, k_fix)
+    assert_same_selection(gpu, ref)
+    return gpu

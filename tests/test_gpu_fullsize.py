@@ -224,3 +224,80 @@ def test_full_size_every_head_selection_from_codes_equals_from_scores():
     pos = torch.arange(cfg.n, device=r.device).view(1, 1, -1)
     valid = pos < r.unsqueeze(-1)
     assert torch.equal(torch.where(valid, a["sel_idx"], -1), torch.where(valid, b["sel_idx"], -1))
+
+
+def test_full_size_stress_every_rho_flattest_and_most_peaked_heads():
+    """The selection stress workload at full size (24 heads, N = 118800) in
+    the benchmark's launch configuration, for every rho of the sweep.  The
+    oracle recomputes the head with the smallest temperature (the flattest
+    proxy softmax: the largest Top-p counts and crossing bins) and the one
+    with the largest: clustering, tables and selection bit for bit at each
+    rho, attention on sampled rows within tolerance."""
+    cfg = inputs.CONFIGS["stress"]
+    x = inputs.generate(cfg)
+    heads = (int(np.argmin(x.tau)), int(np.argmax(x.tau)))
+    G.say(f"[fullsize] stress: heads {heads} tau {[round(float(x.tau[h]), 3) for h in heads]}")
+    layer = ScopeLayer(cfg.heads, cfg.n, cfg.d, cfg.ranges, cfg.c_q, (cfg.c_m,) * 3,
+                       cfg.iters, cfg.rho, cfg.k_fix, dtype=cfg.dtype)
+    q, k, v = G.to_device(x)
+    layer.cluster_queries(q, torch.from_numpy(x.init_q).cuda())
+    layer.cluster_keys(k, torch.from_numpy(x.init_k).cuda())
+    layer.proxy_scores()
+    torch.cuda.synchronize()
+    assert int(layer.status.item()) == 0
+    sl = lambda t, h: t[h:h + 1].cpu().numpy()
+    clus = {h: dict(assign=sl(layer.assign, h), counts=sl(layer.counts, h),
+                    offsets=sl(layer.offsets, h), perm=sl(layer.perm, h),
+                    centroids=sl(layer.q_centroids, h), k_centroids=sl(layer.k_centroids, h),
+                    codes=sl(layer.codes, h).view(np.uint32), tables=sl(layer.tables, h))
+            for h in heads}
+    rhos = (0.5, 0.7, 0.9, 0.95)
+    sels = {}
+    for rho in rhos:
+        layer.select(rho=rho)
+        layer.attend(q, k, v)
+        torch.cuda.synchronize()
+        for h in heads:
+            sels[h, rho] = dict(base=sl(layer.base_counts, h), topp=sl(layer.topp_counts, h),
+                                k_head=sl(layer.k_head, h), sel_counts=sl(layer.sel_counts, h),
+                                sel_idx=sl(layer.sel_idx, h),
+                                out=layer.out[h:h + 1].float().cpu().numpy())
+        G.say(f"[fullsize] stress: GPU rho {rho} done, k_head "
+              f"{[int(sels[h, rho]['k_head'][0]) for h in heads]}")
+    del layer, q, k, v
+    torch.cuda.empty_cache()
+    cm = (cfg.c_m,) * 3
+    for h in heads:
+        gpu = clus.pop(h)
+        hq, hk, hv = x.q[h:h + 1], x.k[h:h + 1], x.v[h:h + 1]
+        qr = oracle.cluster_queries(hq, cfg.c_q, cfg.iters, x.init_q[h:h + 1])
+        for key in ("assign", "counts", "offsets", "perm"):
+            assert np.array_equal(gpu[key], qr[key]), key
+        assert np.array_equal(gpu["centroids"].view(np.uint32), qr["centroids"].view(np.uint32))
+        kr = oracle.cluster_key_subspaces(hk, cfg.ranges, cm, cfg.iters, x.init_k[h:h + 1])
+        assert np.array_equal(gpu["codes"], kr["codes"])
+        assert np.array_equal(gpu["k_centroids"].view(np.uint32), kr["centroids"].view(np.uint32))
+        P = oracle.tables(qr["centroids"], kr["centroids"], cfg.ranges, cm)
+        assert np.array_equal(gpu["tables"].view(np.uint32), P.view(np.uint32))
+        S = oracle.proxy_scores(P, kr["codes"], cfg.d, cm)
+        G.say(f"[fullsize] stress: head {h} clustering and tables bit-exact")
+        rng = np.random.default_rng(100 + h)
+        counts, off, perm = qr["counts"][0], qr["offsets"][0], qr["perm"][0]
+        clusters = rng.choice(np.flatnonzero(counts > 0), 3, replace=False)
+        mask = np.zeros((1, cfg.n), np.uint8)
+        for c in clusters:
+            members = perm[off[c]:off[c + 1]]
+            mask[0, rng.choice(members, min(16, len(members)), replace=False)] = 1
+        rows = np.flatnonzero(mask[0])
+        for rho in rhos:
+            g = sels.pop((h, rho))
+            sel = oracle.select(S, qr["counts"], rho, cfg.k_fix)
+            G.assert_same_selection(g, sel)
+            ref = oracle.attention(hq, hk, hv, qr["offsets"], qr["perm"], sel["sel_counts"],
+                                   sel["sel_idx"], row_mask=mask)
+            mx, mr = G.assert_attention_close(g["out"][0, rows], ref[0, rows])
+            kept = float((sel["sel_counts"][0].astype(np.float64) * counts).sum()) / cfg.n ** 2
+            G.say(f"[fullsize] stress: head {h} rho {rho}: selection bit-exact, k_head "
+                  f"{int(sel['k_head'][0])}, kept {kept:.3f}; attention on {len(rows)} rows "
+                  f"max-abs {mx:.3e} mean-rel {mr:.3e}")
+        del S

@@ -27,9 +27,11 @@ MID_WAN = inputs.LayerConfig("mid_wan", 1, (4, 10, 13), 128, (44, 42, 42), 16, 8
 # d = 64 attention kernel inside the sparse layer
 MID_D64 = inputs.LayerConfig("mid_d64", 2, (4, 12, 17), 64, (16, 24, 24), 24, 12,
                              3, 0.9, inputs.ceil_tenth(4 * 12 * 17), "bf16", 6, 10)
-# the paper's operating point: C_q = 300 and C_m = 333 (not powers of two;
-# C_q = 300 at d = 128 takes the fp32 VALU assignment, C_m = 333 padded
-# bf16 codebooks on the matrix cores)
+# the paper's operating point: C_q = 300 and C_m = 333 (not powers of two).
+# Both take the matrix-core assignment: the 300 x 128 query codebook does
+# not fit one block's LDS and is split into two chunks (km_assign_mfma_part
+# plus km_assign_decide); the 333-centroid subspace codebooks (16 and 56
+# channels) are padded to 352 rows and fit it whole.
 PAPER_POINT = inputs.LayerConfig("paper_point", 1, (6, 20, 24), 128, (16, 56, 56), 300, 333,
                                  3, 0.9, inputs.ceil_tenth(6 * 20 * 24), "bf16", 8, 9)
 
@@ -252,7 +254,8 @@ def _partition_case(cfg, kind, c_m, seed=1):
 ])
 def test_key_partitions_of_the_ablation(kind, c_m):
     # Table 3 variants: any disjoint channel sets, M <= 8, codebooks of any
-    # size (C = 333 at d = 128 takes the fp32 VALU assignment)
+    # size (C = 333 over all 128 channels takes the matrix-core assignment
+    # with the codebook split into two LDS chunks)
     _partition_case(MID_HY, kind, c_m)
 
 
@@ -324,31 +327,7 @@ def test_chunked_codebook_with_tied_centroids():
     assert (ref["counts"] == 0).sum() >= 290
 
 
-def _select_from_codes(tables_np, codes_np, counts_np, d, c_m, rho, k_fix):
-    """scope_select on given tables and packed codes (logits fused from the
-    LUT), against the oracle's selection on the oracle's proxy logits."""
-    H, C, _ = tables_np.shape
-    n = codes_np.shape[1]
-    shape = B.make_shape(H, n, d, B.BF16, ((0, d // 4, d // 2), (d // 4, d // 4, d // 2)))
-    dev = "cuda"
-    tables = torch.from_numpy(tables_np).to(dev)
-    codes = torch.from_numpy(codes_np.view(np.int32)).to(dev)
-    counts = torch.from_numpy(counts_np).to(dev)
-    i32 = dict(dtype=torch.int32, device=dev)
-    base = torch.empty(H, C, **i32)
-    topp = torch.empty(H, C, **i32)
-    kh = torch.empty(H, **i32)
-    sc = torch.empty(H, C, **i32)
-    idx = torch.empty(H, C, n, **i32)
-    ws = B.alloc_workspace(shape, C, c_m, dev)
-    B.scope_select(shape, C, c_m, None, tables, codes, counts, rho, k_fix, base, topp,
-                   kh, sc, idx, ws)
-    torch.cuda.synchronize()
-    gpu = dict(base=base.cpu().numpy(), topp=topp.cpu().numpy(), k_head=kh.cpu().numpy(),
-               sel_counts=sc.cpu().numpy(), sel_idx=idx.cpu().numpy())
-    ref = oracle.select(oracle.proxy_scores(tables_np, codes_np, d, c_m), counts_np, rho, k_fix)
-    G.assert_same_selection(gpu, ref)
-    return gpu
+_select_from_codes = G.select_from_codes
 
 
 def test_selection_with_heavily_shared_codes():

@@ -150,6 +150,27 @@ def test_kmeans_empty_cluster_keeps_centroid(oracle_lib):
     assert a.tolist() == [1, 1, 0, 0, 2] and U[:, 0].tolist() == [10.0, 0.0, 100.0]
 
 
+def test_kmeans_fixed_point_range_depends_on_n(oracle_lib):
+    """The int64 sums of rint(x 2^24) are exact while n terms cannot reach
+    2^63.  The mean of n equal rows is that row exactly when the sums hold
+    it; where n such terms would overflow, the range status (2) is
+    reported.  At n = 2^17 the largest float below 2^22 is inside the range
+    (2^17 (2^46 - 2^22) < 2^63); at n = 2^18 it is not, and the largest
+    float below 2^21 is."""
+    below22 = np.nextafter(np.float32(2.0 ** 22), np.float32(0))
+    below21 = np.nextafter(np.float32(2.0 ** 21), np.float32(0))
+    for n, x, want in ((1 << 17, below22, 0), (1 << 18, below22, 2), (1 << 18, below21, 0)):
+        X = np.full((n, 1), x, np.float32)
+        U, a, cnt, st = oracle.kmeans(X, 1, 1, np.array([0], np.int32), False)
+        assert st == want, (n, x)
+        if want == 0:
+            assert U[0, 0] == x and cnt[0] == n
+    # a non-finite value is outside every range
+    X = np.ones((8, 2), np.float32)
+    X[3, 1] = np.inf
+    assert oracle.kmeans(X, 1, 1, np.array([0], np.int32), False)[3] == 2
+
+
 def test_group_is_a_stable_sort(oracle_lib):
     rng = np.random.default_rng(18)
     g = rng.integers(0, 13, size=1000).astype(np.int32)
