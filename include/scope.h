@@ -19,7 +19,9 @@
  * --------------------------------
  *  - Every array argument is a DEVICE pointer owned by the caller.  Scalars
  *    and the shape/size structs are host values.  The library allocates and
- *    frees nothing and holds no global mutable state.
+ *    frees nothing.  Its only global state belongs to the no-allocation
+ *    attention call (5n): a fixed device array per GPU and a host table of
+ *    their addresses.
  *  - Every call is asynchronous: it validates its arguments on the host,
  *    enqueues its kernels on `stream` (a hipStream_t; NULL = the default
  *    stream) and returns.  No call synchronises or copies to the host.
@@ -62,7 +64,8 @@ typedef enum {
   SCOPE_ERR_INVALID_ARGUMENT = 1,
   SCOPE_ERR_UNSUPPORTED = 2,
   SCOPE_ERR_WORKSPACE = 3,
-  SCOPE_ERR_HIP = 4
+  SCOPE_ERR_HIP = 4,
+  SCOPE_ERR_SCRATCH_LIMIT = 5 /* beyond the no-allocation entry point's list */
 } scope_status;
 
 typedef enum { SCOPE_F32 = 0, SCOPE_BF16 = 1 } scope_dtype;
@@ -281,6 +284,28 @@ int32_t scope_sparse_attention(const scope_shape *shape, const void *q,
                                const int32_t *sel_counts,
                                const int32_t *sel_idx, float scale, void *o,
                                void *workspace, size_t ws_bytes, void *stream);
+
+/* 5n. Sparse attention without allocation or workspace, for callers that
+ * cannot allocate device memory (code under HIP graph capture, serving loops
+ * and harnesses that forbid it).  Arguments, outputs, layout and errors as
+ * call 5 without `workspace`/`ws_bytes`: the call's work list (heads *
+ * (ceil(n / 256) + c_q) entries of 16 bytes) lives in a fixed device array
+ * of SCOPE_NOALLOC_MAX_WORK_ITEMS entries (1 MiB), one per GPU, held until
+ * the process ends; larger problems return SCOPE_ERR_SCRATCH_LIMIT before
+ * anything is enqueued.  The array's device address is looked up on the
+ * first call on each device (the current device).  No call allocates or
+ * frees memory.  Every call on a GPU shares that GPU's array and rewrites
+ * the entries it reads, so calls that overlap on one GPU (two streams, or
+ * two host threads) race; serialise them.                                 */
+#define SCOPE_NOALLOC_MAX_WORK_ITEMS 65536
+int32_t scope_sparse_attention_noalloc(const scope_shape *shape,
+                                       const void *q, const void *k,
+                                       const void *v, int32_t c_q,
+                                       const int32_t *offsets,
+                                       const int32_t *perm,
+                                       const int32_t *sel_counts,
+                                       const int32_t *sel_idx, float scale,
+                                       void *o, void *stream);
 
 /* Diagnostic: the selection's fixed-point exponential (call 4) applied to
  * y[0..count) (y <= 0), results in out[0..count).                          */

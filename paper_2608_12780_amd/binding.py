@@ -25,6 +25,7 @@ ENTRY_POINTS = (
     "scope_sparse_attention", "scope_debug_fixexp",
     "scope_partition_workspace_size", "scope_cluster_key_partition",
     "scope_proxy_scores_partition", "scope_select_partition",
+    "scope_sparse_attention_noalloc",
 )
 MAX_SUBSPACES, MAX_D = 8, 128
 POLICIES = {"online": 0, "fixed": 1, "topp": 2}
@@ -102,6 +103,8 @@ def lib() -> ctypes.CDLL:
                                           P, P, P, P, P, Z, I, P]
         L.scope_sparse_attention.argtypes = [SP, P, P, P, I, P, P, P, P,
                                              ctypes.c_float, P, P, Z, P]
+        L.scope_sparse_attention_noalloc.argtypes = [SP, P, P, P, I, P, P, P, P,
+                                                     ctypes.c_float, P, P]
         L.scope_debug_fixexp.argtypes = [P, P, ctypes.c_int64, P]
         PP = ctypes.POINTER(Partition)
         L.scope_partition_workspace_size.argtypes = [SP, I, PP, ctypes.POINTER(Z)]
@@ -262,6 +265,20 @@ def scope_sparse_attention(shape, q, k, v, c_q, offsets, perm, sel_counts,
         _ptr(o, dt, H * N * D, "o"),
         _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(),
         _stream(stream)))
+
+
+def scope_sparse_attention_noalloc(shape, q, k, v, c_q, offsets, perm, sel_counts,
+                                   sel_idx, scale, o, stream=None):
+    H, N, D = shape.heads, shape.n, shape.d
+    dt = _data_dtype(shape)
+    _check("scope_sparse_attention_noalloc", lib().scope_sparse_attention_noalloc(
+        ctypes.byref(shape), _ptr(q, dt, H * N * D, "q"),
+        _ptr(k, dt, H * N * D, "k"), _ptr(v, dt, H * N * D, "v"), int(c_q),
+        _ptr(offsets, torch.int32, H * (c_q + 1), "offsets"),
+        _ptr(perm, torch.int32, H * N, "perm"),
+        _ptr(sel_counts, torch.int32, H * c_q, "sel_counts"),
+        _ptr(sel_idx, torch.int32, H * c_q * N, "sel_idx"), float(scale),
+        _ptr(o, dt, H * N * D, "o"), _stream(stream)))
 
 
 def scope_debug_fixexp(y, out, stream=None):

@@ -330,6 +330,8 @@ const char *scope_status_string(int32_t status) {
     case SCOPE_ERR_UNSUPPORTED: return "unsupported argument";
     case SCOPE_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
     case SCOPE_ERR_HIP: return "HIP launch failure";
+    case SCOPE_ERR_SCRATCH_LIMIT:
+      return "problem exceeds the fixed work list of the no-allocation entry point";
     default: return "unknown status";
   }
 }
@@ -718,13 +720,14 @@ int32_t scope_select_partition(const scope_shape *shape, int32_t c_q,
   return SCOPE_OK;
 }
 
-int32_t scope_sparse_attention(const scope_shape *shape, const void *q,
-                               const void *k, const void *v, int32_t c_q,
-                               const int32_t *offsets, const int32_t *perm,
-                               const int32_t *sel_counts,
-                               const int32_t *sel_idx, float scale, void *o,
-                               void *workspace, size_t ws_bytes,
-                               void *stream) {
+}  // extern "C"
+
+namespace {
+
+int32_t check_attention(const scope_shape *shape, const void *q, const void *k,
+                        const void *v, int32_t c_q, const int32_t *offsets,
+                        const int32_t *perm, const int32_t *sel_counts,
+                        const int32_t *sel_idx, float scale, const void *o) {
   int32_t st = check_shape(shape);
   if (st) return st;
   if (shape->d != 64 && shape->d != 128) return SCOPE_ERR_UNSUPPORTED;
@@ -736,18 +739,62 @@ int32_t scope_sparse_attention(const scope_shape *shape, const void *q,
   if (!q || !k || !v || !o || !offsets || !perm || !sel_counts || !sel_idx)
     return SCOPE_ERR_INVALID_ARGUMENT;
   // rows are read and written as 16-byte vectors
-  for (const void *p : {q, k, v, static_cast<const void *>(o)})
+  for (const void *p : {q, k, v, o})
     if (reinterpret_cast<uintptr_t>(p) % 16) return SCOPE_ERR_INVALID_ARGUMENT;
   if (!(scale == scale) || isinf(scale)) return SCOPE_ERR_INVALID_ARGUMENT;
+  return SCOPE_OK;
+}
+
+float attention_scale(const scope_shape *shape, float scale) {
+  return scale > 0.0f ? scale
+                      : static_cast<float>(1.0 / sqrt(static_cast<double>(shape->d)));
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t scope_sparse_attention_noalloc(const scope_shape *shape, const void *q,
+                                       const void *k, const void *v,
+                                       int32_t c_q, const int32_t *offsets,
+                                       const int32_t *perm,
+                                       const int32_t *sel_counts,
+                                       const int32_t *sel_idx, float scale,
+                                       void *o, void *stream) {
+  int32_t st = check_attention(shape, q, k, v, c_q, offsets, perm, sel_counts,
+                               sel_idx, scale, o);
+  if (st) return st;
+  const size_t items = static_cast<size_t>(shape->heads) *
+                       scope::attn_items_per_head(shape->n, c_q);
+  if (items > scope::kAttnScratchItems) return SCOPE_ERR_SCRATCH_LIMIT;
+  int4 *list = nullptr;
+  SCOPE_TRY(scope::attention_scratch(&list));
+  SCOPE_TRY(scope::attention_run(shape->heads, shape->n, shape->d,
+                                 shape->dtype == SCOPE_BF16, q, k, v, o, c_q,
+                                 offsets, perm, sel_counts, sel_idx,
+                                 attention_scale(shape, scale), list,
+                                 static_cast<hipStream_t>(stream)));
+  return SCOPE_OK;
+}
+
+int32_t scope_sparse_attention(const scope_shape *shape, const void *q,
+                               const void *k, const void *v, int32_t c_q,
+                               const int32_t *offsets, const int32_t *perm,
+                               const int32_t *sel_counts,
+                               const int32_t *sel_idx, float scale, void *o,
+                               void *workspace, size_t ws_bytes,
+                               void *stream) {
+  int32_t st = check_attention(shape, q, k, v, c_q, offsets, perm, sel_counts,
+                               sel_idx, scale, o);
+  if (st) return st;
   const size_t need = attn_ws(shape, c_q, nullptr, nullptr);
   if ((st = check_ws(workspace, ws_bytes, need))) return st;
   int4 *items = nullptr;
   attn_ws(shape, c_q, workspace, &items);
-  const float sc = scale > 0.0f ? scale
-                                : static_cast<float>(1.0 / sqrt(static_cast<double>(shape->d)));
   SCOPE_TRY(scope::attention_run(shape->heads, shape->n, shape->d,
                                  shape->dtype == SCOPE_BF16, q, k, v, o, c_q,
-                                 offsets, perm, sel_counts, sel_idx, sc, items,
+                                 offsets, perm, sel_counts, sel_idx,
+                                 attention_scale(shape, scale), items,
                                  static_cast<hipStream_t>(stream)));
   return SCOPE_OK;
 }

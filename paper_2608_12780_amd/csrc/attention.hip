@@ -21,6 +21,8 @@
 // (attn_kernel).
 #include <math.h>
 
+#include <mutex>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -664,6 +666,34 @@ hipError_t launch_attn(int heads, int n, bool bf16, const void *q,
 }
 
 }  // namespace
+
+// Work list of the no-allocation entry point: a fixed device array, one copy
+// per GPU, held until the process ends.  Host code never passes `scratch`
+// itself to a kernel (on the host it names a stand-in, not device memory);
+// it looks up the array's device address once per device and uses that.
+static __device__ __align__(256) int4 scratch[kAttnScratchItems];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+int4 *scratch_ptr[kMaxDevices];
+}  // namespace
+
+hipError_t attention_scratch(int4 **items) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_ptr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    scratch_ptr[dev] = static_cast<int4 *>(p);
+  }
+  *items = scratch_ptr[dev];
+  return hipSuccess;
+}
 
 // Slots of one head: sum_c ceil(n_c / kBM) <= ceil(n / kBM) + c_q.
 int attn_items_per_head(int n, int c_q) { return (n + kBM - 1) / kBM + c_q; }

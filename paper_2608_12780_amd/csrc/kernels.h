@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "../../include/scope.h"
+
 namespace scope {
 
 // One batch of k-means problems, one problem per head: the rows of
@@ -140,6 +142,11 @@ hipError_t debug_fixexp(const float *y, uint64_t *out, int64_t count,
                         hipStream_t s);
 
 int attn_items_per_head(int n, int c_q);
+// Work-list entries of the no-allocation attention entry point (1 MiB).
+constexpr size_t kAttnScratchItems = SCOPE_NOALLOC_MAX_WORK_ITEMS;
+// Device address of that work list on the current device (looked up once
+// per device).
+hipError_t attention_scratch(int4 **items);
 hipError_t attention_run(int heads, int n, int d, bool bf16, const void *q,
                          const void *k, const void *v, void *o, int c_q,
                          const int32_t *offsets, const int32_t *perm,

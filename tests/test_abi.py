@@ -36,7 +36,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for s in (OK, INVALID, UNSUPPORTED, WORKSPACE, 4, 99):
+    for s in (OK, INVALID, UNSUPPORTED, WORKSPACE, 4, 5, 99):
         assert isinstance(B.status_string(s), str) and B.status_string(s)
 
 
@@ -140,6 +140,28 @@ def test_attention_validation():
     assert call(hy_shape(), c_q=0) == INVALID
     # bf16 gathers use 32-bit byte offsets within one head: n * d * 2 < 2^32
     assert call(hy_shape(n=1 << 24)) == UNSUPPORTED
+
+
+def test_noalloc_attention_validation():
+    """The no-allocation call validates like the workspace call and rejects
+    problems whose work list exceeds its fixed array, before any GPU work."""
+    L = B.lib()
+
+    def call(shape, scale=0.0, q=FAKE, c_q=256):
+        return L.scope_sparse_attention_noalloc(ctypes.byref(shape), q, FAKE, FAKE, c_q,
+                                                FAKE, FAKE, FAKE, FAKE,
+                                                ctypes.c_float(scale), FAKE, None)
+    assert call(hy_shape(d=96, ranges=((0, 32, 64), (32, 32, 32)))) == UNSUPPORTED
+    assert call(hy_shape(), scale=float("nan")) == INVALID
+    assert call(hy_shape(), q=None) == INVALID
+    assert call(hy_shape(), c_q=0) == INVALID
+    # heads * (ceil(n / 256) + c_q) work items against the fixed list
+    items = lambda sh, c_q: sh.heads * (-(-sh.n // 256) + c_q)
+    big = hy_shape(heads=96)
+    assert items(big, 256) > 65536
+    assert call(big) == 5
+    assert "no-allocation" in B.status_string(5)
+    assert items(hy_shape(), 256) <= 65536
 
 
 def test_proxy_scores_and_fixexp_validation():
