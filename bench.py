@@ -600,6 +600,189 @@ def traffic_probe():
     log("[probe] attention done")
 
 
+def measured_peaks(torch, dev=None, reps=5):
+    """Achievable roofs on this GPU, measured with the library's diagnostic
+    kernels: a 1 GiB device copy (HBM GB/s counting read + write bytes) and
+    a loop of independent bf16 32x32x16 matrix products from registers."""
+    from paper_2608_12780_amd import binding as B
+    dev = dev or torch.device("cuda", 0)
+    stream = torch.cuda.current_stream()
+    src = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    B.scope_debug_copy(src, dst)
+    torch.cuda.synchronize()
+    c_ms = time_events(torch, lambda: B.scope_debug_copy(src, dst), reps, stream)
+    del src, dst
+    blocks, iters = 2048, 4096
+    out = torch.empty(blocks * 256, dtype=torch.float32, device=dev)
+    B.scope_debug_mfma_loop(out, blocks, 64)
+    torch.cuda.synchronize()
+    m_ms = time_events(torch, lambda: B.scope_debug_mfma_loop(out, blocks, iters), reps, stream)
+    flops = blocks * 4 * 8 * 32768.0 * iters
+    return {"hbm_copy_gbs": round(2 * CALIB_BYTES / (c_ms * 1e-3) / 1e9, 1),
+            "mfma_bf16_tflops": round(flops / (m_ms * 1e-3) / 1e12, 1),
+            "copy_ms": round(c_ms, 4), "mfma_loop_ms": round(m_ms, 4)}
+
+
+def counters_probe():
+    """The program profiled by the counter passes: the measured-peak kernels
+    once (their counters calibrate the others), then the HunyuanVideo-720p-like
+    layer twice (the first run warms up)."""
+    import torch
+    from paper_2608_12780_amd import inputs
+    from paper_2608_12780_amd.layer import ScopeLayer
+    dev = torch.device("cuda", 0)
+    peaks = measured_peaks(torch, dev, reps=1)
+    log(f"[counters] peaks {peaks}")
+    cfg = inputs.CONFIGS["hy720"]
+    x = inputs.generate(cfg)
+    up = lambda b: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
+    q, k, v = up(x.q_bits), up(x.k_bits), up(x.v_bits)
+    layer = ScopeLayer(cfg.heads, cfg.n, cfg.d, cfg.ranges, cfg.c_q, (cfg.c_m,) * 3,
+                       cfg.iters, cfg.rho, cfg.k_fix, dtype=cfg.dtype, device=dev)
+    iq, ik = torch.from_numpy(x.init_q).to(dev), torch.from_numpy(x.init_k).to(dev)
+    for i in range(2):
+        layer.forward(q, k, v, iq, ik)
+        torch.cuda.synchronize()
+        log(f"[counters] layer run {i + 1}/2 done")
+    counts = layer.counts.cpu().numpy().astype(np.float64)
+    selc = layer.sel_counts.cpu().numpy().astype(np.float64)
+    print(json.dumps({"attention_algorithmic_flops": 4.0 * cfg.d * float((counts * selc).sum()),
+                      "selected_total": float(selc.sum()), "peaks": peaks}), flush=True)
+
+
+COUNTER_PASSES = [
+    "SQ_CYCLES SQ_BUSY_CYCLES SQ_WAVE_CYCLES SQ_VALU_MFMA_BUSY_CYCLES SQ_VALU_MFMA_COEXEC_CYCLES "
+    "SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_MFMA SQ_INSTS_VALU GRBM_GUI_ACTIVE",
+    "SQ_INSTS_LDS SQ_WAIT_INST_LDS SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE SQ_INSTS_VALU_TRANS_F32 "
+    "SQ_WAIT_INST_ANY SQ_WAIT_ANY SQ_ACTIVE_INST_VALU",
+    "FETCH_SIZE GRBM_GUI_ACTIVE",
+    "WRITE_SIZE TCC_HIT_sum TCC_MISS_sum",
+    "SQ_INSTS_SALU SQ_INSTS_VMEM SQ_INSTS_SMEM SQ_ACTIVE_INST_LDS SQ_ACTIVE_INST_MISC SQ_WAVES "
+    "SQ_INSTS_VALU_FMA_F32 SQ_INSTS_VALU_MUL_F32 TA_BUSY_avr TA_BUSY_max GRBM_GUI_ACTIVE",
+]
+COUNTER_REGEX = "attn_kernel|km_assign|km_accum|select_base|select_final|code_parts_kernel|peak_"
+# MI355X: 8 XCDs x 4 shader engines x 8 CUs x 4 SIMDs
+XCDS, SIMDS_PER_SE = 8, 32
+
+
+def _short_kernel(name):
+    import re
+    name = re.sub(r"scope::\(anonymous namespace\)::", "", name)
+    name = re.sub(r"^void ", "", name)
+    name = re.sub(r"\(.*$", "", name)
+    return name
+
+
+def counter_summary(csvs, cmd):
+    """Per-kernel table of the counter passes (rocprofv3 --pmc CSVs): MFMA and
+    VALU activity, LDS behaviour, HBM traffic (scaled by the calibration copy)
+    and occupancy from each kernel's resources.  Counters are summed over
+    every SIMD/SE/channel of the GPU by rocprofv3; SQ_CYCLES (per SIMD) is the
+    denominator of per-SIMD busy fractions."""
+    import csv
+    import collections
+    agg = collections.defaultdict(lambda: collections.defaultdict(list))
+    res = {}
+    for path in csvs:
+        per = collections.defaultdict(lambda: collections.defaultdict(float))
+        meta = {}
+        for r in csv.DictReader(open(path)):
+            key = (_short_kernel(r["Kernel_Name"]), r["Dispatch_Id"])
+            per[key][r["Counter_Name"]] += float(r["Counter_Value"])
+            meta[key] = r
+        for (kname, _), cv in per.items():
+            m = meta[(kname, _)]
+            for c, v in cv.items():
+                agg[kname][c].append(v)
+            agg[kname]["_dur_us"].append((int(m["End_Timestamp"]) - int(m["Start_Timestamp"])) / 1e3)
+            res[kname] = dict(vgpr=int(m.get("VGPR_Count") or m.get("Arch_VGPR_Count") or 0),
+                              agpr=int(m.get("Accum_VGPR_Count") or 0),
+                              lds=int(m.get("LDS_Block_Size") or 0),
+                              wg=int(m.get("Workgroup_Size") or 0),
+                              sgpr=int(m.get("SGPR_Count") or 0))
+    mean = {k: {c: float(np.mean(v)) for c, v in d.items()} for k, d in agg.items()}
+
+    def occupancy(r):
+        regs = max(r["vgpr"] + r["agpr"], 1)
+        by_regs = 512 // (((regs + 7) // 8) * 8)
+        waves_per_block = max(1, (r["wg"] + 63) // 64)
+        by_lds = (160 * 1024 // r["lds"]) * waves_per_block / 4.0 if r["lds"] else 8
+        return min(8, by_regs, by_lds)
+
+    cal = mean.get("peak_copy_kernel", {})
+    f_fac = (CALIB_BYTES / 1024.0) / cal["FETCH_SIZE"] if cal.get("FETCH_SIZE") else None
+    w_fac = (CALIB_BYTES / 1024.0) / cal["WRITE_SIZE"] if cal.get("WRITE_SIZE") else None
+    lines = [f"command: {cmd}", "",
+             "rocprofv3 --pmc passes (each its own run):"]
+    lines += [f"  {p}" for p in COUNTER_PASSES]
+    lines += ["",
+              "per kernel, averaged over its dispatches:",
+              "  dur       kernel duration under counter collection (us)",
+              "  GHz       GRBM_GUI_ACTIVE / 8 XCDs / duration: the shader clock during the kernel",
+              "  mfma%     SQ_VALU_MFMA_BUSY_CYCLES / (SQ_CYCLES * 32 SIMDs per shader engine):",
+              "            the matrix pipe's busy fraction, over all 1024 SIMDs",
+              "  valu%     4 * SQ_ACTIVE_INST_VALU / the same SIMD cycles (wave time on VALU issue)",
+              "  coexec%   SQ_VALU_MFMA_COEXEC_CYCLES / SQ_VALU_MFMA_BUSY_CYCLES (a VALU op issued",
+              "            while the matrix pipe was busy)",
+              "  bf16 TF   SQ_INSTS_VALU_MFMA_MOPS_BF16 * 512 / dur (performed, padding included)",
+              "  valu/mfma SQ_INSTS_VALU / SQ_INSTS_MFMA (SQ_INSTS_VALU counts MFMAs too)",
+              "  ldsw%     SQ_WAIT_INST_LDS * 4 / SQ_WAVE_CYCLES*4 (wave time waiting to issue LDS)",
+              "  bank%     SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE",
+              "  wait%     SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES (waiting on a dependency)",
+              "  fetch/write GB  FETCH_SIZE, WRITE_SIZE scaled by the calibration copy of "
+              f"{CALIB_BYTES} bytes",
+              "  GB/s      (fetch + write bytes) / duration",
+              "  TA busy%  TA_BUSY_avr / (GRBM_GUI_ACTIVE / 8): the address unit of buffer loads",
+              "  occ       waves per SIMD the kernel's VGPR+AGPR and LDS allow", ""]
+    if f_fac:
+        lines.append(f"calibration copy: FETCH_SIZE factor {f_fac:.4f}, WRITE_SIZE factor "
+                     f"{(w_fac or float('nan')):.4f}")
+    pk = mean.get("peak_mfma_kernel")
+    if pk and pk.get("SQ_CYCLES"):
+        lines.append(f"MFMA loop: mfma% {100 * pk['SQ_VALU_MFMA_BUSY_CYCLES'] / (pk['SQ_CYCLES'] * SIMDS_PER_SE):.1f}, "
+                     f"clock {pk['GRBM_GUI_ACTIVE'] / XCDS / (pk['_dur_us'] * 1e3):.2f} GHz, "
+                     f"bf16 {pk['SQ_INSTS_VALU_MFMA_MOPS_BF16'] * 512 / (pk['_dur_us'] * 1e-6) / 1e12:.0f} TFLOP/s "
+                     "(the measured matrix roof)")
+    lines += ["", f"{'kernel':<44} {'calls':>5} {'dur us':>9} {'GHz':>5} {'mfma%':>6} {'coexec%':>7} "
+              f"{'valu%':>6} {'bf16 TF':>8} {'valu/mfma':>9} {'ldsw%':>6} {'bank%':>6} {'wait%':>6} "
+              f"{'fetch GB':>9} {'write GB':>9} {'GB/s':>6} {'TA busy%':>8} {'vgpr':>5} {'agpr':>5} "
+              f"{'lds KB':>6} {'occ':>4}"]
+    for kname in sorted(mean, key=lambda k: -mean[k]["_dur_us"] * len(agg[k]["_dur_us"])):
+        m, r = mean[kname], res[kname]
+        g = lambda c: m.get(c)
+        def pct(a, b):
+            return f"{100 * a / b:.1f}" if a is not None and b else "-"
+        # SQ_CYCLES counts each of the SE_INSTANCES shader engines once; the
+        # MFMA busy and VALU activity counts cover every SIMD of the GPU
+        simd_cycles = g("SQ_CYCLES") * SIMDS_PER_SE if g("SQ_CYCLES") else None
+        mf = pct(g("SQ_VALU_MFMA_BUSY_CYCLES"), simd_cycles)
+        va = pct(4 * g("SQ_ACTIVE_INST_VALU") if g("SQ_ACTIVE_INST_VALU") else None, simd_cycles)
+        ghz = (f"{g('GRBM_GUI_ACTIVE') / XCDS / (m['_dur_us'] * 1e3):.2f}"
+               if g("GRBM_GUI_ACTIVE") else "-")
+        co = pct(g("SQ_VALU_MFMA_COEXEC_CYCLES"), g("SQ_VALU_MFMA_BUSY_CYCLES"))
+        tf = (f"{g('SQ_INSTS_VALU_MFMA_MOPS_BF16') * 512 / (m['_dur_us'] * 1e-6) / 1e12:.0f}"
+              if g("SQ_INSTS_VALU_MFMA_MOPS_BF16") else "-")
+        vm = f"{g('SQ_INSTS_VALU') / g('SQ_INSTS_MFMA'):.1f}" if g("SQ_INSTS_MFMA") else "-"
+        lw = pct(g("SQ_WAIT_INST_LDS"), g("SQ_WAVE_CYCLES"))
+        bk = pct(g("SQ_LDS_BANK_CONFLICT"), g("SQ_LDS_IDX_ACTIVE"))
+        wt = pct(g("SQ_WAIT_INST_ANY"), g("SQ_WAVE_CYCLES"))
+        fe = f"{g('FETCH_SIZE') * 1024 * f_fac / 1e9:.3f}" if g("FETCH_SIZE") is not None and f_fac else "-"
+        wr = f"{g('WRITE_SIZE') * 1024 * w_fac / 1e9:.3f}" if g("WRITE_SIZE") is not None and w_fac else "-"
+        ta = (f"{g('TA_BUSY_avr') / (g('GRBM_GUI_ACTIVE') / XCDS) * 100:.1f}"
+              if g("TA_BUSY_avr") and g("GRBM_GUI_ACTIVE") else "-")
+        hbm = ((g("FETCH_SIZE") * f_fac + g("WRITE_SIZE") * w_fac) * 1024 / (m["_dur_us"] * 1e-6) / 1e9
+               if g("FETCH_SIZE") is not None and g("WRITE_SIZE") is not None and f_fac and w_fac else None)
+        hb = f"{hbm:.0f}" if hbm is not None else "-"
+        lines.append(f"{kname[:44]:<44} {len(agg[kname]['_dur_us']):>5} {m['_dur_us']:>9.1f} {ghz:>5} {mf:>6} "
+                     f"{co:>7} {va:>6} {tf:>8} {vm:>9} {lw:>6} {bk:>6} {wt:>6} {fe:>9} {wr:>9} {hb:>6} {ta:>8} "
+                     f"{r['vgpr']:>5} {r['agpr']:>5} {r['lds'] / 1024:>6.1f} {occupancy(r):>4.1f}")
+    lines += ["", "raw means per dispatch:"]
+    for kname in sorted(mean):
+        lines.append(f"  {kname}: " + ", ".join(f"{c}={v:.6g}" for c, v in sorted(mean[kname].items())))
+    return "\n".join(lines) + "\n"
+
+
 def lines_summary(kind, paths, cmd):
     """Table of bench.py JSON lines (one per file): kind "workloads" (one
     line per workload) or "rho" (one line per rho of a workload)."""
@@ -652,6 +835,17 @@ def main():
         return
     if len(sys.argv) >= 2 and sys.argv[1] == "--traffic-probe":
         traffic_probe()
+        return
+    if len(sys.argv) >= 2 and sys.argv[1] == "--counters":
+        counters_probe()
+        return
+    if len(sys.argv) >= 2 and sys.argv[1] == "--counter-summary":
+        # --counter-summary "COMMAND" CSV...
+        sys.stdout.write(counter_summary(sys.argv[3:], sys.argv[2]))
+        return
+    if len(sys.argv) >= 2 and sys.argv[1] == "--peaks":
+        import torch
+        print(json.dumps(measured_peaks(torch)), flush=True)
         return
     if len(sys.argv) >= 2 and sys.argv[1] == "--recall-study":
         print(json.dumps(recall_study()), flush=True)
@@ -784,6 +978,15 @@ def main():
         "k_head_mean": float(khead.mean()),
         "floor_bound_fraction": round(floor_bound, 4),
     }
+
+    # the same roofs measured on this GPU (copy bandwidth, MFMA loop)
+    peaks = measured_peaks(torch, dev)
+    result["measured_peaks"] = peaks
+    result["roofline"]["measured_peak"] = peaks["mfma_bf16_tflops"]
+    result["roofline"]["frac_of_measured"] = round(achieved / peaks["mfma_bf16_tflops"], 4)
+    for k_, h_ in result["hbm"].items():
+        h_["frac_of_measured"] = round(h_["gbs"] / peaks["hbm_copy_gbs"], 4)
+    log(f"[bench] measured peaks: {peaks}")
 
     # one GPU's share of an 8-GPU node when the layer is sharded by head
     share = max(1, math.ceil(cfg.heads / 8))

@@ -307,6 +307,18 @@ int32_t scope_sparse_attention_noalloc(const scope_shape *shape,
                                        const int32_t *sel_idx, float scale,
                                        void *o, void *stream);
 
+/* Diagnostics: the measured peaks that roofline fractions are also quoted
+ * against.  scope_debug_copy copies `bytes` (a multiple of 16; src and dst
+ * 16-byte aligned, not overlapping) with a plain vector copy kernel, so its
+ * time gives the achievable HBM bandwidth (2 * bytes moved).
+ * scope_debug_mfma_loop launches `blocks` blocks of 256 threads whose waves
+ * each issue iters * 8 independent bf16 32x32x16 matrix products from
+ * registers (8 * 32768 * iters flops per wave) and write one float per
+ * thread to out[blocks * 256]: the achievable bf16 MFMA rate.              */
+int32_t scope_debug_copy(const void *src, void *dst, size_t bytes, void *stream);
+int32_t scope_debug_mfma_loop(float *out, int32_t blocks, int32_t iters,
+                              void *stream);
+
 /* Diagnostic: the selection's fixed-point exponential (call 4) applied to
  * y[0..count) (y <= 0), results in out[0..count).                          */
 int32_t scope_debug_fixexp(const float *y, uint64_t *out, int64_t count,

@@ -25,7 +25,7 @@ ENTRY_POINTS = (
     "scope_sparse_attention", "scope_debug_fixexp",
     "scope_partition_workspace_size", "scope_cluster_key_partition",
     "scope_proxy_scores_partition", "scope_select_partition",
-    "scope_sparse_attention_noalloc",
+    "scope_sparse_attention_noalloc", "scope_debug_copy", "scope_debug_mfma_loop",
 )
 MAX_SUBSPACES, MAX_D = 8, 128
 POLICIES = {"online": 0, "fixed": 1, "topp": 2}
@@ -106,6 +106,8 @@ def lib() -> ctypes.CDLL:
         L.scope_sparse_attention_noalloc.argtypes = [SP, P, P, P, I, P, P, P, P,
                                                      ctypes.c_float, P, P]
         L.scope_debug_fixexp.argtypes = [P, P, ctypes.c_int64, P]
+        L.scope_debug_copy.argtypes = [P, P, Z, P]
+        L.scope_debug_mfma_loop.argtypes = [P, I, I, P]
         PP = ctypes.POINTER(Partition)
         L.scope_partition_workspace_size.argtypes = [SP, I, PP, ctypes.POINTER(Z)]
         L.scope_cluster_key_partition.argtypes = [SP, P, PP, I, P, I, P, P, P, Z, P, P]
@@ -279,6 +281,21 @@ def scope_sparse_attention_noalloc(shape, q, k, v, c_q, offsets, perm, sel_count
         _ptr(sel_counts, torch.int32, H * c_q, "sel_counts"),
         _ptr(sel_idx, torch.int32, H * c_q * N, "sel_idx"), float(scale),
         _ptr(o, dt, H * N * D, "o"), _stream(stream)))
+
+
+def scope_debug_copy(src, dst, stream=None):
+    """Copies src into dst (same byte size) with the library's copy kernel."""
+    n = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != n:
+        raise ValueError("src and dst must have the same byte size")
+    _check("scope_debug_copy", lib().scope_debug_copy(
+        _ptr(src, None, None, "src"), _ptr(dst, None, None, "dst"), n, _stream(stream)))
+
+
+def scope_debug_mfma_loop(out, blocks, iters, stream=None):
+    _check("scope_debug_mfma_loop", lib().scope_debug_mfma_loop(
+        _ptr(out, torch.float32, int(blocks) * 256, "out"), int(blocks), int(iters),
+        _stream(stream)))
 
 
 def scope_debug_fixexp(y, out, stream=None):

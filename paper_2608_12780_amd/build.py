@@ -12,7 +12,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libscope.so")
 SOURCES = ["api.cpp", "kmeans.hip", "kmeans_mfma.hip", "kmeans_update.hip", "score.hip",
            "select.hip",
-           "attention.hip"]
+           "attention.hip", "peaks.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [

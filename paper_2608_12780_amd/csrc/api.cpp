@@ -799,6 +799,24 @@ int32_t scope_sparse_attention(const scope_shape *shape, const void *q,
   return SCOPE_OK;
 }
 
+int32_t scope_debug_copy(const void *src, void *dst, size_t bytes, void *stream) {
+  if (bytes % 16) return SCOPE_ERR_INVALID_ARGUMENT;
+  if (bytes == 0) return SCOPE_OK;
+  if (!src || !dst || reinterpret_cast<uintptr_t>(src) % 16 ||
+      reinterpret_cast<uintptr_t>(dst) % 16)
+    return SCOPE_ERR_INVALID_ARGUMENT;
+  const uintptr_t a = reinterpret_cast<uintptr_t>(src), b = reinterpret_cast<uintptr_t>(dst);
+  if (a < b + bytes && b < a + bytes) return SCOPE_ERR_INVALID_ARGUMENT;
+  SCOPE_TRY(scope::peak_copy(src, dst, bytes, static_cast<hipStream_t>(stream)));
+  return SCOPE_OK;
+}
+
+int32_t scope_debug_mfma_loop(float *out, int32_t blocks, int32_t iters, void *stream) {
+  if (!out || blocks < 1 || blocks > (1 << 20) || iters < 1) return SCOPE_ERR_INVALID_ARGUMENT;
+  SCOPE_TRY(scope::peak_mfma(out, blocks, iters, static_cast<hipStream_t>(stream)));
+  return SCOPE_OK;
+}
+
 int32_t scope_debug_fixexp(const float *y, uint64_t *out, int64_t count,
                            void *stream) {
   if (count < 0 || (count > 0 && (!y || !out))) return SCOPE_ERR_INVALID_ARGUMENT;

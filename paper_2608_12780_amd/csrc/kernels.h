@@ -138,6 +138,10 @@ hipError_t select_run(int heads, int n, int c_q, const Subspaces &sub, int d,
 // 32-bit words of the distinct-code scratch of select_run
 size_t select_dedup_words(int heads, int n);
 constexpr int kSelCoarseBins = 2048;  // coarse histogram bins per cluster row
+// Measured-peak microbenchmarks (diagnostics).
+hipError_t peak_copy(const void *src, void *dst, size_t bytes, hipStream_t s);
+hipError_t peak_mfma(float *out, int blocks, int iters, hipStream_t s);
+
 hipError_t debug_fixexp(const float *y, uint64_t *out, int64_t count,
                         hipStream_t s);
 
