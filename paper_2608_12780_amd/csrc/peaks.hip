@@ -11,15 +11,16 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 // Grid-stride copy, four 16-byte loads in flight per lane before the
 // stores; count16 = bytes / 16.
-__global__ __launch_bounds__(256) void peak_copy_kernel(const uint4 *__restrict__ src,
-                                                        uint4 *__restrict__ dst, size_t count16) {
+__global__ __launch_bounds__(256) void peak_copy_kernel(const u32x4 *__restrict__ src,
+                                                        u32x4 *__restrict__ dst, size_t count16) {
   const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
   size_t i = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   for (; i + 3 * stride < count16; i += 4 * stride) {
-    uint4 v[4];
+    u32x4 v[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) v[u] = __builtin_nontemporal_load(&src[i + u * stride]);
 #pragma unroll
@@ -69,7 +70,7 @@ hipError_t peak_copy(const void *src, void *dst, size_t bytes, hipStream_t s) {
   const size_t want = (n16 + 255) / 256;
   const unsigned blocks = static_cast<unsigned>(want < static_cast<size_t>(cus) * 8 ? want : static_cast<size_t>(cus) * 8);
   hipLaunchKernelGGL(peak_copy_kernel, dim3(blocks), dim3(256), 0, s,
-                     static_cast<const uint4 *>(src), static_cast<uint4 *>(dst), n16);
+                     static_cast<const u32x4 *>(src), static_cast<u32x4 *>(dst), n16);
   return hipGetLastError();
 }
 
