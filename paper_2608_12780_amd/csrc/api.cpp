@@ -147,6 +147,7 @@ struct KeyWs {
   uint16_t *ubf[3];
   float *nu[3], *bnd[3];
   float *split;  // shared by the subspaces, whose assignments run in turn
+  char *args3;   // arguments of the one-pass assignment of the three subspaces
 };
 size_t key_ws(const scope_shape *s, const int32_t *c_m, void *base, KeyWs *w) {
   Carver cv(base);
@@ -169,6 +170,7 @@ size_t key_ws(const scope_shape *s, const int32_t *c_m, void *base, KeyWs *w) {
     split = f > split ? f : split;
   }
   k.split = cv.take<float>(split);
+  k.args3 = cv.take<char>(scope::km_assign3_scratch_bytes());
   if (w) *w = k;
   return cv.used;
 }
@@ -477,13 +479,24 @@ int32_t scope_cluster_key_subspaces(const scope_shape *shape, const void *k,
     SCOPE_TRY(scope::km_init(pm, init, 3 * init_stride, dev_status, s));
   }
   const scope::AccPlan plan = key_plan(shape, c_m);
+  // the three assignments in one pass over K when the codebooks fit the LDS
+  // together, else one pass per subspace
+  const bool fused = scope::km_assign3_ok(p);
+  auto assign_all = [&]() -> hipError_t {
+    if (fused) return scope::km_assign3(p, w.args3, s);
+    for (int m = 0; m < 3; ++m) {
+      const hipError_t e = scope::km_assign(p[m], false, s);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  };
   for (int it = 0; it < iters; ++it) {
-    for (int m = 0; m < 3; ++m) SCOPE_TRY(scope::km_assign(p[m], false, s));
+    SCOPE_TRY(assign_all());
     SCOPE_TRY(scope::km_accum(plan, k, p[0].bf16, p[0].x_head_stride, d, n, shape->heads,
                               w.assign3, static_cast<size_t>(3) * n, n, w.slab, w.cslab,
                               k_centroids, per_head, it == 0 ? dev_status : nullptr, s));
   }
-  for (int m = 0; m < 3; ++m) SCOPE_TRY(scope::km_assign(p[m], false, s));
+  SCOPE_TRY(assign_all());
   SCOPE_TRY(scope::km_pack_codes(w.assign3, static_cast<size_t>(3) * n, n, n,
                                  shape->heads, codes, s));
   return SCOPE_OK;

@@ -56,6 +56,12 @@ hipError_t km_init(const KmProblem &p, const int32_t *init, int init_stride,
                    int32_t *status, hipStream_t s);
 hipError_t km_assign(const KmProblem &p, bool with_hist, hipStream_t s);
 hipError_t km_group(const KmProblem &p, hipStream_t s);
+// The three key subspaces' assignments in one pass over the rows (matrix
+// cores; codebooks side by side in LDS): applies when km_assign3_ok.
+bool km_assign3_ok(const KmProblem (&p)[3]);
+// scratch: km_assign3_scratch_bytes() of device memory (its arguments)
+size_t km_assign3_scratch_bytes();
+hipError_t km_assign3(const KmProblem (&p)[3], void *scratch, hipStream_t s);
 
 // Centroid update by one streaming pass over the rows.  Up to kMaxSub
 // subspaces of the same rows (channels col0[m] .. col0[m]+dx[m], C[m]

@@ -181,6 +181,284 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// The bound constants of one head's codebook (maxima of the per-row parts,
+// with a small upward slack on top of their fp64 evaluation).
+struct FilterBound {
+  float E, Nmax, numax;
+};
+
+// The head's bound constants from the per-wave maxima in red.
+template <int NW>
+__device__ __forceinline__ FilterBound reduce_bound(const float (*red)[NW]) {
+  float E = 0.0f, Nmax = 0.0f, numax = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    E = fmaxf(E, red[0][i]);
+    Nmax = fmaxf(Nmax, red[1][i]);
+    numax = fmaxf(numax, red[2][i]);
+  }
+  E = E * 1.001f + 1e-30f;
+  Nmax *= 1.001f;
+  numax *= 1.001f;
+  return FilterBound{E, Nmax, numax};
+}
+
+// Stages head h's two-term codebook (16-byte pieces of each row; LDS row
+// stride 2 DXP + 8) and its norms into LDS and returns the head's bound
+// constants.  Ends with a block barrier; the caller makes sure no wave still
+// reads the previous contents.
+template <int DXP, int NW = kWavesPerBlock>
+__device__ __forceinline__ FilterBound stage_codebook(uint16_t *Us, float *nus,
+                                                      float (*red)[NW],
+                                                      const uint16_t *__restrict__ ubf,
+                                                      const float *__restrict__ nu,
+                                                      const float *__restrict__ bnd, int h,
+                                                      int C, int cpad) {
+  constexpr int US = 2 * DXP + 8;
+  const int t = threadIdx.x;
+  const int lane = t & 63, w = t >> 6;
+  const uint16_t *ub = ubf + static_cast<size_t>(h) * cpad * (2 * DXP);
+  for (int e = t; e < cpad * (DXP / 4); e += 64 * NW) {
+    const int r = e / (DXP / 4), q = e % (DXP / 4);
+    *reinterpret_cast<uint4 *>(&Us[r * US + 8 * q]) =
+        *reinterpret_cast<const uint4 *>(ub + static_cast<size_t>(r) * (2 * DXP) + 8 * q);
+  }
+  // the head's bound constants: maxima of the per-row parts, with a small
+  // upward slack on top of their fp64 evaluation
+  float e_max = 0.0f, n_max = 0.0f, nu_max = 0.0f;
+  for (int r = t; r < cpad; r += 64 * NW) {
+    const size_t row = static_cast<size_t>(h) * cpad + r;
+    const float v = nu[row];
+    nus[r] = v;
+    if (r < C) {
+      e_max = fmaxf(e_max, bnd[2 * row + 0]);
+      n_max = fmaxf(n_max, bnd[2 * row + 1]);
+      nu_max = fmaxf(nu_max, fabsf(v));
+    }
+  }
+  e_max = wave_max(e_max);
+  n_max = wave_max(n_max);
+  nu_max = wave_max(nu_max);
+  if (lane == 0) {
+    red[0][w] = e_max;
+    red[1][w] = n_max;
+    red[2][w] = nu_max;
+  }
+  __syncthreads();
+  return reduce_bound<NW>(red);
+}
+
+// One codebook's view of the rows: channels col0 .. col0+dx of X[h] (row
+// stride ld), C centroids (padded to cpad) U[h] in fp32 for the canonical
+// re-score, and where the assignment goes.
+struct SliceArgs {
+  const uint16_t *X;
+  size_t x_hs;
+  int ld, col0, dx, n, C, cpad;
+  const float *U;
+  size_t u_hs;
+  int32_t *assign;
+  size_t a_hs;
+  int32_t *chunk_hist;
+  int nchunks;
+};
+
+// The assignment of the 32 points of slice sl of head h by one wave, against
+// the codebook staged in Us/nus with bound constants B (candidate scratch of
+// this wave: cand, best, ncand).
+template <int DXP>
+__device__ __forceinline__ void assign_slice(const SliceArgs &A, const uint16_t *Us,
+                                             const float *nus, FilterBound B, int h, int sl,
+                                             uint32_t *cand_w, unsigned long long *best_w,
+                                             int *ncand_w) {
+  constexpr int US = 2 * DXP + 8;  // LDS row stride of the two-term codebook
+  constexpr int KS = DXP / 16;     // MFMA k-steps per term
+  const int lane = threadIdx.x & 63, l32 = lane & 31, hf = lane >> 5;
+  const uint16_t *X = A.X;
+  const size_t x_hs = A.x_hs;
+  const int ld = A.ld, col0 = A.col0, dx = A.dx, n = A.n, C = A.C, cpad = A.cpad;
+  int32_t *assign = A.assign;
+  const size_t a_hs = A.a_hs;
+  int32_t *chunk_hist = A.chunk_hist;
+  const int nchunks = A.nchunks;
+  const float E = B.E, Nmax = B.Nmax, numax = B.numax;
+  const float kappa = 8.0f * DXP * 0x1p-24f;
+  // index bits packed into the low mantissa of the scores
+  const int ib = 32 - __clz(cpad - 1);
+  const uint32_t imask = (1u << ib) - 1u;
+  const float dpack = __uint_as_float(static_cast<uint32_t>(127 + ib - 23) << 23);  // 2^(ib-23)
+  // every row's first channel is 16-byte aligned
+  const bool vec = ((reinterpret_cast<uintptr_t>(X + col0) & 15) | ((x_hs | static_cast<size_t>(ld)) & 7)) == 0;
+  const float *Uh = A.U + h * A.u_hs;
+  const int i = sl * 32 + l32;
+  const bool valid = i < n;
+  const uint16_t *xrow = X + h * x_hs + static_cast<size_t>(valid ? i : 0) * ld + col0;
+  bf16x8 xf[KS];
+  float ss = 0.0f;
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    const uint4 v4 = load_group8(xrow, 16 * s + 8 * hf, dx, valid, vec);
+    const uint32_t wv[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float a = __uint_as_float(wv[q] << 16), b = __uint_as_float(wv[q] & 0xFFFF0000u);
+      ss = fmaf(a, a, ss);
+      ss = fmaf(b, b, ss);
+    }
+    xf[s] = __builtin_bit_cast(bf16x8, v4);
+  }
+  ss += __shfl_xor(ss, 32);
+  const float nx = sqrtf(ss) * 1.0001f + 1e-30f;
+  const float beta = (2.0f * nx * (E + kappa * Nmax) +
+                      0x1p-23f * (numax + 2.02f * nx * Nmax)) * 1.01f + 1e-25f;
+
+  // approximate scores of the 32 centroids rb .. rb+31 for the 32 points
+  auto chain = [&](int rb) {
+    f32x16 acc;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+    const uint16_t *urow = &Us[(rb + l32) * US + 8 * hf];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const bf16x8 a_hi = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(urow + 16 * s));
+      const bf16x8 a_lo = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(urow + DXP + 16 * s));
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_hi, xf[s], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_lo, xf[s], acc, 0, 0, 0);
+    }
+    return acc;
+  };
+  // one pass: the three smallest packed scores per point (each med3 keeps
+  // the smaller two of its inputs' upper pair; the start value lies above
+  // every score of valid inputs)
+  float m1 = 0x1.1p127f, m2 = 0x1.1p127f, m3 = 0x1.1p127f;
+  auto fold = [&](const f32x16 &acc, int rb) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const uint32_t r = static_cast<uint32_t>(rb + 8 * (e >> 2) + 4 * hf + (e & 3));
+      const float sc = fmaf(-2.0f, acc[e], nus[r]);
+      const float sp = __uint_as_float((__float_as_uint(sc) & ~imask) | r);
+      m3 = __builtin_amdgcn_fmed3f(m2, m3, sp);
+      m2 = __builtin_amdgcn_fmed3f(m1, m2, sp);
+      m1 = __builtin_amdgcn_fmed3f(m1, sp, -0x1.1p127f);
+    }
+  };
+  // software pipeline: the scores of block rb are folded while the
+  // MFMAs of block rb + 32 run
+  f32x16 prev = chain(0);
+  for (int rb = 32; rb < cpad; rb += 32) {
+    const f32x16 cur = chain(rb);
+    fold(prev, rb - 32);
+    prev = cur;
+    // each MFMA of this block is followed by an LDS read and a share
+    // of the previous block's fold
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+    for (int k = 0; k < 2 * KS; ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+    }
+  }
+  fold(prev, cpad - 32);
+  {
+    // the other half-wave's three into this one's (same multiset, same
+    // result in both halves)
+    const float o[3] = {__shfl_xor(m1, 32), __shfl_xor(m2, 32), __shfl_xor(m3, 32)};
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      m3 = __builtin_amdgcn_fmed3f(m2, m3, o[q]);
+      m2 = __builtin_amdgcn_fmed3f(m1, m2, o[q]);
+      m1 = fminf(m1, o[q]);
+    }
+  }
+  const float slack = (2.0f * beta + 2.0f * dpack * fabsf(m1)) * 1.001f;
+  const float lim = m1 + slack;
+  const float thr = lim + fabsf(lim) * 2e-6f + 1e-30f;
+  const bool needy = valid && !(m2 > thr);
+  // three or more candidates (very rare)
+  const bool wide = needy && !(m3 > thr);
+  int arg = static_cast<int>(__float_as_uint(m1) & imask);
+
+  if (__ballot(needy && !wide)) {
+    // exactly two candidates, the two smallest packed scores: the point's
+    // two half-wave lanes re-score one each canonically and exchange
+    unsigned long long key = ~0ull;
+    if (needy && !wide) {
+      const int r = min(static_cast<int>(__float_as_uint(hf ? m2 : m1) & imask), C - 1);
+      const uint16_t *xr = X + h * x_hs + static_cast<size_t>(i) * ld + col0;
+      const float dot = canon_dot(xr, Uh + static_cast<size_t>(r) * dx, dx);
+      const float sc = fmaf(-2.0f, dot, nus[r]) + 0.0f;
+      key = (static_cast<unsigned long long>(asc_key(sc)) << 32) | static_cast<unsigned>(r);
+    }
+    const uint32_t ok_lo = __shfl_xor(static_cast<uint32_t>(key), 32);
+    const uint32_t ok_hi = __shfl_xor(static_cast<uint32_t>(key >> 32), 32);
+    const unsigned long long other = (static_cast<unsigned long long>(ok_hi) << 32) | ok_lo;
+    if (needy && !wide) arg = static_cast<int>((key < other ? key : other) & 0xFFFFFFFFu);
+  }
+  if (__ballot(wide)) {
+    // every candidate of the wide points, re-scored canonically
+    wave_sync();
+    if (lane == 0) *ncand_w = 0;
+    if (lane < 32) best_w[lane] = ~0ull;
+    wave_sync();
+    bool over = false;
+    for (int rb = 0; rb < cpad; rb += 32) {
+      const f32x16 acc = chain(rb);
+      if (wide) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const uint32_t r = static_cast<uint32_t>(rb + 8 * (e >> 2) + 4 * hf + (e & 3));
+          const float sc = fmaf(-2.0f, acc[e], nus[r]);
+          const float sp = __uint_as_float((__float_as_uint(sc) & ~imask) | r);
+          if (static_cast<int>(r) < C && sp <= thr) {
+            const int slot = atomicAdd(ncand_w, 1);
+            if (slot < kWaveCand)
+              cand_w[slot] = (static_cast<uint32_t>(l32) << 16) | r;
+            else
+              over = true;
+          }
+        }
+      }
+    }
+    // a point whose candidates did not fit scans every centroid
+    const bool full = __shfl_xor(static_cast<int>(over), 32) || over;
+    wave_sync();
+    const int cnt = min(*ncand_w, kWaveCand);
+    for (int k = lane; k < cnt; k += 64) {
+      const uint32_t pr = cand_w[k];
+      const int q = static_cast<int>(pr >> 16), r = static_cast<int>(pr & 0xFFFFu);
+      const uint16_t *xr = X + h * x_hs + static_cast<size_t>(sl * 32 + q) * ld + col0;
+      const float *u = Uh + static_cast<size_t>(r) * dx;
+      const float dot = canon_dot(xr, u, dx);
+      const float sc = fmaf(-2.0f, dot, nus[r]) + 0.0f;
+      atomicMin(&best_w[q], (static_cast<unsigned long long>(asc_key(sc)) << 32) | static_cast<unsigned>(r));
+    }
+    wave_sync();
+    if (wide && hf == 0) {
+      unsigned long long b = best_w[l32];
+      if (full) {
+        const uint16_t *xr = X + h * x_hs + static_cast<size_t>(i) * ld + col0;
+        b = ~0ull;
+        for (int r = 0; r < C; ++r) {
+          const float *u = Uh + static_cast<size_t>(r) * dx;
+          const float dot = canon_dot(xr, u, dx);
+          const float sc = fmaf(-2.0f, dot, nus[r]) + 0.0f;
+          const unsigned long long key = (static_cast<unsigned long long>(asc_key(sc)) << 32) | static_cast<unsigned>(r);
+          b = key < b ? key : b;
+        }
+      }
+      arg = b == ~0ull ? 0 : static_cast<int>(b & 0xFFFFFFFFu);
+    }
+    arg = __shfl(arg, l32);  // the lower half-wave holds the result
+  }
+  if (valid && hf == 0) {
+    arg = min(max(arg, 0), C - 1);
+    assign[h * a_hs + i] = arg;
+    if (chunk_hist)
+      atomicAdd(&chunk_hist[(static_cast<size_t>(h) * nchunks + (i / kAssignBlock)) * C + arg], 1);
+  }
+}
+
 template <int DXP>
 __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
     const uint16_t *__restrict__ X, size_t x_hs, int ld, int col0, int dx,
@@ -188,25 +466,15 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
     const uint16_t *__restrict__ ubf, const float *__restrict__ nu,
     const float *__restrict__ bnd, int C, int cpad, int32_t *assign,
     size_t a_hs, int32_t *chunk_hist, int nchunks) {
-  constexpr int US = 2 * DXP + 8;  // LDS row stride of the two-term codebook
-  constexpr int KS = DXP / 16;     // MFMA k-steps per term
   __shared__ __attribute__((aligned(16))) uint16_t Us[kUbfLds];
   __shared__ float nus[kMaxCpad];
   __shared__ uint32_t cand[kWavesPerBlock][kWaveCand];
   __shared__ unsigned long long best[kWavesPerBlock][32];
   __shared__ int ncand[kWavesPerBlock];
   __shared__ float red[3][kWavesPerBlock];
-  const int t = threadIdx.x;
-  const int lane = t & 63, w = t >> 6, l32 = lane & 31, hf = lane >> 5;
-
-  const float kappa = 8.0f * DXP * 0x1p-24f;
-  // index bits packed into the low mantissa of the scores
-  const int ib = 32 - __clz(cpad - 1);
-  const uint32_t imask = (1u << ib) - 1u;
-  const float dpack = __uint_as_float(static_cast<uint32_t>(127 + ib - 23) << 23);  // 2^(ib-23)
+  const int w = threadIdx.x >> 6;
+  const SliceArgs A{X, x_hs, ld, col0, dx, n, C, cpad, U, u_hs, assign, a_hs, chunk_hist, nchunks};
   const int nslices = (n + 31) / 32;
-  // every row's first channel is 16-byte aligned
-  const bool vec = ((reinterpret_cast<uintptr_t>(X + col0) & 15) | ((x_hs | static_cast<size_t>(ld)) & 7)) == 0;
 
   // this block's contiguous range of (head, slice) pairs
   const long long total = static_cast<long long>(heads) * nslices;
@@ -217,216 +485,79 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
     const int h = static_cast<int>(beg / nslices);
     const long long seg_end = end < static_cast<long long>(h + 1) * nslices
                                   ? end : static_cast<long long>(h + 1) * nslices;
-    // stage this head's codebook (16-byte pieces of each row) and norms
     __syncthreads();
-    const uint16_t *ub = ubf + static_cast<size_t>(h) * cpad * (2 * DXP);
-    for (int e = t; e < cpad * (DXP / 4); e += 64 * kWavesPerBlock) {
-      const int r = e / (DXP / 4), q = e % (DXP / 4);
-      *reinterpret_cast<uint4 *>(&Us[r * US + 8 * q]) =
-          *reinterpret_cast<const uint4 *>(ub + static_cast<size_t>(r) * (2 * DXP) + 8 * q);
-    }
-    // the head's bound constants: maxima of the per-row parts, with a small
-    // upward slack on top of their fp64 evaluation
-    float e_max = 0.0f, n_max = 0.0f, nu_max = 0.0f;
-    for (int r = t; r < cpad; r += 64 * kWavesPerBlock) {
-      const size_t row = static_cast<size_t>(h) * cpad + r;
-      const float v = nu[row];
-      nus[r] = v;
-      if (r < C) {
-        e_max = fmaxf(e_max, bnd[2 * row + 0]);
-        n_max = fmaxf(n_max, bnd[2 * row + 1]);
-        nu_max = fmaxf(nu_max, fabsf(v));
-      }
-    }
-    e_max = wave_max(e_max);
-    n_max = wave_max(n_max);
-    nu_max = wave_max(nu_max);
-    if (lane == 0) {
-      red[0][w] = e_max;
-      red[1][w] = n_max;
-      red[2][w] = nu_max;
-    }
+    const FilterBound B = stage_codebook<DXP>(Us, nus, red, ubf, nu, bnd, h, C, cpad);
+    for (long long g = beg + w; g < seg_end; g += kWavesPerBlock)
+      assign_slice<DXP>(A, Us, nus, B, h, static_cast<int>(g - static_cast<long long>(h) * nslices),
+                        cand[w], best[w], &ncand[w]);
+    beg = seg_end;
+  }
+}
+
+// The three key subspaces in one pass over the rows: their codebooks are
+// staged in LDS side by side (subspace m at element offset uoff[m] and norm
+// offset noff[m]), and the block's waves are split into three groups, group
+// m assigning subspace m over the block's slices.  The groups walk the same
+// slices in the same order, so a row fetched from HBM by one group is found
+// in cache by the others, and each wave keeps the registers of a single
+// codebook width.  Group sizes follow the subspaces' work (wave0[m] is the
+// first wave of group m, wave0[3] = the block's wave count).
+struct Sub3 {
+  SliceArgs a[3];
+  const uint16_t *ubf[3];
+  const float *nu[3];
+  const float *bnd[3];
+  int uoff[3], noff[3];
+  int wave0[4];
+};
+
+template <int D0, int D1, int D2>
+__global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma3_kernel(
+    const Sub3 *__restrict__ Sp, int n, int heads) {
+  __shared__ __attribute__((aligned(16))) uint16_t Us[kUbfLds];
+  __shared__ float nus[kMaxCpad];
+  __shared__ uint32_t cand[kWavesPerBlock][kWaveCand];
+  __shared__ unsigned long long best[kWavesPerBlock][32];
+  __shared__ int ncand[kWavesPerBlock];
+  __shared__ float red[3][3][kWavesPerBlock];
+  const int w = threadIdx.x >> 6;
+  const int nslices = (n + 31) / 32;
+  const long long total = static_cast<long long>(heads) * nslices;
+  const long long per = (total + gridDim.x - 1) / gridDim.x;
+  long long beg = static_cast<long long>(blockIdx.x) * per;
+  const long long end = beg + per < total ? beg + per : total;
+  while (beg < end) {
+    const int h = static_cast<int>(beg / nslices);
+    const long long seg_end = end < static_cast<long long>(h + 1) * nslices
+                                  ? end : static_cast<long long>(h + 1) * nslices;
     __syncthreads();
-    float E = 0.0f, Nmax = 0.0f, numax = 0.0f;
-#pragma unroll
-    for (int i = 0; i < kWavesPerBlock; ++i) {
-      E = fmaxf(E, red[0][i]);
-      Nmax = fmaxf(Nmax, red[1][i]);
-      numax = fmaxf(numax, red[2][i]);
-    }
-    E = E * 1.001f + 1e-30f;
-    Nmax *= 1.001f;
-    numax *= 1.001f;
-    const float *Uh = U + h * u_hs;
-    for (long long g = beg + w; g < seg_end; g += kWavesPerBlock) {
-      const int sl = static_cast<int>(g - static_cast<long long>(h) * nslices);
-      const int i = sl * 32 + l32;
-      const bool valid = i < n;
-      const uint16_t *xrow = X + h * x_hs + static_cast<size_t>(valid ? i : 0) * ld + col0;
-      bf16x8 xf[KS];
-      float ss = 0.0f;
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const uint4 v4 = load_group8(xrow, 16 * s + 8 * hf, dx, valid, vec);
-        const uint32_t wv[4] = {v4.x, v4.y, v4.z, v4.w};
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float a = __uint_as_float(wv[q] << 16), b = __uint_as_float(wv[q] & 0xFFFF0000u);
-          ss = fmaf(a, a, ss);
-          ss = fmaf(b, b, ss);
-        }
-        xf[s] = __builtin_bit_cast(bf16x8, v4);
-      }
-      ss += __shfl_xor(ss, 32);
-      const float nx = sqrtf(ss) * 1.0001f + 1e-30f;
-      const float beta = (2.0f * nx * (E + kappa * Nmax) +
-                          0x1p-23f * (numax + 2.02f * nx * Nmax)) * 1.01f + 1e-25f;
-
-      // approximate scores of the 32 centroids rb .. rb+31 for the 32 points
-      auto chain = [&](int rb) {
-        f32x16 acc;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
-        const uint16_t *urow = &Us[(rb + l32) * US + 8 * hf];
-#pragma unroll
-        for (int s = 0; s < KS; ++s) {
-          const bf16x8 a_hi = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(urow + 16 * s));
-          const bf16x8 a_lo = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(urow + DXP + 16 * s));
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_hi, xf[s], acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_lo, xf[s], acc, 0, 0, 0);
-        }
-        return acc;
-      };
-      // one pass: the three smallest packed scores per point (each med3 keeps
-      // the smaller two of its inputs' upper pair; the start value lies above
-      // every score of valid inputs)
-      float m1 = 0x1.1p127f, m2 = 0x1.1p127f, m3 = 0x1.1p127f;
-      auto fold = [&](const f32x16 &acc, int rb) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const uint32_t r = static_cast<uint32_t>(rb + 8 * (e >> 2) + 4 * hf + (e & 3));
-          const float sc = fmaf(-2.0f, acc[e], nus[r]);
-          const float sp = __uint_as_float((__float_as_uint(sc) & ~imask) | r);
-          m3 = __builtin_amdgcn_fmed3f(m2, m3, sp);
-          m2 = __builtin_amdgcn_fmed3f(m1, m2, sp);
-          m1 = __builtin_amdgcn_fmed3f(m1, sp, -0x1.1p127f);
-        }
-      };
-      // software pipeline: the scores of block rb are folded while the
-      // MFMAs of block rb + 32 run
-      f32x16 prev = chain(0);
-      for (int rb = 32; rb < cpad; rb += 32) {
-        const f32x16 cur = chain(rb);
-        fold(prev, rb - 32);
-        prev = cur;
-        // each MFMA of this block is followed by an LDS read and a share
-        // of the previous block's fold
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-#pragma unroll
-        for (int k = 0; k < 2 * KS; ++k) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
-        }
-      }
-      fold(prev, cpad - 32);
-      {
-        // the other half-wave's three into this one's (same multiset, same
-        // result in both halves)
-        const float o[3] = {__shfl_xor(m1, 32), __shfl_xor(m2, 32), __shfl_xor(m3, 32)};
-#pragma unroll
-        for (int q = 0; q < 3; ++q) {
-          m3 = __builtin_amdgcn_fmed3f(m2, m3, o[q]);
-          m2 = __builtin_amdgcn_fmed3f(m1, m2, o[q]);
-          m1 = fminf(m1, o[q]);
-        }
-      }
-      const float slack = (2.0f * beta + 2.0f * dpack * fabsf(m1)) * 1.001f;
-      const float lim = m1 + slack;
-      const float thr = lim + fabsf(lim) * 2e-6f + 1e-30f;
-      const bool needy = valid && !(m2 > thr);
-      // three or more candidates (very rare)
-      const bool wide = needy && !(m3 > thr);
-      int arg = static_cast<int>(__float_as_uint(m1) & imask);
-
-      if (__ballot(needy && !wide)) {
-        // exactly two candidates, the two smallest packed scores: the point's
-        // two half-wave lanes re-score one each canonically and exchange
-        unsigned long long key = ~0ull;
-        if (needy && !wide) {
-          const int r = min(static_cast<int>(__float_as_uint(hf ? m2 : m1) & imask), C - 1);
-          const uint16_t *xr = X + h * x_hs + static_cast<size_t>(i) * ld + col0;
-          const float dot = canon_dot(xr, Uh + static_cast<size_t>(r) * dx, dx);
-          const float sc = fmaf(-2.0f, dot, nus[r]) + 0.0f;
-          key = (static_cast<unsigned long long>(asc_key(sc)) << 32) | static_cast<unsigned>(r);
-        }
-        const uint32_t ok_lo = __shfl_xor(static_cast<uint32_t>(key), 32);
-        const uint32_t ok_hi = __shfl_xor(static_cast<uint32_t>(key >> 32), 32);
-        const unsigned long long other = (static_cast<unsigned long long>(ok_hi) << 32) | ok_lo;
-        if (needy && !wide) arg = static_cast<int>((key < other ? key : other) & 0xFFFFFFFFu);
-      }
-      if (__ballot(wide)) {
-        // every candidate of the wide points, re-scored canonically
-        wave_sync();
-        if (lane == 0) ncand[w] = 0;
-        if (lane < 32) best[w][lane] = ~0ull;
-        wave_sync();
-        bool over = false;
-        for (int rb = 0; rb < cpad; rb += 32) {
-          const f32x16 acc = chain(rb);
-          if (wide) {
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-              const uint32_t r = static_cast<uint32_t>(rb + 8 * (e >> 2) + 4 * hf + (e & 3));
-              const float sc = fmaf(-2.0f, acc[e], nus[r]);
-              const float sp = __uint_as_float((__float_as_uint(sc) & ~imask) | r);
-              if (static_cast<int>(r) < C && sp <= thr) {
-                const int slot = atomicAdd(&ncand[w], 1);
-                if (slot < kWaveCand)
-                  cand[w][slot] = (static_cast<uint32_t>(l32) << 16) | r;
-                else
-                  over = true;
-              }
-            }
-          }
-        }
-        // a point whose candidates did not fit scans every centroid
-        const bool full = __shfl_xor(static_cast<int>(over), 32) || over;
-        wave_sync();
-        const int cnt = min(ncand[w], kWaveCand);
-        for (int k = lane; k < cnt; k += 64) {
-          const uint32_t pr = cand[w][k];
-          const int q = static_cast<int>(pr >> 16), r = static_cast<int>(pr & 0xFFFFu);
-          const uint16_t *xr = X + h * x_hs + static_cast<size_t>(sl * 32 + q) * ld + col0;
-          const float *u = Uh + static_cast<size_t>(r) * dx;
-          const float dot = canon_dot(xr, u, dx);
-          const float sc = fmaf(-2.0f, dot, nus[r]) + 0.0f;
-          atomicMin(&best[w][q], (static_cast<unsigned long long>(asc_key(sc)) << 32) | static_cast<unsigned>(r));
-        }
-        wave_sync();
-        if (wide && hf == 0) {
-          unsigned long long b = best[w][l32];
-          if (full) {
-            const uint16_t *xr = X + h * x_hs + static_cast<size_t>(i) * ld + col0;
-            b = ~0ull;
-            for (int r = 0; r < C; ++r) {
-              const float *u = Uh + static_cast<size_t>(r) * dx;
-              const float dot = canon_dot(xr, u, dx);
-              const float sc = fmaf(-2.0f, dot, nus[r]) + 0.0f;
-              const unsigned long long key = (static_cast<unsigned long long>(asc_key(sc)) << 32) | static_cast<unsigned>(r);
-              b = key < b ? key : b;
-            }
-          }
-          arg = b == ~0ull ? 0 : static_cast<int>(b & 0xFFFFFFFFu);
-        }
-        arg = __shfl(arg, l32);  // the lower half-wave holds the result
-      }
-      if (valid && hf == 0) {
-        arg = min(max(arg, 0), C - 1);
-        assign[h * a_hs + i] = arg;
-        if (chunk_hist)
-          atomicAdd(&chunk_hist[(static_cast<size_t>(h) * nchunks + (i / kAssignBlock)) * C + arg], 1);
-      }
+    stage_codebook<D0>(Us + Sp->uoff[0], nus + Sp->noff[0], red[0], Sp->ubf[0], Sp->nu[0],
+                       Sp->bnd[0], h, Sp->a[0].C, Sp->a[0].cpad);
+    stage_codebook<D1>(Us + Sp->uoff[1], nus + Sp->noff[1], red[1], Sp->ubf[1], Sp->nu[1],
+                       Sp->bnd[1], h, Sp->a[1].C, Sp->a[1].cpad);
+    stage_codebook<D2>(Us + Sp->uoff[2], nus + Sp->noff[2], red[2], Sp->ubf[2], Sp->nu[2],
+                       Sp->bnd[2], h, Sp->a[2].C, Sp->a[2].cpad);
+    const long long first = static_cast<long long>(h) * nslices;
+    const int m = w < Sp->wave0[1] ? 0 : w < Sp->wave0[2] ? 1 : 2;
+    const int wi = w - Sp->wave0[m], nw = Sp->wave0[m + 1] - Sp->wave0[m];
+    if (m == 0) {
+      const SliceArgs A = Sp->a[0];
+      const FilterBound B = reduce_bound<kWavesPerBlock>(red[0]);
+      for (long long g = beg + wi; g < seg_end; g += nw)
+        assign_slice<D0>(A, Us + Sp->uoff[0], nus + Sp->noff[0], B, h, static_cast<int>(g - first),
+                         cand[w], best[w], &ncand[w]);
+    } else if (m == 1) {
+      const SliceArgs A = Sp->a[1];
+      const FilterBound B = reduce_bound<kWavesPerBlock>(red[1]);
+      for (long long g = beg + wi; g < seg_end; g += nw)
+        assign_slice<D1>(A, Us + Sp->uoff[1], nus + Sp->noff[1], B, h, static_cast<int>(g - first),
+                         cand[w], best[w], &ncand[w]);
+    } else {
+      const SliceArgs A = Sp->a[2];
+      const FilterBound B = reduce_bound<kWavesPerBlock>(red[2]);
+      for (long long g = beg + wi; g < seg_end; g += nw)
+        assign_slice<D2>(A, Us + Sp->uoff[2], nus + Sp->noff[2], B, h, static_cast<int>(g - first),
+                         cand[w], best[w], &ncand[w]);
     }
     beg = seg_end;
   }
@@ -698,7 +829,107 @@ hipError_t launch_mfma(const KmProblem &p, bool with_hist, hipStream_t s) {
   return hipGetLastError();
 }
 
+__global__ void store_sub3_kernel(Sub3 S, Sub3 *dst) { *dst = S; }
+
+template <int D0, int D1, int D2>
+hipError_t launch_mfma3(const KmProblem (&p)[3], Sub3 *dev_args, hipStream_t s) {
+  Sub3 S{};
+  int uoff = 0, noff = 0;
+  const int dxp[3] = {D0, D1, D2};
+  for (int m = 0; m < 3; ++m) {
+    const KmProblem &q = p[m];
+    S.a[m] = SliceArgs{static_cast<const uint16_t *>(q.x), q.x_head_stride, q.ld, q.col0, q.dx,
+                       q.n, q.C, q.cpad, q.u, q.u_head_stride, q.assign, q.a_head_stride,
+                       nullptr, 0};
+    S.ubf[m] = q.ubf;
+    S.nu[m] = q.nu;
+    S.bnd[m] = q.bnd;
+    S.uoff[m] = uoff;
+    S.noff[m] = noff;
+    uoff += q.cpad * (2 * dxp[m] + 8);
+    noff += q.cpad;
+  }
+  // waves per group in proportion to each subspace's work per slice: the
+  // fold (per centroid) plus the matrix products (per centroid and 16
+  // channels, two terms), at least two waves each
+  double work[3], tot = 0.0;
+  for (int m = 0; m < 3; ++m) {
+    work[m] = p[m].cpad * (1.0 + 0.25 * dxp[m] / 16.0);
+    tot += work[m];
+  }
+  S.wave0[0] = 0;
+  for (int m = 0; m < 2; ++m) {
+    int wm = static_cast<int>(work[m] / tot * kWavesPerBlock + 0.5);
+    wm = wm < 2 ? 2 : wm;
+    S.wave0[m + 1] = S.wave0[m] + wm;
+  }
+  if (S.wave0[2] > kWavesPerBlock - 2) S.wave0[2] = kWavesPerBlock - 2;
+  if (S.wave0[1] > S.wave0[2] - 2) S.wave0[1] = S.wave0[2] - 2;
+  S.wave0[3] = kWavesPerBlock;
+  const long long slices = static_cast<long long>(p[0].heads) * ((p[0].n + 31) / 32);
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    cus = 256;
+  const int blocks = static_cast<int>(slices < static_cast<long long>(cus) * kWavesPerBlock
+                                          ? (slices + kWavesPerBlock - 1) / kWavesPerBlock : cus);
+  // the arguments go to device memory, so each wave group loads only its own
+  hipLaunchKernelGGL(store_sub3_kernel, dim3(1), dim3(1), 0, s, S, dev_args);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((km_assign_mfma3_kernel<D0, D1, D2>), dim3(blocks), dim3(64 * kWavesPerBlock),
+                     0, s, dev_args, p[0].n, p[0].heads);
+  return hipGetLastError();
+}
+
+template <int DXP>
+hipError_t prep(const KmProblem &p, hipStream_t s) {
+  hipLaunchKernelGGL(km_prep_kernel<DXP>, dim3((p.cpad + 3) / 4, p.heads), dim3(256), 0, s, p.u,
+                     p.u_head_stride, p.C, p.cpad, p.dx, p.ubf, p.nu, p.bnd);
+  return hipGetLastError();
+}
+
+hipError_t prep_any(const KmProblem &p, hipStream_t s) {
+  switch (p.dxp) {
+    case 16: return prep<16>(p, s);
+    case 32: return prep<32>(p, s);
+    case 48: return prep<48>(p, s);
+    case 64: return prep<64>(p, s);
+    default: return prep<128>(p, s);
+  }
+}
+
 }  // namespace
+
+bool km_assign3_ok(const KmProblem (&p)[3]) {
+  int lds = 0, rows = 0;
+  for (int m = 0; m < 3; ++m) {
+    const KmProblem &q = p[m];
+    if (!q.mfma || q.x != p[0].x || q.ld != p[0].ld || q.n != p[0].n ||
+        q.heads != p[0].heads || q.x_head_stride != p[0].x_head_stride)
+      return false;
+    lds += q.cpad * (2 * q.dxp + 8);
+    rows += q.cpad;
+  }
+  if (lds > kUbfLds || rows > kMaxCpad) return false;
+  const int a = p[0].dxp, b = p[1].dxp, c = p[2].dxp;
+  return (a == 16 && b == 64 && c == 64) || (a == 48 && b == 48 && c == 48) ||
+         (a == 16 && b == 32 && c == 32);
+}
+
+size_t km_assign3_scratch_bytes() { return sizeof(Sub3); }
+
+hipError_t km_assign3(const KmProblem (&p)[3], void *scratch, hipStream_t s) {
+  for (int m = 0; m < 3; ++m) {
+    const hipError_t e = prep_any(p[m], s);
+    if (e != hipSuccess) return e;
+  }
+  Sub3 *args = static_cast<Sub3 *>(scratch);
+  const int a = p[0].dxp, b = p[1].dxp;
+  if (a == 16 && b == 64) return launch_mfma3<16, 64, 64>(p, args, s);
+  if (a == 48) return launch_mfma3<48, 48, 48>(p, args, s);
+  return launch_mfma3<16, 32, 32>(p, args, s);
+}
 
 int km_cpad(int C) { return (C + 31) / 32 * 32; }
 int km_dxp(int dx) { return dx <= 16 ? 16 : dx <= 32 ? 32 : dx <= 48 ? 48 : dx <= 64 ? 64 : 128; }
