@@ -18,19 +18,26 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "scope_oracle.c")
-LIB = os.path.join(HERE, "libscope_oracle.so")
+# SCOPE_ORACLE_LIBRARY selects another build (e.g. the sanitizer build)
+LIB = os.environ.get("SCOPE_ORACLE_LIBRARY") or os.path.join(HERE, "libscope_oracle.so")
+SAN_LIB = os.path.join(HERE, "libscope_oracle_san.so")
 
 CFLAGS = ["-O2", "-std=gnu11", "-ffp-contract=off", "-fno-fast-math",
           "-fopenmp", "-mfma", "-fPIC", "-shared"]
+SAN_FLAGS = ["-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+             "-fno-omit-frame-pointer", "-g"]
 
 
-def build(force: bool = True) -> str:
-    """Compile the oracle with gcc into oracle/libscope_oracle.so."""
-    if force or not os.path.exists(LIB):
-        tmp = LIB + ".tmp"
-        subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, SRC, "-lm"])
-        os.replace(tmp, LIB)
-    return LIB
+def build(force: bool = True, sanitize: bool = False) -> str:
+    """Compile the oracle with gcc into oracle/libscope_oracle.so, or with
+    sanitize into libscope_oracle_san.so under ASan and UBSan."""
+    out = SAN_LIB if sanitize else LIB
+    if force or not os.path.exists(out):
+        tmp = out + ".tmp"
+        flags = CFLAGS + (SAN_FLAGS if sanitize else [])
+        subprocess.check_call(["gcc", *flags, "-o", tmp, SRC, "-lm"])
+        os.replace(tmp, out)
+    return out
 
 
 _lib = None
@@ -69,6 +76,13 @@ def lib():
                                     P, P]
         L.oracle_attention.argtypes = [I, I, I, P, P, P, I, P, P, P, P,
                                        ctypes.c_double, P, P]
+        D = ctypes.c_double
+        L.oracle_block_proxy.argtypes = [I, I, I, P, P, I, D, P]
+        L.oracle_matched_retention.argtypes = [I, I, P, P, I, I, P, P]
+        L.oracle_recall_at_density.argtypes = [I, I, P, P, I, P]
+        for name in ("oracle_block_proxy", "oracle_matched_retention",
+                     "oracle_recall_at_density"):
+            getattr(L, name).restype = I
         for name in ("oracle_kmeans", "oracle_group", "oracle_assign_rows",
                      "oracle_mean_rows", "oracle_cluster_queries",
                      "oracle_cluster_key_subspaces", "oracle_tables",
@@ -363,3 +377,57 @@ def layer(q, k, v, ranges, c_q, c_m, iters, init_q, init_k, rho, k_fix,
     O = attention(q, k, v, qr["offsets"], qr["perm"], sel["sel_counts"],
                   sel["sel_idx"])
     return dict(q=qr, k=kr, tables=P, scores=S, sel=sel, out=O)
+
+
+# --- proxy comparison measurements (App. C, Fig. 9; Fig. 2) ---------------
+
+def block_proxy(qrep, k, block, scale):
+    """Block-wise proxy scores [rows][n]: each key scored by the mean of its
+    block of `block` consecutive tokens against the row's query
+    representative (qrep [rows][d]), times scale; fp64 arithmetic."""
+    qrep = _c(qrep, np.float32)
+    k = _c(k, np.float32)
+    rows, d = qrep.shape
+    n = k.shape[0]
+    out = np.empty((rows, n), np.float32)
+    _check(lib().oracle_block_proxy(rows, n, d, _p(qrep), _p(k), int(block), float(scale),
+                                    _p(out)), "block_proxy")
+    return out
+
+
+def _ceil_frac(x, m):
+    """ceil(x * m) for a decimal fraction x, in exact rationals."""
+    from fractions import Fraction
+    v = Fraction(str(x)) * m
+    return -(-v.numerator // v.denominator)
+
+
+def matched_retention(exact, proxy, top_frac=0.1, target=0.958):
+    """Per row: retained fraction and oracle recall when keys are taken in
+    proxy order until `target` of the exact top `top_frac` is held (whole
+    tie groups of the proxy kept); kt = ceil(top_frac n), need =
+    ceil(target kt)."""
+    exact = _c(exact, np.float32)
+    proxy = _c(proxy, np.float32)
+    rows, n = exact.shape
+    kt = max(1, _ceil_frac(top_frac, n))
+    need = max(1, _ceil_frac(target, kt))
+    ret = np.empty(rows, np.float64)
+    rec = np.empty(rows, np.float64)
+    _check(lib().oracle_matched_retention(rows, n, _p(exact), _p(proxy), kt, need, _p(ret),
+                                          _p(rec)), "matched_retention")
+    return ret, rec
+
+
+def recall_at_density(p_exact, proxy, density):
+    """Per row: exact attention mass held by the first max(1, round(density
+    n)) keys in proxy order."""
+    p = _c(p_exact, np.float64)
+    proxy = _c(proxy, np.float32)
+    rows, n = proxy.shape
+    count = max(1, int(round(density * n)))
+    out = np.empty(rows, np.float64)
+    _check(lib().oracle_recall_at_density(rows, n, _p(p), _p(proxy), count, _p(out)),
+           "recall_at_density")
+    return out
+

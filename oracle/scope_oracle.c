@@ -102,10 +102,21 @@ static float range_limit(int n) {
   return ldexpf(1.0f, 39 - L < 22 ? 39 - L : 22);
 }
 
-/* returns OR_ERR_RANGE if some |x| >= range_limit(n) or is not finite */
+/* rint(x * 2^24) as a two's complement 64-bit pattern.  Within the range
+ * the value is exact; outside it (flagged by the caller) a finite value
+ * still gives a defined pattern and a non-finite one gives 0.             */
+static uint64_t fixed24(float x) {
+  const double t = rint((double)x * 16777216.0);
+  if (!(fabs(t) < 9.0e18)) return 0;
+  return (uint64_t)(int64_t)t;
+}
+
+/* returns OR_ERR_RANGE if some |x| >= range_limit(n) or is not finite.  The
+ * sums wrap modulo 2^64 (unsigned), so out-of-range input yields some
+ * value, never undefined arithmetic; within the range no sum wraps.     */
 static int km_update(const float *X, long ldx, int n, int dx, const int *a,
                      int C, float *U, int *cnt) {
-  int64_t *S = (int64_t *)calloc((size_t)C * dx, sizeof(int64_t));
+  uint64_t *S = (uint64_t *)calloc((size_t)C * dx, sizeof(uint64_t));
   if (!S) return OR_ERR_MEM;
   int status = OR_OK;
   const float lim = range_limit(n);
@@ -116,14 +127,14 @@ static int km_update(const float *X, long ldx, int n, int dx, const int *a,
     cnt[r] += 1;
     for (int c = 0; c < dx; ++c) {
       if (!(fabsf(x[c]) < lim)) status = OR_ERR_RANGE;
-      S[(size_t)r * dx + c] += (int64_t)rintf(x[c] * 16777216.0f);
+      S[(size_t)r * dx + c] += fixed24(x[c]);
     }
   }
   for (int r = 0; r < C; ++r) {
     if (cnt[r] == 0) continue; /* empty cluster: keep previous centroid */
     double den = (double)cnt[r] * 16777216.0;
     for (int c = 0; c < dx; ++c)
-      U[(size_t)r * dx + c] = (float)((double)S[(size_t)r * dx + c] / den);
+      U[(size_t)r * dx + c] = (float)((double)(int64_t)S[(size_t)r * dx + c] / den);
   }
   free(S);
   return status;
@@ -602,4 +613,138 @@ int oracle_mean_rows(const float *X, long ldx, int n, int dx, const int *assign,
   for (int i = 0; i < n; ++i)
     if (assign[i] < 0 || assign[i] >= C) return OR_ERR_ARG;
   return km_update(X, ldx, n, dx, assign, C, U, counts);
+}
+
+/* ------------------------------------------------------------------------
+ * Proxy comparison measurements (App. C, Fig. 9: matched oracle recall;
+ * Fig. 2: attention recall against density).  They compare key-side
+ * proxies of the exact scores and are not part of the layer.  A proxy row
+ * scores every key for one query; keys are ranked by proxy descending, ties
+ * by ascending key index.                                                  */
+
+/* Block-wise proxy: the keys cut into blocks of `block` consecutive tokens
+ * (the last block may be shorter), each represented by the mean of its keys
+ * (fp64 sums divided by the block's size).  Row r scores key j by
+ * <qrep_r, mean of j's block> * scale, in fp64, stored as fp32.           */
+int oracle_block_proxy(int rows, int n, int d, const float *qrep, const float *k,
+                       int block, double scale, float *proxy) {
+  if (rows < 0 || n < 1 || d < 1 || block < 1) return OR_ERR_ARG;
+  const int nb = (n + block - 1) / block;
+  double *kbar = (double *)malloc(sizeof(double) * (size_t)nb * d);
+  if (!kbar) return OR_ERR_MEM;
+  for (int b = 0; b < nb; ++b) {
+    const int j0 = b * block, j1 = j0 + block < n ? j0 + block : n;
+    for (int c = 0; c < d; ++c) {
+      double s = 0.0;
+      for (int j = j0; j < j1; ++j) s += (double)k[(size_t)j * d + c];
+      kbar[(size_t)b * d + c] = s / (double)(j1 - j0);
+    }
+  }
+#pragma omp parallel for schedule(static)
+  for (int r = 0; r < rows; ++r) {
+    for (int b = 0; b < nb; ++b) {
+      double s = 0.0;
+      for (int c = 0; c < d; ++c) s += (double)qrep[(size_t)r * d + c] * kbar[(size_t)b * d + c];
+      const float v = (float)(s * scale);
+      const int j0 = b * block, j1 = j0 + block < n ? j0 + block : n;
+      for (int j = j0; j < j1; ++j) proxy[(size_t)r * n + j] = v;
+    }
+  }
+  free(kbar);
+  return OR_OK;
+}
+
+typedef struct {
+  float v;
+  int j;
+} ranked_t;
+
+static int cmp_ranked(const void *pa, const void *pb) {
+  const ranked_t *a = (const ranked_t *)pa, *b = (const ranked_t *)pb;
+  if (a->v > b->v) return -1;
+  if (a->v < b->v) return 1;
+  return (a->j > b->j) - (a->j < b->j);
+}
+
+/* keys of one row in ranked order: value descending, index ascending */
+static void rank_row(const float *row, int n, ranked_t *out) {
+  for (int j = 0; j < n; ++j) {
+    out[j].v = row[j] + 0.0f; /* -0 ranks with +0 */
+    out[j].j = j;
+  }
+  qsort(out, (size_t)n, sizeof(ranked_t), cmp_ranked);
+}
+
+/* Matched oracle recall, per row: the oracle set O is the first kt keys of
+ * the exact ranking; keys are taken in proxy order until `need` keys of O
+ * are held, and then every key whose proxy equals the last one taken (a
+ * block or a centroid is kept whole).  retention[r] = kept / n and
+ * recall[r] = |kept and O| / kt.                                          */
+int oracle_matched_retention(int rows, int n, const float *exact, const float *proxy,
+                             int kt, int need, double *retention, double *recall) {
+  if (rows < 0 || n < 1 || kt < 1 || kt > n || need < 1 || need > kt) return OR_ERR_ARG;
+  int status = OR_OK;
+#pragma omp parallel
+  {
+    ranked_t *re = (ranked_t *)malloc(sizeof(ranked_t) * (size_t)n);
+    ranked_t *rp = (ranked_t *)malloc(sizeof(ranked_t) * (size_t)n);
+    char *in_o = (char *)malloc((size_t)n);
+    if (!re || !rp || !in_o) {
+#pragma omp atomic write
+      status = OR_ERR_MEM;
+    } else {
+#pragma omp for schedule(dynamic)
+      for (int r = 0; r < rows; ++r) {
+        rank_row(exact + (size_t)r * n, n, re);
+        memset(in_o, 0, (size_t)n);
+        for (int i = 0; i < kt; ++i) in_o[re[i].j] = 1;
+        rank_row(proxy + (size_t)r * n, n, rp);
+        int hits = 0, pos = 0;
+        for (; pos < n; ++pos) {
+          hits += in_o[rp[pos].j];
+          if (hits >= need) break;
+        }
+        const float s_star = rp[pos].v;
+        long kept = 0, kept_o = 0;
+        for (int j = 0; j < n; ++j) {
+          if (proxy[(size_t)r * n + j] + 0.0f >= s_star) {
+            ++kept;
+            kept_o += in_o[j];
+          }
+        }
+        retention[r] = (double)kept / (double)n;
+        recall[r] = (double)kept_o / (double)kt;
+      }
+    }
+    free(re);
+    free(rp);
+    free(in_o);
+  }
+  return status;
+}
+
+/* Attention recall at a density: per row, the sum (fp64) of the exact
+ * attention weights p of the first `count` keys in proxy order.          */
+int oracle_recall_at_density(int rows, int n, const double *p, const float *proxy,
+                             int count, double *mass) {
+  if (rows < 0 || n < 1 || count < 1 || count > n) return OR_ERR_ARG;
+  int status = OR_OK;
+#pragma omp parallel
+  {
+    ranked_t *rp = (ranked_t *)malloc(sizeof(ranked_t) * (size_t)n);
+    if (!rp) {
+#pragma omp atomic write
+      status = OR_ERR_MEM;
+    } else {
+#pragma omp for schedule(dynamic)
+      for (int r = 0; r < rows; ++r) {
+        rank_row(proxy + (size_t)r * n, n, rp);
+        double s = 0.0;
+        for (int i = 0; i < count; ++i) s += p[(size_t)r * n + rp[i].j];
+        mass[r] = s;
+      }
+    }
+    free(rp);
+  }
+  return status;
 }

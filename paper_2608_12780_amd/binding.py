@@ -15,7 +15,8 @@ import os
 import torch
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libscope.so")
+# SCOPE_LIBRARY selects another build of the library (e.g. libscope_san.so)
+LIB_PATH = os.environ.get("SCOPE_LIBRARY") or os.path.join(PKG, "libscope.so")
 
 F32, BF16 = 0, 1
 ENTRY_POINTS = (
