@@ -393,9 +393,11 @@ def matched_retention(exact, proxy, top_frac=0.1, target=0.958):
     time, until `target` of the oracle set is held.  Returns the retained
     fraction of all keys and the oracle recall reached, per row."""
     import torch
+    from fractions import Fraction
     Q, N = exact.shape
-    kt = math.ceil(top_frac * N)
-    need = math.ceil(target * kt)
+    ceil = lambda f: -((-f.numerator) // f.denominator)
+    kt = max(1, ceil(Fraction(str(top_frac)) * N))
+    need = max(1, ceil(Fraction(str(target)) * kt))
     order_e = torch.argsort(exact, dim=1, descending=True, stable=True)
     oracle = torch.zeros(exact.shape, dtype=torch.bool, device=exact.device)
     oracle.scatter_(1, order_e[:, :kt], True)
@@ -418,43 +420,44 @@ def recall_at_density(p_exact, proxy, density):
     return torch.gather(p_exact, 1, top).sum(1)
 
 
-def recall_study(config_name="hy720", heads=4, c_q=300, c_m=333, block=64, sample=256,
-                 densities=(0.05, 0.1, 0.2, 0.3, 0.5)):
-    """Matched-recall retention (App. C, Fig. 9) and attention recall against
-    density (Fig. 2) of three key-side proxies that all score a query by its
-    cluster centroid: SCOPE's subspace lookup sum (RoPE t/h/w, C_m per
-    subspace), full-dimensional key clusters (C_m centroids) and block means
-    of `block` consecutive tokens.  Exact scores of sampled queries come
-    from their own rows of Q K^T."""
+def recall_study_rows(cfg, heads, c_q, c_m, block, sample, dev=None):
+    """The three key-side proxies of the matched-recall study on the first
+    `heads` heads of workload cfg, each scoring a query by its cluster
+    centroid: SCOPE's subspace lookup sum (RoPE t/h/w ranges, c_m centroids
+    per subspace), full-dimensional key clusters (c_m centroids; the one-set
+    partition) and block means of `block` consecutive tokens.  Per head
+    yields the sampled query rows and their exact scores, exact attention
+    weights and proxy rows (torch tensors on the GPU)."""
     import torch
     from paper_2608_12780_amd import inputs
     from paper_2608_12780_amd.layer import ScopeLayer, ScopePartitionLayer
-    cfg = inputs.CONFIGS[config_name].with_(c_q=c_q, c_m=c_m)
+    cfg = cfg.with_(c_q=c_q, c_m=c_m)
     x = inputs.generate(cfg.with_(heads=heads))
-    dev = torch.device("cuda", 0)
-    up = lambda b: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
-    q, k, v = up(x.q_bits), up(x.k_bits), up(x.v_bits)
+    dev = dev or torch.device("cuda", 0)
+    if cfg.dtype == "bf16":
+        up = lambda b: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
+        q, k = up(x.q_bits), up(x.k_bits)
+    else:
+        q, k = torch.from_numpy(x.q).to(dev), torch.from_numpy(x.k).to(dev)
     iq = torch.from_numpy(x.init_q).to(dev)
     sig = 1.0 / math.sqrt(cfg.d)
-    # SCOPE proxy (materialised logits of the three-range calls)
+    init3 = inputs.partition_init(cfg, 3, c_m, heads)
+    init1 = inputs.partition_init(cfg, 1, c_m, heads)
     scope = ScopeLayer(heads, cfg.n, cfg.d, cfg.ranges, c_q, (c_m,) * 3, cfg.iters,
                        cfg.rho, cfg.k_fix, dtype=cfg.dtype, device=dev,
                        materialize_scores=True)
     scope.cluster_queries(q, iq)
-    scope.cluster_keys(k, torch.from_numpy(inputs.partition_init(cfg, 3, c_m, heads)).to(dev))
+    scope.cluster_keys(k, torch.from_numpy(init3).to(dev))
     scope.proxy_scores()
-    # full-dimensional key clusters: the one-set partition
     full = ScopePartitionLayer(heads, cfg.n, cfg.d, inputs.partition_sets(cfg, "1"), c_q,
                                (c_m,), cfg.iters, cfg.rho, cfg.k_fix, dtype=cfg.dtype,
                                device=dev, materialize_scores=True)
     full.cluster_queries(q, iq)
-    full.cluster_keys(k, torch.from_numpy(inputs.partition_init(cfg, 1, c_m, heads)).to(dev))
+    full.cluster_keys(k, torch.from_numpy(init1).to(dev))
     full.proxy_scores()
     torch.cuda.synchronize()
     assert torch.equal(scope.assign, full.assign)   # same query clusters
     rng = np.random.default_rng(cfg.seed + 7)
-    rows = {"scope_subspaces": [], "full_dim_clusters": [], "blocks": []}
-    dens = {name: {str(dd): [] for dd in densities} for name in rows}
     nb = (cfg.n + block - 1) // block
     for h in range(heads):
         kf = k[h].float()
@@ -465,16 +468,33 @@ def recall_study(config_name="hy720", heads=4, c_q=300, c_m=333, block=64, sampl
         qi = torch.from_numpy(rng.choice(cfg.n, sample, replace=False)).to(dev)
         c_ = scope.assign[h, qi].long()
         exact = (q[h, qi].float() @ kf.T) * sig
-        p_exact = torch.softmax(exact, dim=1)
         qbar = scope.q_centroids[h, c_]
-        prox = {"scope_subspaces": scope.scores[h, c_],
-                "full_dim_clusters": full.scores[h, c_],
-                "blocks": ((qbar @ kbar.T) * sig).repeat_interleave(block, dim=1)[:, :cfg.n]}
-        for name, pr in prox.items():
-            ret, rec = matched_retention(exact, pr)
+        yield dict(head=h, x=x, init3=init3, init1=init1, qi=qi, clusters=c_, exact=exact,
+                   p_exact=torch.softmax(exact, dim=1), qbar=qbar,
+                   proxies={"scope_subspaces": scope.scores[h, c_],
+                            "full_dim_clusters": full.scores[h, c_],
+                            "blocks": ((qbar @ kbar.T) * sig).repeat_interleave(block, dim=1)[:, :cfg.n]})
+
+
+def recall_study(config_name="hy720", heads=4, c_q=300, c_m=333, block=64, sample=256,
+                 densities=(0.05, 0.1, 0.2, 0.3, 0.5)):
+    """Matched-recall retention (App. C, Fig. 9) and attention recall against
+    density (Fig. 2) of three key-side proxies that all score a query by its
+    cluster centroid: SCOPE's subspace lookup sum (RoPE t/h/w, C_m per
+    subspace), full-dimensional key clusters (C_m centroids) and block means
+    of `block` consecutive tokens.  Exact scores of sampled queries come
+    from their own rows of Q K^T."""
+    import torch
+    from paper_2608_12780_amd import inputs
+    cfg = inputs.CONFIGS[config_name]
+    rows = {"scope_subspaces": [], "full_dim_clusters": [], "blocks": []}
+    dens = {name: {str(dd): [] for dd in densities} for name in rows}
+    for hd in recall_study_rows(cfg, heads, c_q, c_m, block, sample):
+        for name, pr in hd["proxies"].items():
+            ret, rec = matched_retention(hd["exact"], pr)
             rows[name].append(torch.stack([ret, rec], 1))
             for dd in densities:
-                dens[name][str(dd)].append(recall_at_density(p_exact, pr, dd))
+                dens[name][str(dd)].append(recall_at_density(hd["p_exact"], pr, dd))
     out = []
     for name in rows:
         r = torch.cat(rows[name])
