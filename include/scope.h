@@ -155,6 +155,30 @@ int32_t scope_cluster_key_subspaces(const scope_shape *shape, const void *k,
                                     size_t ws_bytes, int32_t *dev_status,
                                     void *stream);
 
+/* 1w, 2w. Warm starts across denoising steps (Sec. 4 setup: SCOPE runs at
+ * every step after a dense prefix, and the query and key distributions of
+ * one head change little from step to step).  As calls 1 and 2, but Lloyd's
+ * iterations start from the centroids already in q_centroids (call 1w) or
+ * k_centroids (call 2w), e.g. the previous step's results, instead of the
+ * rows init_idx; those buffers are read, then overwritten with the result.
+ * Arguments, layouts, outputs and errors otherwise as calls 1 and 2 (no
+ * init_idx; the starting centroids must be finite).  With the centroids a
+ * call returned, iters more iterations from them give exactly what a
+ * single call with the total iteration count gives.                      */
+int32_t scope_cluster_queries_warm(const scope_shape *shape, const void *q,
+                                   int32_t c_q, int32_t iters,
+                                   float *q_centroids, int32_t *assign,
+                                   int32_t *counts, int32_t *offsets,
+                                   int32_t *perm, void *workspace,
+                                   size_t ws_bytes, int32_t *dev_status,
+                                   void *stream);
+int32_t scope_cluster_key_subspaces_warm(const scope_shape *shape,
+                                         const void *k, const int32_t c_m[3],
+                                         int32_t iters, float *k_centroids,
+                                         uint32_t *codes, void *workspace,
+                                         size_t ws_bytes, int32_t *dev_status,
+                                         void *stream);
+
 /* 3. Score tables and proxy logits (Eq. 5-6; Alg. 2 scoring steps).
  * tables [heads][c_q][C_T+C_H+C_W]: P_m[c][r] = <qbar_c[I_m], u_r^m> as an
  * fp32 fma chain over the subspace channels in ascending order, columns

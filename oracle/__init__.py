@@ -76,6 +76,12 @@ def lib():
                                     P, P]
         L.oracle_attention.argtypes = [I, I, I, P, P, P, I, P, P, P, P,
                                        ctypes.c_double, P, P]
+        L.oracle_cluster_queries_from.argtypes = [I, I, I, P, I, I, P, P, P, P, P]
+        L.oracle_cluster_key_subspaces_from.argtypes = [I, I, I, P, P, P, P, I, P, P, P]
+        L.oracle_kmeans_from.argtypes = [P, ctypes.c_long, I, I, I, I, I, P, P, P]
+        for name in ("oracle_cluster_queries_from", "oracle_cluster_key_subspaces_from",
+                     "oracle_kmeans_from"):
+            getattr(L, name).restype = I
         D = ctypes.c_double
         L.oracle_block_proxy.argtypes = [I, I, I, P, P, I, D, P]
         L.oracle_matched_retention.argtypes = [I, I, P, P, I, I, P, P]
@@ -177,6 +183,38 @@ def cluster_queries(q, c_q, iters, init):
     _check(st, "cluster_queries")
     return dict(centroids=cen, assign=g, counts=cnt, offsets=off, perm=perm,
                 status=st)
+
+
+def cluster_queries_from(q, c_q, iters, centroids):
+    """Query clustering warm-started from the given centroids [heads][c_q][d]."""
+    q = _c(q, np.float32)
+    heads, n, d = q.shape
+    cen = np.array(centroids, dtype=np.float32, copy=True).reshape(heads, c_q, d)
+    g = np.empty((heads, n), np.int32)
+    cnt = np.empty((heads, c_q), np.int32)
+    off = np.empty((heads, c_q + 1), np.int32)
+    perm = np.empty((heads, n), np.int32)
+    st = lib().oracle_cluster_queries_from(heads, n, d, _p(q), c_q, iters, _p(cen), _p(g),
+                                           _p(cnt), _p(off), _p(perm))
+    _check(st, "cluster_queries_from")
+    return dict(centroids=cen, assign=g, counts=cnt, offsets=off, perm=perm, status=st)
+
+
+def cluster_key_subspaces_from(k, ranges, c_m, iters, centroids):
+    """Key subspace clustering warm-started from the given codebooks
+    [heads][sum_m c_m len_m] (U^T, U^H, U^W back to back)."""
+    k = _c(k, np.float32)
+    heads, n, d = k.shape
+    off = _c(ranges[0], np.int32)
+    ln = _c(ranges[1], np.int32)
+    cm = _c(c_m, np.int32)
+    cen = np.array(centroids, dtype=np.float32, copy=True).reshape(heads, -1)
+    codes = np.empty((heads, n), np.uint32)
+    a3 = np.empty((heads, 3, n), np.int32)
+    st = lib().oracle_cluster_key_subspaces_from(heads, n, d, _p(off), _p(ln), _p(k), _p(cm),
+                                                 iters, _p(cen), _p(codes), _p(a3))
+    _check(st, "cluster_key_subspaces_from")
+    return dict(centroids=cen, codes=codes, assign3=a3, status=st)
 
 
 def cluster_key_subspaces(k, ranges, c_m, iters, init):

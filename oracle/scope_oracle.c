@@ -140,14 +140,10 @@ static int km_update(const float *X, long ldx, int n, int dx, const int *a,
   return status;
 }
 
-int oracle_kmeans(const float *X, long ldx, int n, int dx, int C, int iters,
-                  const int *init, int final_assign, float *U, int *assign,
-                  int *counts) {
+/* Lloyd's iterations from the centroids in U (in/out). */
+int oracle_kmeans_from(const float *X, long ldx, int n, int dx, int C, int iters,
+                       int final_assign, float *U, int *assign, int *counts) {
   if (n < 1 || dx < 1 || C < 1 || C > n || iters < 0) return OR_ERR_ARG;
-  for (int r = 0; r < C; ++r) {
-    if (init[r] < 0 || init[r] >= n) return OR_ERR_ARG;
-    memcpy(U + (size_t)r * dx, X + (size_t)init[r] * ldx, sizeof(float) * (size_t)dx);
-  }
   int status = OR_OK;
   for (int r = 0; r < C; ++r) counts[r] = 0;
   for (int it = 0; it < iters; ++it) {
@@ -162,6 +158,18 @@ int oracle_kmeans(const float *X, long ldx, int n, int dx, int C, int iters,
     for (int i = 0; i < n; ++i) counts[assign[i]] += 1;
   }
   return status;
+}
+
+/* Lloyd's k-means from the rows init[0..C) of X. */
+int oracle_kmeans(const float *X, long ldx, int n, int dx, int C, int iters,
+                  const int *init, int final_assign, float *U, int *assign,
+                  int *counts) {
+  if (n < 1 || dx < 1 || C < 1 || C > n || iters < 0) return OR_ERR_ARG;
+  for (int r = 0; r < C; ++r) {
+    if (init[r] < 0 || init[r] >= n) return OR_ERR_ARG;
+    memcpy(U + (size_t)r * dx, X + (size_t)init[r] * ldx, sizeof(float) * (size_t)dx);
+  }
+  return oracle_kmeans_from(X, ldx, n, dx, C, iters, final_assign, U, assign, counts);
 }
 
 /* Grouping of queries by cluster (the cluster-based query permutation of
@@ -184,15 +192,18 @@ int oracle_group(const int *assign, int n, int C, int *counts, int *offsets,
 }
 
 /* Alg. 1, first steps: (Qbar, g) <- KMeans(Q, C_q); Q_c, n_c.               */
-int oracle_cluster_queries(int heads, int n, int d, const float *q, int c_q,
+/* init == NULL: warm start from the centroids already in `centroids` */
+static int cluster_queries(int heads, int n, int d, const float *q, int c_q,
                            int iters, const int *init, float *centroids,
                            int *assign, int *counts, int *offsets, int *perm) {
   int status = OR_OK;
   for (int h = 0; h < heads; ++h) {
-    int s = oracle_kmeans(q + (size_t)h * n * d, d, n, d, c_q, iters,
-                          init + (size_t)h * c_q, 0,
-                          centroids + (size_t)h * c_q * d,
-                          assign + (size_t)h * n, counts + (size_t)h * c_q);
+    float *U = centroids + (size_t)h * c_q * d;
+    int s = init ? oracle_kmeans(q + (size_t)h * n * d, d, n, d, c_q, iters,
+                                 init + (size_t)h * c_q, 0, U,
+                                 assign + (size_t)h * n, counts + (size_t)h * c_q)
+                 : oracle_kmeans_from(q + (size_t)h * n * d, d, n, d, c_q, iters, 0, U,
+                                      assign + (size_t)h * n, counts + (size_t)h * c_q);
     if (s == OR_ERR_ARG || s == OR_ERR_MEM) return s;
     if (s != OR_OK) status = s;
     s = oracle_group(assign + (size_t)h * n, n, c_q, counts + (size_t)h * c_q,
@@ -206,7 +217,25 @@ int oracle_cluster_queries(int heads, int n, int d, const float *q, int c_q,
  * and the composite code z_j = (z_j^T, z_j^H, z_j^W) of Eq. 4, packed as
  * zT | zH << 10 | zW << 20.  Centroids per head: U^T, U^H, U^W back to back,
  * each [C_m][d_m].  init: [heads][3][init_stride].                          */
-int oracle_cluster_key_subspaces(int heads, int n, int d, const int *off,
+int oracle_cluster_queries(int heads, int n, int d, const float *q, int c_q,
+                           int iters, const int *init, float *centroids,
+                           int *assign, int *counts, int *offsets, int *perm) {
+  if (!init) return OR_ERR_ARG;
+  return cluster_queries(heads, n, d, q, c_q, iters, init, centroids, assign, counts,
+                         offsets, perm);
+}
+
+/* Query clustering from the centroids in `centroids` (in/out): a warm
+ * start, e.g. from the previous denoising step's result. */
+int oracle_cluster_queries_from(int heads, int n, int d, const float *q, int c_q,
+                                int iters, float *centroids, int *assign, int *counts,
+                                int *offsets, int *perm) {
+  return cluster_queries(heads, n, d, q, c_q, iters, NULL, centroids, assign, counts,
+                         offsets, perm);
+}
+
+/* init == NULL: warm start from the codebooks already in `centroids` */
+static int cluster_key_subspaces(int heads, int n, int d, const int *off,
                                  const int *len, const float *k,
                                  const int *c_m, int iters, const int *init,
                                  int init_stride, float *centroids,
@@ -223,9 +252,10 @@ int oracle_cluster_key_subspaces(int heads, int n, int d, const int *off,
     float *U = centroids + (size_t)h * per_head;
     for (int m = 0; m < 3; ++m) {
       int *a = assign3 + ((size_t)h * 3 + m) * n;
-      int s = oracle_kmeans(k + (size_t)h * n * d + off[m], d, n, len[m], c_m[m],
-                            iters, init + ((size_t)h * 3 + m) * init_stride, 1,
-                            U, a, cnt);
+      const float *X = k + (size_t)h * n * d + off[m];
+      int s = init ? oracle_kmeans(X, d, n, len[m], c_m[m], iters,
+                                   init + ((size_t)h * 3 + m) * init_stride, 1, U, a, cnt)
+                   : oracle_kmeans_from(X, d, n, len[m], c_m[m], iters, 1, U, a, cnt);
       if (s == OR_ERR_ARG || s == OR_ERR_MEM) { free(cnt); return s; }
       if (s != OR_OK) status = s;
       U += (size_t)c_m[m] * len[m];
@@ -239,6 +269,25 @@ int oracle_cluster_key_subspaces(int heads, int n, int d, const int *off,
   }
   free(cnt);
   return status;
+}
+
+int oracle_cluster_key_subspaces(int heads, int n, int d, const int *off,
+                                 const int *len, const float *k,
+                                 const int *c_m, int iters, const int *init,
+                                 int init_stride, float *centroids,
+                                 uint32_t *codes, int *assign3) {
+  if (!init) return OR_ERR_ARG;
+  return cluster_key_subspaces(heads, n, d, off, len, k, c_m, iters, init, init_stride,
+                               centroids, codes, assign3);
+}
+
+/* Key subspace clustering from the codebooks in `centroids` (in/out). */
+int oracle_cluster_key_subspaces_from(int heads, int n, int d, const int *off,
+                                      const int *len, const float *k, const int *c_m,
+                                      int iters, float *centroids, uint32_t *codes,
+                                      int *assign3) {
+  return cluster_key_subspaces(heads, n, d, off, len, k, c_m, iters, NULL, 0, centroids,
+                               codes, assign3);
 }
 
 /* Eq. 5: P_m[c, r] = <qbar_c^m, u_r^m>, the query-centroid slice on I_m

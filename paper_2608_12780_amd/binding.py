@@ -27,6 +27,7 @@ ENTRY_POINTS = (
     "scope_partition_workspace_size", "scope_cluster_key_partition",
     "scope_proxy_scores_partition", "scope_select_partition",
     "scope_sparse_attention_noalloc", "scope_debug_copy", "scope_debug_mfma_loop",
+    "scope_cluster_queries_warm", "scope_cluster_key_subspaces_warm",
 )
 MAX_SUBSPACES, MAX_D = 8, 128
 POLICIES = {"online": 0, "fixed": 1, "topp": 2}
@@ -97,6 +98,8 @@ def lib() -> ctypes.CDLL:
         L.scope_workspace_size.argtypes = [SP, I, P, ctypes.POINTER(Z)]
         L.scope_cluster_queries.argtypes = [SP, P, I, I, P, P, P, P, P, P, P, Z, P, P]
         L.scope_cluster_key_subspaces.argtypes = [SP, P, P, I, P, I, P, P, P, Z, P, P]
+        L.scope_cluster_queries_warm.argtypes = [SP, P, I, I, P, P, P, P, P, P, Z, P, P]
+        L.scope_cluster_key_subspaces_warm.argtypes = [SP, P, P, I, P, P, P, Z, P, P]
         L.scope_proxy_scores.argtypes = [SP, P, I, P, P, P, P, P, P]
         L.scope_select.argtypes = [SP, I, P, P, P, P, P, ctypes.c_float, I, P, P,
                                    P, P, P, P, Z, P]
@@ -187,6 +190,38 @@ def scope_cluster_queries(shape, q, c_q, iters, init_idx, q_centroids, assign,
         _ptr(counts, torch.int32, H * c_q, "counts"),
         _ptr(offsets, torch.int32, H * (c_q + 1), "offsets"),
         _ptr(perm, torch.int32, H * N, "perm"),
+        _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(),
+        _ptr(dev_status, torch.int32, 1, "dev_status", optional=True),
+        _stream(stream)))
+
+
+def scope_cluster_queries_warm(shape, q, c_q, iters, q_centroids, assign, counts, offsets,
+                               perm, workspace, dev_status=None, stream=None):
+    """Call 1w: q_centroids holds the starting centroids and receives the result."""
+    H, N, D = shape.heads, shape.n, shape.d
+    _check("scope_cluster_queries_warm", lib().scope_cluster_queries_warm(
+        ctypes.byref(shape), _ptr(q, _data_dtype(shape), H * N * D, "q"),
+        int(c_q), int(iters),
+        _ptr(q_centroids, torch.float32, H * c_q * D, "q_centroids"),
+        _ptr(assign, torch.int32, H * N, "assign"),
+        _ptr(counts, torch.int32, H * c_q, "counts"),
+        _ptr(offsets, torch.int32, H * (c_q + 1), "offsets"),
+        _ptr(perm, torch.int32, H * N, "perm"),
+        _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(),
+        _ptr(dev_status, torch.int32, 1, "dev_status", optional=True),
+        _stream(stream)))
+
+
+def scope_cluster_key_subspaces_warm(shape, k, c_m, iters, k_centroids, codes, workspace,
+                                     dev_status=None, stream=None):
+    """Call 2w: k_centroids holds the starting codebooks and receives the result."""
+    H, N, D = shape.heads, shape.n, shape.d
+    per_head = sum(int(c_m[m]) * shape.range_len[m] for m in range(3))
+    _check("scope_cluster_key_subspaces_warm", lib().scope_cluster_key_subspaces_warm(
+        ctypes.byref(shape), _ptr(k, _data_dtype(shape), H * N * D, "k"),
+        _cm(c_m), int(iters),
+        _ptr(k_centroids, torch.float32, H * per_head, "k_centroids"),
+        _ptr(codes, torch.int32, H * N, "codes"),
         _ptr(workspace, torch.uint8, None, "workspace"), workspace.numel(),
         _ptr(dev_status, torch.int32, 1, "dev_status", optional=True),
         _stream(stream)))

@@ -358,13 +358,16 @@ int32_t scope_workspace_size(const scope_shape *shape, int32_t c_q,
   return SCOPE_OK;
 }
 
-int32_t scope_cluster_queries(const scope_shape *shape, const void *q,
-                              int32_t c_q, int32_t iters,
-                              const int32_t *init_idx, float *q_centroids,
-                              int32_t *assign, int32_t *counts,
-                              int32_t *offsets, int32_t *perm, void *workspace,
-                              size_t ws_bytes, int32_t *dev_status,
-                              void *stream) {
+}  // extern "C"
+
+namespace {
+
+// Query clustering; `warm` starts from the centroids already in q_centroids
+// instead of the rows init_idx.
+int32_t cluster_queries(const scope_shape *shape, const void *q, int32_t c_q, int32_t iters,
+                        const int32_t *init_idx, bool warm, float *q_centroids,
+                        int32_t *assign, int32_t *counts, int32_t *offsets, int32_t *perm,
+                        void *workspace, size_t ws_bytes, int32_t *dev_status, void *stream) {
   int32_t st = check_shape(shape);
   if (st) return st;
   if ((st = check_cq(shape, c_q))) return st;
@@ -406,7 +409,7 @@ int32_t scope_cluster_queries(const scope_shape *shape, const void *q,
   p.bnd = w.bnd;
   set_split(p, w.split);
   const scope::AccPlan plan = query_plan(shape, c_q);
-  SCOPE_TRY(scope::km_init(p, init_idx, c_q, dev_status, s));
+  if (!warm) SCOPE_TRY(scope::km_init(p, init_idx, c_q, dev_status, s));
   // the returned grouping is that of the last assignment, taken before the
   // last update
   for (int it = 0; it < iters; ++it) {
@@ -421,13 +424,12 @@ int32_t scope_cluster_queries(const scope_shape *shape, const void *q,
   return SCOPE_OK;
 }
 
-int32_t scope_cluster_key_subspaces(const scope_shape *shape, const void *k,
-                                    const int32_t c_m[3], int32_t iters,
-                                    const int32_t *init_idx,
-                                    int32_t init_stride, float *k_centroids,
-                                    uint32_t *codes, void *workspace,
-                                    size_t ws_bytes, int32_t *dev_status,
-                                    void *stream) {
+// Key subspace clustering; `warm` starts from the codebooks already in
+// k_centroids instead of the rows init_idx.
+int32_t cluster_key_subspaces(const scope_shape *shape, const void *k, const int32_t c_m[3],
+                              int32_t iters, const int32_t *init_idx, int32_t init_stride,
+                              bool warm, float *k_centroids, uint32_t *codes, void *workspace,
+                              size_t ws_bytes, int32_t *dev_status, void *stream) {
   int32_t st = check_shape(shape);
   if (st) return st;
   if ((st = check_cm(shape, c_m))) return st;
@@ -476,7 +478,7 @@ int32_t scope_cluster_key_subspaces(const scope_shape *shape, const void *k,
     ucol += static_cast<size_t>(c_m[m]) * pm.dx;
     const int32_t *init = init_idx ? init_idx + static_cast<size_t>(m) * init_stride : nullptr;
     // init rows of head h, subspace m live at init_idx[(h*3 + m)*init_stride]
-    SCOPE_TRY(scope::km_init(pm, init, 3 * init_stride, dev_status, s));
+    if (!warm) SCOPE_TRY(scope::km_init(pm, init, 3 * init_stride, dev_status, s));
   }
   const scope::AccPlan plan = key_plan(shape, c_m);
   // the three assignments in one pass over K when the codebooks fit the LDS
@@ -500,6 +502,46 @@ int32_t scope_cluster_key_subspaces(const scope_shape *shape, const void *k,
   SCOPE_TRY(scope::km_pack_codes(w.assign3, static_cast<size_t>(3) * n, n, n,
                                  shape->heads, codes, s));
   return SCOPE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t scope_cluster_queries(const scope_shape *shape, const void *q, int32_t c_q,
+                              int32_t iters, const int32_t *init_idx, float *q_centroids,
+                              int32_t *assign, int32_t *counts, int32_t *offsets,
+                              int32_t *perm, void *workspace, size_t ws_bytes,
+                              int32_t *dev_status, void *stream) {
+  return cluster_queries(shape, q, c_q, iters, init_idx, false, q_centroids, assign, counts,
+                         offsets, perm, workspace, ws_bytes, dev_status, stream);
+}
+
+int32_t scope_cluster_queries_warm(const scope_shape *shape, const void *q, int32_t c_q,
+                                   int32_t iters, float *q_centroids, int32_t *assign,
+                                   int32_t *counts, int32_t *offsets, int32_t *perm,
+                                   void *workspace, size_t ws_bytes, int32_t *dev_status,
+                                   void *stream) {
+  return cluster_queries(shape, q, c_q, iters, nullptr, true, q_centroids, assign, counts,
+                         offsets, perm, workspace, ws_bytes, dev_status, stream);
+}
+
+int32_t scope_cluster_key_subspaces(const scope_shape *shape, const void *k,
+                                    const int32_t c_m[3], int32_t iters,
+                                    const int32_t *init_idx, int32_t init_stride,
+                                    float *k_centroids, uint32_t *codes, void *workspace,
+                                    size_t ws_bytes, int32_t *dev_status, void *stream) {
+  return cluster_key_subspaces(shape, k, c_m, iters, init_idx, init_stride, false, k_centroids,
+                               codes, workspace, ws_bytes, dev_status, stream);
+}
+
+int32_t scope_cluster_key_subspaces_warm(const scope_shape *shape, const void *k,
+                                         const int32_t c_m[3], int32_t iters,
+                                         float *k_centroids, uint32_t *codes,
+                                         void *workspace, size_t ws_bytes,
+                                         int32_t *dev_status, void *stream) {
+  return cluster_key_subspaces(shape, k, c_m, iters, nullptr, 0, true, k_centroids, codes,
+                               workspace, ws_bytes, dev_status, stream);
 }
 
 int32_t scope_proxy_scores(const scope_shape *shape, const float *q_centroids,

@@ -49,15 +49,28 @@ class ScopeLayer:
         self.status = torch.zeros(1, **i32)
 
     # the five stages -------------------------------------------------------
-    def cluster_queries(self, q, init_q=None, stream=None):
-        B.scope_cluster_queries(self.shape, q, self.c_q, self.iters, init_q,
+    def cluster_queries(self, q, init_q=None, stream=None, warm=False, iters=None):
+        """warm: start from the centroids this layer holds (calls 1w)."""
+        it = self.iters if iters is None else int(iters)
+        if warm:
+            B.scope_cluster_queries_warm(self.shape, q, self.c_q, it, self.q_centroids,
+                                         self.assign, self.counts, self.offsets, self.perm,
+                                         self.workspace, self.status, stream)
+            return
+        B.scope_cluster_queries(self.shape, q, self.c_q, it, init_q,
                                 self.q_centroids, self.assign, self.counts,
                                 self.offsets, self.perm, self.workspace,
                                 self.status, stream)
 
-    def cluster_keys(self, k, init_k=None, stream=None):
+    def cluster_keys(self, k, init_k=None, stream=None, warm=False, iters=None):
+        """warm: start from the codebooks this layer holds (call 2w)."""
+        it = self.iters if iters is None else int(iters)
+        if warm:
+            B.scope_cluster_key_subspaces_warm(self.shape, k, self.c_m, it, self.k_centroids,
+                                               self.codes, self.workspace, self.status, stream)
+            return
         stride = init_k.shape[-1] if init_k is not None else 0
-        B.scope_cluster_key_subspaces(self.shape, k, self.c_m, self.iters,
+        B.scope_cluster_key_subspaces(self.shape, k, self.c_m, it,
                                       init_k, stride, self.k_centroids,
                                       self.codes, self.workspace, self.status,
                                       stream)
@@ -87,11 +100,13 @@ class ScopeLayer:
                                  scale, self.out, self.workspace, stream)
 
     def forward(self, q, k, v, init_q=None, init_k=None, stream=None,
-                marks=None):
+                marks=None, warm=False, warm_iters=None):
         """Runs the layer; `marks(i)` (if given) is called before stage i and
-        after the last one, e.g. to record timing events."""
-        steps = (lambda: self.cluster_queries(q, init_q, stream),
-                 lambda: self.cluster_keys(k, init_k, stream),
+        after the last one, e.g. to record timing events.  warm: the
+        clusterings start from the centroids the layer holds (the previous
+        denoising step's), with warm_iters iterations (default: iters)."""
+        steps = (lambda: self.cluster_queries(q, init_q, stream, warm, warm_iters),
+                 lambda: self.cluster_keys(k, init_k, stream, warm, warm_iters),
                  lambda: self.proxy_scores(stream),
                  lambda: self.select(stream),
                  lambda: self.attend(q, k, v, 0.0, stream))
@@ -102,6 +117,31 @@ class ScopeLayer:
         if marks:
             marks(len(steps))
         return self.out
+
+
+class SparsitySchedule:
+    """Where the layer runs across a DiT's layers and denoising steps (Sec. 4
+    setup): the first attention layer stays dense at every step, and the
+    other layers stay dense during the first `dense_fraction` of the steps
+    (20% for the Wan models, 10% for HunyuanVideo), SCOPE afterwards.  The
+    first SCOPE step of a layer clusters from seeded rows; later steps may
+    warm-start from the previous step's centroids."""
+
+    def __init__(self, steps, dense_fraction, dense_layers=(0,)):
+        self.steps = int(steps)
+        self.dense_fraction = float(dense_fraction)
+        self.dense_layers = frozenset(int(x) for x in dense_layers)
+        # the dense prefix in whole steps, ceil(fraction * steps) exactly
+        from fractions import Fraction
+        f = Fraction(str(dense_fraction)) * self.steps
+        self.dense_steps = -((-f.numerator) // f.denominator)
+
+    def dense(self, layer, step):
+        return layer in self.dense_layers or step < self.dense_steps
+
+    def warm(self, layer, step):
+        """True when the previous step of this layer also ran SCOPE."""
+        return not self.dense(layer, step) and step > self.dense_steps
 
 
 def _dummy_ranges(d):
@@ -133,9 +173,12 @@ class ScopePartitionLayer(ScopeLayer):
         self.tables = torch.empty(H, C, sum(self.c_m), dtype=torch.float32, device=device)
         self.workspace = B.alloc_partition_workspace(self.shape, C, self.part, device)
 
-    def cluster_keys(self, k, init_k=None, stream=None):
+    def cluster_keys(self, k, init_k=None, stream=None, warm=False, iters=None):
+        if warm:
+            raise NotImplementedError("warm starts are offered for the three RoPE ranges only")
         stride = init_k.shape[-1] if init_k is not None else 0
-        B.scope_cluster_key_partition(self.shape, k, self.part, self.iters, init_k,
+        B.scope_cluster_key_partition(self.shape, k, self.part,
+                                      self.iters if iters is None else int(iters), init_k,
                                       stride, self.k_centroids, self.codes,
                                       self.workspace, self.status, stream)
 
