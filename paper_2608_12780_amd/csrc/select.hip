@@ -26,7 +26,10 @@
 //   (reused from the base kernel when r_c == t_c; otherwise from the kept
 //   coarse histogram, one gathering pass and the digit rounds), then an
 //   ordered block compaction, four keys per thread, emits every key above
-//   it plus the lowest-index ties, in ascending key order.
+//   it plus the lowest-index ties, in ascending key order.  With distinct
+//   codes each key is classified by one LDS read: the row first writes two
+//   bits per distinct code (above / tied with the rank-r_c logit), and the
+//   code build stores each key's index among the distinct codes.
 #include <math.h>
 
 #include "common.h"
@@ -47,19 +50,52 @@ __device__ __forceinline__ int coarse_bin(float y) {
   return static_cast<int>(fminf(-y * 64.0f, static_cast<float>(kCoarseBins - 1)));
 }
 
+// Inclusive prefix sum over the 64 lanes of 32-bit values with DPP moves:
+// shifts by 1, 2, 4, 8 inside each row of 16 lanes, then the last lane of
+// row 0 (2) added to row 1 (3), then the last lane of row 1 to rows 2 and 3.
+// Lanes whose source falls outside the row read 0.
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v) {
+  v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x111, 0xf, 0xf, false));
+  v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x112, 0xf, 0xf, false));
+  v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x114, 0xf, 0xf, false));
+  v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x118, 0xf, 0xf, false));
+  v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x142, 0xa, 0xf, false));
+  v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x143, 0xc, 0xf, false));
+  return v;
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_scan(T v) {
+  if constexpr (sizeof(T) == 4) return static_cast<T>(wave_incl_scan_u32(static_cast<uint32_t>(v)));
+  else return wave_incl_scan(v);
+}
+
 template <typename T>
 __device__ T block_excl_scan(T v, T *total) {
-  __shared__ T ws[kSelBlock / 64];
+  constexpr int kWaves = kSelBlock / 64;
+  __shared__ __attribute__((aligned(16))) T ws[kWaves];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const T incl = wave_incl_scan(v);
+  const T incl = wave_scan(v);
   if (lane == 63) ws[w] = incl;
   __syncthreads();
   T base = 0, tot = 0;
+  if constexpr (sizeof(T) == 4 && kWaves == 16) {
+    // lanes 0..15 scan the wave totals inside DPP row 0
+    uint32_t x = lane < kWaves ? static_cast<uint32_t>(ws[lane]) : 0u;
+    x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x111, 0xf, 0xf, false));
+    x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x112, 0xf, 0xf, false));
+    x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x114, 0xf, 0xf, false));
+    x += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), 0x118, 0xf, 0xf, false));
+    tot = static_cast<T>(__builtin_amdgcn_readlane(static_cast<int>(x), kWaves - 1));
+    const int wu = __builtin_amdgcn_readfirstlane(w);  // the wave index, in a scalar register
+    base = wu > 0 ? static_cast<T>(__builtin_amdgcn_readlane(static_cast<int>(x), wu - 1)) : T(0);
+  } else {
 #pragma unroll
-  for (int i = 0; i < kSelBlock / 64; ++i) {
-    const T x = ws[i];
-    if (i < w) base += x;
-    tot += x;
+    for (int i = 0; i < kWaves; ++i) {
+      const T x = ws[i];
+      if (i < w) base += x;
+      tot += x;
+    }
   }
   __syncthreads();
   *total = tot;
@@ -133,6 +169,8 @@ struct CodeBooks {
   const uint32_t *ucodes;  // [heads][n]: distinct packed codes, KIND == kFromUnique
   const uint32_t *umult;   // [heads][n]: keys carrying each of them
   const int *ucount;       // [heads]: number of distinct codes
+  const uint32_t *uidx;    // [heads][upitch]: each key's distinct code, or null
+  int upitch;              // n rounded up to a multiple of 4
   CodePlanes cp;           // M and the table columns of each subspace
 };
 
@@ -239,25 +277,34 @@ __device__ int gather_bin(const LogitSource<KIND> &src, float M, int cbin,
   __syncthreads();
   const int lane = threadIdx.x & 63;
   const int n = src.count;
-  for (int j0 = 0; j0 < n; j0 += kSelBlock) {
-    const int j = j0 + threadIdx.x;
-    float s = 0.0f;
-    bool in = false;
-    if (j < n) {
-      s = src(j);
-      in = coarse_bin(s - M) == cbin;
+  // four entries per thread in flight (read at clamped positions; those
+  // past the end are not in the bin)
+  constexpr int kG = 4;
+  for (int j0 = 0; j0 < n; j0 += kG * kSelBlock) {
+    float sv[kG];
+    uint32_t wv[kG];
+#pragma unroll
+    for (int g = 0; g < kG; ++g) {
+      const int j = min(j0 + g * kSelBlock + static_cast<int>(threadIdx.x), n - 1);
+      sv[g] = src(j);
+      wv[g] = src.weight(j);
     }
-    const uint64_t mask = __ballot(in);
-    if (mask) {
-      int first = 0;
-      if (lane == static_cast<int>(__ffsll(static_cast<long long>(mask))) - 1)
-        first = atomicAdd(ncand, __popcll(mask));
-      first = __shfl(first, __ffsll(static_cast<long long>(mask)) - 1);
-      const int slot = first + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
-          static_cast<uint32_t>(mask >> 32), __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u)));
-      if (in && slot < CAP) {
-        cand[slot] = s;
-        candw[slot] = src.weight(j);
+#pragma unroll
+    for (int g = 0; g < kG; ++g) {
+      const int j = j0 + g * kSelBlock + static_cast<int>(threadIdx.x);
+      const bool in = j < n && coarse_bin(sv[g] - M) == cbin;
+      const uint64_t mask = __ballot(in);
+      if (mask) {
+        int first = 0;
+        if (lane == static_cast<int>(__ffsll(static_cast<long long>(mask))) - 1)
+          first = atomicAdd(ncand, __popcll(mask));
+        first = __shfl(first, __ffsll(static_cast<long long>(mask)) - 1);
+        const int slot = first + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+            static_cast<uint32_t>(mask >> 32), __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u)));
+        if (in && slot < CAP) {
+          cand[slot] = sv[g];
+          candw[slot] = wv[g];
+        }
       }
     }
   }
@@ -305,8 +352,15 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) 
   const LogitSource<KIND> src =
       make_source<KIND>(lut, h, c, n, c_q, cb, sigma, scores, tables);
   const int ne = src.count;
+  // four logits per thread in flight; clamped positions repeat a real entry
   float mloc = -INFINITY;
-  for (int j = threadIdx.x; j < ne; j += kSelBlock) mloc = fmaxf(mloc, src(j));
+  for (int j0 = threadIdx.x; j0 < ne; j0 += 4 * kSelBlock) {
+    float v[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) v[g] = src(min(j0 + g * kSelBlock, ne - 1));
+#pragma unroll
+    for (int g = 0; g < 4; ++g) mloc = fmaxf(mloc, v[g]);
+  }
   const float M = block_max(mloc);
   int t_p = n;
   uint32_t key_star = 0, above_star = 0;
@@ -323,11 +377,20 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) 
       int cb = -1;
       uint32_t cc = 0;
       uint64_t cm = 0;
+      float yv[4];
+      uint32_t wv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        // loads at clamped positions, all four in flight
+        const int j = min(j0 + i, ne - 1);
+        yv[i] = src(j) - M;
+        wv[i] = src.weight(j);
+      }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         if (j0 + i < ne) {
-          const float y = src(j0 + i) - M;
-          const uint32_t wt = src.weight(j0 + i);
+          const float y = yv[i];
+          const uint32_t wt = wv[i];
           const int bin = coarse_bin(y);
           const uint64_t e = fixexp(y) * wt;
           tloc += e;
@@ -399,6 +462,17 @@ __global__ __launch_bounds__(kSelBlock) void select_head_kernel(
   }
 }
 
+// Class words of the compaction: the distinct codes u of a head in groups of
+// 32, one uint2 per group: bit u%32 of .x is set when the code's logit ranks
+// above the rank-r_c logit, of .y when it ties with it.  They replace the
+// coarse histogram and candidate list in LDS once the crossing is known.
+constexpr int kPoolWords = kCoarseBins + 2 * kCandFinal;
+constexpr int kClassCodes = kPoolWords / 2 * 32;  // distinct codes the words cover
+// Keys per thread per compaction pass: with four, the 16 waves' output
+// slices take 16 KB of LDS and two blocks still fit on a CU.
+constexpr int kSelKeys = 4;
+static_assert(kSelKeys % 4 == 0 && kSelKeys * kSelBlock < 65536, "packed 16-bit counts");
+
 template <int KIND, int RKIND>
 __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) void select_final_kernel(
     int n, int c_q, CodeBooks cb, float sigma, const float *__restrict__ scores,
@@ -406,10 +480,11 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) 
     const uint32_t *__restrict__ row_state,
     const uint32_t *__restrict__ coarse_hist, int32_t *sel_idx) {
   __shared__ float lut[kMaxTable];
-  __shared__ uint32_t hc[kCoarseBins];
-  __shared__ float cand[kCandFinal];
-  __shared__ uint32_t candw[kCandFinal];
+  __shared__ __attribute__((aligned(16))) uint32_t pool[kPoolWords];
   __shared__ int ncand;
+  uint32_t *hc = pool;
+  float *cand = reinterpret_cast<float *>(pool + kCoarseBins);
+  uint32_t *candw = pool + kCoarseBins + kCandFinal;
   const int c = blockIdx.x, h = blockIdx.y;
   const size_t row = static_cast<size_t>(h) * c_q + c;
   int32_t *out = sel_idx + row * n;
@@ -453,37 +528,159 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) 
     refine_bin<RKIND, false, kCandFinal>(rsrc, M, x.bin, static_cast<uint64_t>(r), hc, nullptr,
                              cand, candw, &ncand, &key_r, &above, &unused);
   }
-  // ordered compaction, four consecutive keys per thread: keys above key_r
-  // and the first `need` ties in index order
+  // with distinct codes the keys are classified through their code's class
+  // bits (one LDS read per key); otherwise each key's logit is recomputed
+  const int ucnt = RKIND == kFromUnique ? min(max(cb.ucount[h], 0), n) : 0;
+  const bool by_class = RKIND == kFromUnique && cb.uidx != nullptr && ucnt > 0 && ucnt <= kClassCodes;
+  const uint2 *cls = reinterpret_cast<const uint2 *>(pool);
+  const uint32_t *kidx = by_class ? cb.uidx + static_cast<size_t>(h) * cb.upitch : nullptr;
+  if (by_class) {
+    __syncthreads();  // the crossing search is done with the pool
+    const uint32_t *uc = cb.ucodes + static_cast<size_t>(h) * n;
+    uint2 *clsw = reinterpret_cast<uint2 *>(pool);
+    const int lane = threadIdx.x & 63;
+    // four groups of 64 codes per wave in flight (codes read from clamped
+    // positions; those past the list are masked out of the ballots)
+    constexpr int kG = 4;
+    for (int u0 = 64 * kG * (threadIdx.x >> 6); u0 < ucnt; u0 += kG * kSelBlock) {
+      uint32_t code[kG];
+#pragma unroll
+      for (int g = 0; g < kG; ++g) code[g] = uc[min(u0 + 64 * g + lane, ucnt - 1)];
+#pragma unroll
+      for (int g = 0; g < kG; ++g) {
+        const int u = u0 + 64 * g + lane;
+        const uint32_t key =
+            desc_key(proxy_logit(src.P, cb.cp.col[1], cb.cp.col[2], cb.cp.col[3], code[g], sigma));
+        const uint64_t ab = __ballot(u < ucnt && key < key_r);
+        const uint64_t tb = __ballot(u < ucnt && key == key_r);
+        if (lane < 2 && u0 + 64 * g < ucnt)
+          clsw[((u0 + 64 * g) >> 5) + lane] =
+              lane == 0 ? make_uint2(static_cast<uint32_t>(ab), static_cast<uint32_t>(tb))
+                        : make_uint2(static_cast<uint32_t>(ab >> 32), static_cast<uint32_t>(tb >> 32));
+      }
+    }
+    __syncthreads();
+  }
+  const int cls_last = max((ucnt + 31) / 32 - 1, 0);
+  // Ordered compaction: every key above key_r and the first `need` ties in
+  // index order, in ascending key order.  Each pass takes kSelKeys
+  // consecutive keys per thread (their indices or codes read from clamped
+  // positions, unconditionally, so a pass's loads are in flight together;
+  // with class words the next pass's indices load during this one); one
+  // block scan of the packed per-thread counts places them: a selected key
+  // goes to (#above before it) + min(#ties before it, need).  A wave's keys
+  // are consecutive and so are its outputs, which it stages in its LDS slice
+  // and stores with consecutive lanes through a buffer resource spanning the
+  // row's r outputs (offsets past it are dropped by the hardware).
   const uint32_t need = static_cast<uint32_t>(r) - above;
+  const __amdgpu_buffer_rsrc_t rout =
+      __builtin_amdgcn_make_buffer_rsrc(out, static_cast<short>(0), r * 4, 0x00020000);
+  constexpr uint32_t kDropped = 0x80000000u;   // past any row (r * 4 < 2^31)
   uint32_t out_run = 0, ties_run = 0;
-  constexpr int KPT = 4;
-  for (int j0 = 0; j0 < n; j0 += KPT * kSelBlock) {
+  constexpr int KPT = kSelKeys;
+  __shared__ uint32_t stage_all[kSelBlock * KPT];
+  const int lane = threadIdx.x & 63;
+  uint32_t *stage = stage_all + (threadIdx.x >> 6) * 64 * KPT;
+  // the pitch is a multiple of 4, so a group that starts before n lies in
+  // the row; groups at or past n reread the row's last group
+  auto load_idx = [&](int j, uint4 (&v)[KPT / 4]) {
+#pragma unroll
+    for (int g = 0; g < KPT / 4; ++g)
+      v[g] = *reinterpret_cast<const uint4 *>(kidx + min(j + 4 * g, (n - 1) & ~3));
+  };
+  // one pass over keys j0 .. j0 + KPT * kSelBlock - 1 with this pass's
+  // indices in cur; the next pass's are loaded into nxt meanwhile (two
+  // buffers that trade places, so no register copy waits for the load)
+  auto pass = [&](int j0, const uint4 (&cur)[KPT / 4], uint4 (&nxt)[KPT / 4]) __attribute__((always_inline)) {
     const int jb = j0 + KPT * threadIdx.x;
     uint32_t fa = 0, ft = 0;  // per-key flags, bit i = key jb + i
+    if (by_class) {
+      uint32_t uu[KPT];
 #pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      if (jb + i < n) {
-        const uint32_t key = desc_key(src(jb + i));
+      for (int g = 0; g < KPT / 4; ++g) {
+        uu[4 * g + 0] = cur[g].x;
+        uu[4 * g + 1] = cur[g].y;
+        uu[4 * g + 2] = cur[g].z;
+        uu[4 * g + 3] = cur[g].w;
+      }
+      // the next pass's indices are in flight during this pass's scan
+      load_idx(jb + KPT * kSelBlock, nxt);
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) {
+        const uint2 wd = cls[min(static_cast<int>(uu[i] >> 5), cls_last)];
+        const uint32_t bit = uu[i] & 31u;
+        fa |= ((wd.x >> bit) & 1u) << i;
+        ft |= ((wd.y >> bit) & 1u) << i;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) {
+        const uint32_t key = desc_key(src(min(jb + i, n - 1)));
         fa |= static_cast<uint32_t>(key < key_r) << i;
         ft |= static_cast<uint32_t>(key == key_r) << i;
       }
     }
+    // keys at or past n count for nothing
+    const int valid = min(max(n - jb, 0), KPT);
+    const uint32_t vmask = valid >= 32 ? 0xFFFFFFFFu : (1u << valid) - 1u;
+    fa &= vmask;
+    ft &= vmask;
     uint32_t tot;
     const uint32_t ex = block_excl_scan<uint32_t>((static_cast<uint32_t>(__popc(ft)) << 16) |
                                                       static_cast<uint32_t>(__popc(fa)), &tot);
-    uint32_t a_pre = ex & 0xFFFFu, t_pre = ex >> 16;
+    const uint32_t a_pre = ex & 0xFFFFu, t_pre = ex >> 16;
     const uint32_t remaining = need > ties_run ? need - ties_run : 0u;
+    // this thread keeps its keys above and its first remaining - t_pre ties
+    uint32_t sel = fa;
+    if (ft) {
+      uint32_t take = remaining > t_pre ? remaining - t_pre : 0u;
+      uint32_t m = ft;
+      while (take && m) {
+        sel |= m & (0u - m);
+        m &= m - 1u;
+        --take;
+      }
+    }
+    // a wave's keys are consecutive, so are its outputs: stage them in the
+    // wave's LDS slice, then store the slice with consecutive lanes
+    const uint32_t pos0 = out_run + a_pre + min(t_pre, remaining);
+    const uint32_t wbase = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(pos0)));
+    const uint32_t wend = static_cast<uint32_t>(
+        __builtin_amdgcn_readlane(static_cast<int>(pos0 + static_cast<uint32_t>(__popc(sel))), 63));
+    uint32_t at = pos0 - wbase;
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
-      const bool a = (fa >> i) & 1u, tie = (ft >> i) & 1u;
-      if (a || (tie && t_pre < remaining))
-        out[out_run + a_pre + min(t_pre, remaining)] = jb + i;
-      a_pre += a;
-      t_pre += tie;
+      if ((sel >> i) & 1u) stage[at] = static_cast<uint32_t>(jb + i);
+      at += (sel >> i) & 1u;
     }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // a fixed count of stores (lanes past the wave's outputs store to an
+    // offset past the row, which is dropped), so the wait for the next
+    // pass's indices need not wait for these stores
+    const uint32_t wcnt = wend - wbase;
+#pragma unroll
+    for (int q = 0; q < KPT; ++q) {
+      const uint32_t k = static_cast<uint32_t>(64 * q + lane);
+      __builtin_amdgcn_raw_buffer_store_b32(stage[k], rout, k < wcnt ? (wbase + k) * 4u : kDropped, 0, 0);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     out_run += (tot & 0xFFFFu) + min(tot >> 16, remaining);
     ties_run += tot >> 16;
+  };
+  uint4 ia[KPT / 4], ib[KPT / 4];
+  constexpr int kStep = KPT * kSelBlock;
+  if (by_class) {
+    load_idx(KPT * threadIdx.x, ia);
+    for (int j0 = 0; j0 < n; j0 += 2 * kStep) {
+      pass(j0, ia, ib);
+      if (j0 + kStep < n) pass(j0 + kStep, ib, ia);
+    }
+  } else {
+    for (int j0 = 0; j0 < n; j0 += kStep) pass(j0, ia, ib);
   }
 }
 
@@ -492,12 +689,18 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) 
 // a free slot.  The code space is hashed into P parts of a head; block
 // (part, head) reads all of the head's codes and counts the ones of its
 // part in an LDS table with open addressing, then stores the part's
-// (code, count) pairs.  P is chosen so that the tables are at most half
-// full even if every key has its own code; should a skewed part still fill
-// its table, the head falls back to one entry per key (count 1), which the
-// selection treats exactly like the keys themselves.
+// (code, count) pairs, each occupied slot's rank among them, and for every
+// key of the part its (part, slot).  P is chosen so that the tables are at
+// most half full even if every key has its own code; should a skewed part
+// still fill its table, the head falls back to one entry per key (count 1),
+// which the selection treats exactly like the keys themselves.
 constexpr uint32_t kFreeSlot = 0xFFFFFFFFu;
 constexpr int kPartSlots = 16384;   // LDS table of one part: 128 KB
+constexpr int kSlotBits = 14;       // log2(kPartSlots)
+constexpr int kGatherBlocks = 16;   // blocks per head that assemble the lists
+// Every part reads all of a head's codes, so the build costs parts x n
+// reads; beyond kMaxParts parts (n > 262144) the passes visit every key.
+constexpr int kMaxParts = 32;
 
 __device__ __forceinline__ uint32_t code_hash(uint32_t code) { return code * 0x9E3779B1u; }
 
@@ -507,8 +710,9 @@ __global__ void code_parts_clear_kernel(int *overflow, int heads) {
 }
 
 __global__ __launch_bounds__(kSelBlock) void code_parts_kernel(
-    const uint32_t *__restrict__ codes, int n, int parts, uint32_t *stage_codes,
-    uint32_t *stage_mult, int *part_count, int *overflow) {
+    const uint32_t *__restrict__ codes, int n, int parts, int upitch, uint32_t *stage_codes,
+    uint32_t *stage_mult, uint32_t *stage_rank, int *part_count, uint32_t *key_slot,
+    int *overflow) {
   __shared__ uint32_t lk[kPartSlots];
   __shared__ uint32_t lc[kPartSlots];
   __shared__ int full;
@@ -520,22 +724,34 @@ __global__ __launch_bounds__(kSelBlock) void code_parts_kernel(
   if (threadIdx.x == 0) full = 0;
   __syncthreads();
   const uint32_t *hc = codes + static_cast<size_t>(h) * n;
-  for (int j = threadIdx.x; j < n; j += kSelBlock) {
-    const uint32_t code = hc[j] & 0x3FFFFFFFu;
-    const uint32_t hv = code_hash(code);
-    if (static_cast<int>((static_cast<uint64_t>(hv) * parts) >> 32) != p) continue;
-    uint32_t slot = hv & (kPartSlots - 1);
-    bool done = false;
-    for (int probe = 0; probe < kPartSlots; ++probe) {
-      const uint32_t prev = atomicCAS(&lk[slot], kFreeSlot, code);
-      if (prev == kFreeSlot || prev == code) {
-        atomicAdd(&lc[slot], 1u);
-        done = true;
-        break;
+  uint32_t *ks = key_slot + static_cast<size_t>(h) * upitch;
+  // four codes per thread in flight (clamped positions; the extra ones are
+  // skipped below)
+  constexpr int kG = 4;
+  for (int j0 = threadIdx.x; j0 < n; j0 += kG * kSelBlock) {
+    uint32_t cv[kG];
+#pragma unroll
+    for (int g = 0; g < kG; ++g) cv[g] = hc[min(j0 + g * kSelBlock, n - 1)];
+#pragma unroll
+    for (int g = 0; g < kG; ++g) {
+      const int j = j0 + g * kSelBlock;
+      const uint32_t code = cv[g] & 0x3FFFFFFFu;
+      const uint32_t hv = code_hash(code);
+      if (j >= n || static_cast<int>((static_cast<uint64_t>(hv) * parts) >> 32) != p) continue;
+      uint32_t slot = hv & (kPartSlots - 1);
+      bool done = false;
+      for (int probe = 0; probe < kPartSlots; ++probe) {
+        const uint32_t prev = atomicCAS(&lk[slot], kFreeSlot, code);
+        if (prev == kFreeSlot || prev == code) {
+          atomicAdd(&lc[slot], 1u);
+          ks[j] = (static_cast<uint32_t>(p) << kSlotBits) | slot;
+          done = true;
+          break;
+        }
+        slot = (slot + 1u) & (kPartSlots - 1);
       }
-      slot = (slot + 1u) & (kPartSlots - 1);
+      if (!done) full = 1;
     }
-    if (!done) full = 1;
   }
   __syncthreads();
   if (full) {
@@ -556,42 +772,64 @@ __global__ __launch_bounds__(kSelBlock) void code_parts_kernel(
     if (lk[i] != kFreeSlot) {
       stage_codes[base + at] = lk[i];
       stage_mult[base + at] = lc[i];
+      stage_rank[base + i] = at;
       ++at;
     }
   }
   if (threadIdx.x == 0) part_count[static_cast<size_t>(h) * parts + p] = static_cast<int>(total);
 }
 
-// One block per head: the parts' pairs concatenated into the head's list,
-// or one entry per key after an overflow.
+// Blocks (g, head): the parts' pairs concatenated into the head's list, and
+// each key's (part, slot) turned into its index in that list; or one entry
+// per key (its own index) after an overflow.
 __global__ __launch_bounds__(kSelBlock) void code_parts_gather_kernel(
-    const uint32_t *__restrict__ codes, int n, int parts, const uint32_t *__restrict__ stage_codes,
-    const uint32_t *__restrict__ stage_mult, const int *__restrict__ part_count,
-    const int *__restrict__ overflow, uint32_t *ucodes, uint32_t *umult, int *ucount) {
-  const int h = blockIdx.x;
+    const uint32_t *__restrict__ codes, int n, int parts, int upitch,
+    const uint32_t *__restrict__ stage_codes, const uint32_t *__restrict__ stage_mult,
+    const uint32_t *__restrict__ stage_rank, const int *__restrict__ part_count,
+    const int *__restrict__ overflow, uint32_t *ucodes, uint32_t *umult, int *ucount,
+    uint32_t *uidx) {
+  __shared__ int pbase[kMaxParts + 1];
+  const int g = blockIdx.x, h = blockIdx.y;
+  const int first = g * kSelBlock + threadIdx.x, stride = gridDim.x * kSelBlock;
   uint32_t *uc = ucodes + static_cast<size_t>(h) * n;
   uint32_t *um = umult + static_cast<size_t>(h) * n;
+  uint32_t *ui = uidx + static_cast<size_t>(h) * upitch;
   if (overflow[h]) {
-    for (int j = threadIdx.x; j < n; j += kSelBlock) {
+    for (int j = first; j < n; j += stride) {
       uc[j] = codes[static_cast<size_t>(h) * n + j] & 0x3FFFFFFFu;
       um[j] = 1u;
+      ui[j] = static_cast<uint32_t>(j);
     }
-    if (threadIdx.x == 0) ucount[h] = n;
+    if (g == 0 && threadIdx.x == 0) ucount[h] = n;
     return;
   }
-  int off = 0;
-  for (int p = 0; p < parts; ++p) {
-    const int cnt = part_count[static_cast<size_t>(h) * parts + p];
-    const size_t base = (static_cast<size_t>(h) * parts + p) * kPartSlots;
-    for (int i = threadIdx.x; i < cnt; i += kSelBlock) {
-      if (off + i < n) {
-        uc[off + i] = stage_codes[base + i];
-        um[off + i] = stage_mult[base + i];
+  if (threadIdx.x == 0) {
+    int off = 0;
+    for (int q = 0; q < parts; ++q) {
+      pbase[q] = off;
+      off += part_count[static_cast<size_t>(h) * parts + q];
+    }
+    pbase[parts] = off;
+  }
+  __syncthreads();
+  for (int q = 0; q < parts; ++q) {
+    const int cnt = pbase[q + 1] - pbase[q];
+    const size_t base = (static_cast<size_t>(h) * parts + q) * kPartSlots;
+    for (int i = first; i < cnt; i += stride) {
+      if (pbase[q] + i < n) {
+        uc[pbase[q] + i] = stage_codes[base + i];
+        um[pbase[q] + i] = stage_mult[base + i];
       }
     }
-    off += cnt;
   }
-  if (threadIdx.x == 0) ucount[h] = off < n ? off : n;
+  for (int j = first; j < n; j += stride) {
+    const uint32_t e = ui[j];
+    const int q = min(static_cast<int>(e >> kSlotBits), parts - 1);
+    const uint32_t slot = e & (kPartSlots - 1);
+    ui[j] = static_cast<uint32_t>(pbase[q]) +
+            stage_rank[(static_cast<size_t>(h) * parts + q) * kPartSlots + slot];
+  }
+  if (g == 0 && threadIdx.x == 0) ucount[h] = pbase[parts] < n ? pbase[parts] : n;
 }
 
 __global__ void fixexp_kernel(const float *y, uint64_t *out, int64_t count) {
@@ -606,16 +844,17 @@ int code_parts(int n) {
   return p < 1 ? 1 : static_cast<int>(p);
 }
 
-// Every part reads all of a head's codes, so the build costs parts x n
-// reads; beyond kMaxParts parts (n > 262144) the passes visit every key.
-constexpr int kMaxParts = 32;
 bool use_distinct_codes(int n) { return code_parts(n) <= kMaxParts; }
+
+// Row pitch of the per-key index arrays: n rounded up to 4 entries, so the
+// final kernel reads four keys' indices as one 16-byte load.
+static size_t key_pitch(int n) { return (static_cast<size_t>(n) + 3) & ~static_cast<size_t>(3); }
 
 size_t select_dedup_words(int heads, int n) {
   if (!use_distinct_codes(n)) return 0;
   const size_t parts = static_cast<size_t>(code_parts(n));
   return static_cast<size_t>(heads) *
-         (2 * parts * kPartSlots + parts + 2 * static_cast<size_t>(n) + 2);
+         (key_pitch(n) + 3 * parts * kPartSlots + parts + 2 * static_cast<size_t>(n) + 2);
 }
 
 hipError_t select_run(int heads, int n, int c_q, const Subspaces &sub, int d,
@@ -636,12 +875,16 @@ hipError_t select_run(int heads, int n, int c_q, const Subspaces &sub, int d,
   hipError_t e = hipSuccess;
   const bool distinct = kind == kFromPacked && use_distinct_codes(n);
   if (distinct) {
-    // the head's distinct codes and their multiplicities
+    // the head's distinct codes, their multiplicities and each key's index
+    // among them (the index array first: 16-byte aligned like the scratch)
     const int parts = code_parts(n);
+    const int upitch = static_cast<int>(key_pitch(n));
     const size_t stage = static_cast<size_t>(heads) * parts * kPartSlots;
-    uint32_t *stage_codes = dedup;
+    uint32_t *uidx = dedup;
+    uint32_t *stage_codes = uidx + static_cast<size_t>(heads) * upitch;
     uint32_t *stage_mult = stage_codes + stage;
-    uint32_t *ucodes = stage_mult + stage;
+    uint32_t *stage_rank = stage_mult + stage;
+    uint32_t *ucodes = stage_rank + stage;
     uint32_t *umult = ucodes + static_cast<size_t>(heads) * n;
     int *part_count = reinterpret_cast<int *>(umult + static_cast<size_t>(heads) * n);
     int *ucount = part_count + static_cast<size_t>(heads) * parts;
@@ -649,15 +892,18 @@ hipError_t select_run(int heads, int n, int c_q, const Subspaces &sub, int d,
     hipLaunchKernelGGL(code_parts_clear_kernel, dim3((heads + 255) / 256), dim3(256), 0, s,
                        overflow, heads);
     hipLaunchKernelGGL(code_parts_kernel, dim3(parts, heads), dim3(kSelBlock), 0, s, codes32, n,
-                       parts, stage_codes, stage_mult, part_count, overflow);
-    hipLaunchKernelGGL(code_parts_gather_kernel, dim3(heads), dim3(kSelBlock), 0, s, codes32, n,
-                       parts, stage_codes, stage_mult, part_count, overflow, ucodes, umult,
-                       ucount);
+                       parts, upitch, stage_codes, stage_mult, stage_rank, part_count, uidx,
+                       overflow);
+    hipLaunchKernelGGL(code_parts_gather_kernel, dim3(kGatherBlocks, heads), dim3(kSelBlock), 0, s,
+                       codes32, n, parts, upitch, stage_codes, stage_mult, stage_rank, part_count,
+                       overflow, ucodes, umult, ucount, uidx);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     cb.ucodes = ucodes;
     cb.umult = umult;
     cb.ucount = ucount;
+    cb.uidx = uidx;
+    cb.upitch = upitch;
   }
 #define SCOPE_SEL_BASE(K)                                                          \
   hipLaunchKernelGGL(select_base_kernel<K>, grid, block, 0, s, n, c_q, cb, sigma,  \
