@@ -71,6 +71,19 @@ __device__ __forceinline__ uint4 load8(const void *base, size_t elem) {
 // head, clusters in order with their row chunks adjacent.  All XCDs work on
 // the same head at a time, so one head's K/V (60 MB at 118800 x 128 bf16) is
 // what the 256 MB memory-side cache has to hold.
+//
+// Block b runs on XCD b mod 8.  Runs of kRun consecutive work items (the
+// chunks of one cluster, which gather the same K/V rows) go to one XCD so
+// that they share its L2; windows of 8 * kRun items still follow the list
+// order.  A partial last window keeps the identity map.
+constexpr int kXcds = 8, kRun = 4;
+__device__ __forceinline__ int xcd_item(int b, int total) {
+  constexpr int W = kXcds * kRun;
+  const int w0 = b / W * W;
+  if (w0 + W > total) return b;
+  const int r = b - w0;
+  return w0 + (r % kXcds) * kRun + r / kXcds;
+}
 
 template <int D, bool BF16IN>
 __global__ __launch_bounds__(kNW * 64) void attn_kernel(
@@ -97,7 +110,7 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel(
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kBN * KS];
   __shared__ __attribute__((aligned(16))) uint16_t Vs[2][kBN * KSV];
 
-  const int item = blockIdx.x;
+  const int item = xcd_item(static_cast<int>(blockIdx.x), total_items);
   if (item >= total_items) return;
   const int h = item / items_per_head;
   const int4 it = items[item];
@@ -376,7 +389,7 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
   __shared__ __attribute__((aligned(16))) uint16_t V0[kBN * D];
   __shared__ __attribute__((aligned(16))) uint16_t V1[kBN * D];
 
-  const int item = blockIdx.x;
+  const int item = xcd_item(static_cast<int>(blockIdx.x), total_items);
   if (item >= total_items) return;
   const int h = item / items_per_head;
   const int4 it = items[item];
