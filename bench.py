@@ -97,26 +97,29 @@ def sdpa_ms(torch, q, k, v, reps):
     return None, None
 
 
+ATTN_ROWS = 16384  # query rows of the CPU baseline's attention sample
+
+
 def cpu_baseline(cfg, x, layer_np):
     """The oracle on one head of the workload, timed on this host's cores.
 
-    Sample: head 0; query k-means with 3 of the iterations; key-subspace
-    k-means with 1 iteration plus the final assignment; score tables and
-    proxy logits; selection for every query cluster; attention for 256 query
-    rows.  Each stage is scaled to its full per-head work (iterations, rows)
-    and the per-head sum to all heads."""
+    Sample (about 15-20 s of CPU work at 720p): head 0 with every stage run
+    in full (all k-means iterations, tables, logits, selection of every
+    cluster) except attention, which runs for a seeded uniform sample of
+    ATTN_ROWS query rows (each row's cost follows its cluster's key count,
+    so the sample is unbiased) and is scaled to all rows; the per-head sum
+    is scaled to all heads."""
     import oracle
     oracle.lib()
     cm = (cfg.c_m,) * 3
     q, k, v = x.q[:1], x.k[:1], x.v[:1]
     t = {}
-    it_q = min(3, cfg.iters)
     s = time.perf_counter()
-    qr = oracle.cluster_queries(q, cfg.c_q, it_q, x.init_q[:1])
-    t["query_kmeans"] = (time.perf_counter() - s) * cfg.iters / it_q
+    qr = oracle.cluster_queries(q, cfg.c_q, cfg.iters, x.init_q[:1])
+    t["query_kmeans"] = time.perf_counter() - s
     s = time.perf_counter()
-    kr = oracle.cluster_key_subspaces(k, cfg.ranges, cm, 1, x.init_k[:1])
-    t["key_kmeans"] = (time.perf_counter() - s) * (cfg.iters + 1) / 2
+    kr = oracle.cluster_key_subspaces(k, cfg.ranges, cm, cfg.iters, x.init_k[:1])
+    t["key_kmeans"] = time.perf_counter() - s
     s = time.perf_counter()
     P = oracle.tables(qr["centroids"], kr["centroids"], cfg.ranges, cm)
     S = oracle.proxy_scores(P, kr["codes"], cfg.d, cm)
@@ -125,13 +128,15 @@ def cpu_baseline(cfg, x, layer_np):
     sel = oracle.select(S, qr["counts"], cfg.rho, cfg.k_fix)
     t["select"] = time.perf_counter() - s
     del S
-    rows = 256
+    rows = min(ATTN_ROWS, cfg.n)
     mask = np.zeros((1, cfg.n), np.uint8)
     mask[0, np.random.default_rng(0).choice(cfg.n, rows, replace=False)] = 1
     s = time.perf_counter()
     oracle.attention(q, k, v, qr["offsets"], qr["perm"], sel["sel_counts"],
                      sel["sel_idx"], row_mask=mask)
-    t["attention"] = (time.perf_counter() - s) * cfg.n / rows
+    t_attn = time.perf_counter() - s
+    t["attention"] = t_attn * cfg.n / rows
+    measured = sum(t.values()) - t["attention"] + t_attn
     per_head = sum(t.values())
     layer_s = per_head * cfg.heads
     return {
@@ -142,11 +147,12 @@ def cpu_baseline(cfg, x, layer_np):
         "kind": "oracle",
         "layer_s_extrapolated": layer_s,
         "per_head_stage_s": {k_: round(v_, 3) for k_, v_ in t.items()},
-        "sample": (f"head 0 of {cfg.heads}: query k-means {it_q}/{cfg.iters} "
-                   f"iterations, key k-means 1/{cfg.iters} iterations + final "
-                   f"assignment, tables, logits, selection of all {cfg.c_q} "
-                   f"clusters, attention for {rows}/{cfg.n} query rows; each "
-                   f"stage scaled to its full work, x{cfg.heads} heads"),
+        "measured_s": round(measured, 2),
+        "sample": (f"head 0 of {cfg.heads}, every stage in full (query and key "
+                   f"k-means, {cfg.iters} iterations each, tables, logits, selection "
+                   f"of all {cfg.c_q} clusters) except attention: {rows} of {cfg.n} "
+                   f"query rows (seeded uniform sample), scaled to all rows; "
+                   f"x{cfg.heads} heads"),
     }
 
 
