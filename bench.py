@@ -730,7 +730,10 @@ def counter_summary(csvs, cmd):
     mean = {k: {c: float(np.mean(v)) for c, v in d.items()} for k, d in agg.items()}
 
     def occupancy(r):
-        regs = max(r["vgpr"] + r["agpr"], 1)
+        # the trace's VGPR_Count is half the allocated count on this GPU
+        # (granules of 8 registers read as granules of 4): the compiler
+        # reports 190 VGPRs for attn_kernel_dma, the trace 96
+        regs = max(2 * r["vgpr"] + r["agpr"], 1)
         by_regs = 512 // (((regs + 7) // 8) * 8)
         waves_per_block = max(1, (r["wg"] + 63) // 64)
         by_lds = (160 * 1024 // r["lds"]) * waves_per_block / 4.0 if r["lds"] else 8
@@ -760,7 +763,8 @@ def counter_summary(csvs, cmd):
               f"{CALIB_BYTES} bytes",
               "  GB/s      (fetch + write bytes) / duration",
               "  TA busy%  TA_BUSY_avr / (GRBM_GUI_ACTIVE / 8): the address unit of buffer loads",
-              "  occ       waves per SIMD the kernel's VGPR+AGPR and LDS allow", ""]
+              "  vgpr      VGPR_Count as the trace reports it (half the allocated registers)",
+              "  occ       waves per SIMD the kernel's registers and LDS allow", ""]
     if f_fac:
         lines.append(f"calibration copy: FETCH_SIZE factor {f_fac:.4f}, WRITE_SIZE factor "
                      f"{(w_fac or float('nan')):.4f}")
