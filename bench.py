@@ -103,7 +103,7 @@ ATTN_ROWS = 16384  # query rows of the CPU baseline's attention sample
 def cpu_baseline(cfg, x, layer_np):
     """The oracle on one head of the workload, timed on this host's cores.
 
-    Sample (about 15-20 s of CPU work at 720p): head 0 with every stage run
+    Sample (about 12-20 s of CPU work at 720p): head 0 with every stage run
     in full (all k-means iterations, tables, logits, selection of every
     cluster) except attention, which runs for a seeded uniform sample of
     ATTN_ROWS query rows (each row's cost follows its cluster's key count,
