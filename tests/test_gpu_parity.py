@@ -375,6 +375,20 @@ def test_selection_beyond_the_distinct_code_limit():
     _select_from_codes(tables, codes, counts, d, c_m, 0.8, (n + 9) // 10)
 
 
+def test_selection_with_more_distinct_codes_than_the_class_bits_hold():
+    """200000 keys, every code distinct: the distinct-code passes run (25
+    parts), but the final compaction's LDS class bits cover 163840 codes, so
+    it classifies each key from its own logit instead.  Against the oracle."""
+    rng = np.random.default_rng(24)
+    H, C, n, d, c_m = 1, 4, 200000, 64, (64, 64, 64)
+    flat = rng.permutation(64 ** 3)[:n].astype(np.uint32)
+    codes = ((flat % 64) | (((flat // 64) % 64) << 10) | ((flat // 4096) << 20)).reshape(H, n)
+    assert np.unique(codes).size == n > 163840
+    tables = rng.standard_normal((H, C, sum(c_m))).astype(np.float32) * 2
+    counts = rng.multinomial(n, np.ones(C) / C, size=H).astype(np.int32)
+    _select_from_codes(tables, codes.astype(np.uint32), counts, d, c_m, 0.8, (n + 9) // 10)
+
+
 def test_points_at_exactly_zero_score():
     """A point whose score against its best centroid is exactly zero (centroid
     u = (2, 0, ...), point x = (1, 5, 0, ...): |u|^2 - 2<x, u> = 0) packs its
