@@ -691,7 +691,7 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) 
 // part in an LDS table with open addressing, then stores the part's
 // (code, count) pairs, each occupied slot's rank among them, and for every
 // key of the part its (part, slot).  P is chosen so that the tables are at
-// most half full even if every key has its own code; should a skewed part
+// most 80% full even if every key has its own code; should a skewed part
 // still fill its table, the head falls back to one entry per key (count 1),
 // which the selection treats exactly like the keys themselves.
 constexpr uint32_t kFreeSlot = 0xFFFFFFFFu;
@@ -699,8 +699,9 @@ constexpr int kPartSlots = 16384;   // LDS table of one part: 128 KB
 constexpr int kSlotBits = 14;       // log2(kPartSlots)
 constexpr int kGatherBlocks = 16;   // blocks per head that assemble the lists
 // Every part reads all of a head's codes, so the build costs parts x n
-// reads; beyond kMaxParts parts (n > 262144) the passes visit every key.
+// reads; beyond kMaxDistinctKeys keys the passes visit every key.
 constexpr int kMaxParts = 32;
+constexpr int kMaxDistinctKeys = 262144;
 
 __device__ __forceinline__ uint32_t code_hash(uint32_t code) { return code * 0x9E3779B1u; }
 
@@ -840,11 +841,13 @@ __global__ void fixexp_kernel(const float *y, uint64_t *out, int64_t count) {
 }  // namespace
 
 int code_parts(int n) {
-  const long long p = (2LL * n + kPartSlots - 1) / kPartSlots;
+  // tables at most 80% full even if every key has its own code: at 720p
+  // (n = 118800) 10 parts, so 24 heads' blocks run in one round on 256 CUs
+  const long long p = (5LL * n + 4LL * kPartSlots - 1) / (4LL * kPartSlots);
   return p < 1 ? 1 : static_cast<int>(p);
 }
 
-bool use_distinct_codes(int n) { return code_parts(n) <= kMaxParts; }
+bool use_distinct_codes(int n) { return n <= kMaxDistinctKeys && code_parts(n) <= kMaxParts; }
 
 // Row pitch of the per-key index arrays: n rounded up to 4 entries, so the
 // final kernel reads four keys' indices as one 16-byte load.

@@ -350,7 +350,7 @@ def test_selection_when_one_dedup_part_overflows():
     must give the oracle's sets."""
     rng = np.random.default_rng(22)
     H, C, n, d, c_m = 2, 4, 40000, 64, (1024, 1024, 1024)
-    parts = (2 * n + 16383) // 16384
+    parts = (5 * n + 4 * 16384 - 1) // (4 * 16384)  # the build's part count
     cand = np.arange(0, 1 << 22, dtype=np.uint64)
     hv = (cand * np.uint64(0x9E3779B1)) & np.uint64(0xFFFFFFFF)
     same_part = cand[((hv * np.uint64(parts)) >> np.uint64(32)) == 0][:n].astype(np.uint32)
@@ -376,7 +376,7 @@ def test_selection_beyond_the_distinct_code_limit():
 
 
 def test_selection_with_more_distinct_codes_than_the_class_bits_hold():
-    """200000 keys, every code distinct: the distinct-code passes run (25
+    """200000 keys, every code distinct: the distinct-code passes run (16
     parts), but the final compaction's LDS class bits cover 163840 codes, so
     it classifies each key from its own logit instead.  Against the oracle."""
     rng = np.random.default_rng(24)
