@@ -468,6 +468,12 @@ __global__ __launch_bounds__(kSelBlock) void select_head_kernel(
 // coarse histogram and candidate list in LDS once the crossing is known.
 constexpr int kPoolWords = kCoarseBins + 2 * kCandFinal;
 constexpr int kClassCodes = kPoolWords / 2 * 32;  // distinct codes the words cover
+// the merged crossing pass keeps class words, the coarse histogram and a
+// list of the crossing bin's codes in the pool at once
+constexpr int kMergedCand = 2048;
+constexpr int kMergedClassWords = kPoolWords - kCoarseBins - kMergedCand;  // 32-bit words
+constexpr int kMergedCodes = kMergedClassWords / 2 * 32;
+static_assert(kMergedClassWords % 2 == 0 && kMergedCodes >= 65536, "merged pool layout");
 // Keys per thread per compaction pass: with four, the 16 waves' output
 // slices take 16 KB of LDS and two blocks still fit on a CU.
 constexpr int kSelKeys = 4;
@@ -497,11 +503,101 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) 
   const LogitSource<KIND> src =
       make_source<KIND>(lut, h, c, n, c_q, cb, sigma, scores, tables);
   const float M = row_max[row];
-  uint32_t key_r, above;
-  if (static_cast<uint32_t>(r) == row_state[4 * row + 0]) {
+  uint32_t key_r = 0, above = 0;
+  const bool have_key = static_cast<uint32_t>(r) == row_state[4 * row + 0];
+  if (have_key) {
     key_r = row_state[4 * row + 1];
     above = row_state[4 * row + 2];
-  } else {
+  }
+  // with distinct codes the keys are classified through their code's class
+  // bits (one LDS read per key); otherwise each key's logit is recomputed
+  const int ucnt = RKIND == kFromUnique ? min(max(cb.ucount[h], 0), n) : 0;
+  const bool by_class = RKIND == kFromUnique && cb.uidx != nullptr && ucnt > 0 && ucnt <= kClassCodes;
+  // Without the key, and with few enough distinct codes, one pass over them
+  // both classifies them by coarse bin (a code whose bin precedes the
+  // crossing bin ranks above the rank-r_c logit, one after it below) and
+  // lists the codes of the crossing bin; the digit rounds then find the key
+  // among those and fix their bits.  Pool: class words, then the coarse
+  // histogram, then the listed codes' indices.
+  const bool merged = by_class && !have_key && ucnt <= kMergedCodes;
+  const uint2 *cls = reinterpret_cast<const uint2 *>(pool);
+  const uint32_t *kidx = by_class ? cb.uidx + static_cast<size_t>(h) * cb.upitch : nullptr;
+  const uint32_t *uc = by_class ? cb.ucodes + static_cast<size_t>(h) * n : nullptr;
+  const uint32_t *um = by_class ? cb.umult + static_cast<size_t>(h) * n : nullptr;
+  const int lane = threadIdx.x & 63;
+  auto ulogit = [&](uint32_t code) __attribute__((always_inline)) {
+    return proxy_logit(src.P, cb.cp.col[1], cb.cp.col[2], cb.cp.col[3], code, sigma);
+  };
+  bool exact_build = by_class;   // class bits by exact comparison with key_r
+  if (merged) {
+    uint32_t *hm2 = pool + kMergedClassWords;
+    uint32_t *candu = hm2 + kCoarseBins;
+    for (int b = threadIdx.x; b < kCoarseBins; b += kSelBlock)
+      hm2[b] = coarse_hist[row * kCoarseBins + b];
+    if (threadIdx.x == 0) ncand = 0;
+    __syncthreads();
+    const Crossing x = find_crossing<false>(hm2, nullptr, kCoarseBins, 0,
+                                            static_cast<uint64_t>(r));
+    above = x.cnt_before;
+    const int cbin = x.bin;
+    uint2 *clsw = reinterpret_cast<uint2 *>(pool);
+    constexpr int kG = 4;
+    for (int u0 = 64 * kG * (threadIdx.x >> 6); u0 < ucnt; u0 += kG * kSelBlock) {
+      uint32_t code[kG];
+#pragma unroll
+      for (int g = 0; g < kG; ++g) code[g] = uc[min(u0 + 64 * g + lane, ucnt - 1)];
+#pragma unroll
+      for (int g = 0; g < kG; ++g) {
+        const int u = u0 + 64 * g + lane;
+        const int bin = coarse_bin(ulogit(code[g]) - M);
+        const bool in = u < ucnt && bin == cbin;
+        const uint64_t ab = __ballot(u < ucnt && bin < cbin);
+        const uint64_t cbm = __ballot(in);
+        if (lane < 2 && u0 + 64 * g < ucnt)
+          clsw[((u0 + 64 * g) >> 5) + lane] =
+              make_uint2(static_cast<uint32_t>(lane == 0 ? ab : ab >> 32), 0u);
+        if (cbm) {
+          int first = 0;
+          const int lead = static_cast<int>(__ffsll(static_cast<long long>(cbm))) - 1;
+          if (lane == lead) first = atomicAdd(&ncand, __popcll(cbm));
+          first = __shfl(first, lead);
+          const int slot = first + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+              static_cast<uint32_t>(cbm >> 32), __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(cbm), 0u)));
+          if (in && slot < kMergedCand) candu[slot] = static_cast<uint32_t>(u);
+        }
+      }
+    }
+    __syncthreads();
+    const int cnt = ncand;
+    uint64_t unused = 0;
+    if (cnt <= kMergedCand) {
+      refine<false>([&](auto f) {
+        for (int k2 = threadIdx.x; k2 < cnt; k2 += kSelBlock) {
+          const uint32_t u = candu[k2];
+          f(ulogit(uc[u]), um[u]);
+        }
+      }, M, static_cast<uint64_t>(r), hm2, nullptr, &key_r, &above, &unused);
+      // the listed codes' bits, now that the key is known
+      uint32_t *clsw32 = pool;
+      for (int k2 = threadIdx.x; k2 < cnt; k2 += kSelBlock) {
+        const uint32_t u = candu[k2];
+        const uint32_t key = desc_key(ulogit(uc[u]));
+        const uint32_t bit = 1u << (u & 31u);
+        if (key < key_r) atomicOr(&clsw32[2 * (u >> 5)], bit);
+        else if (key == key_r) atomicOr(&clsw32[2 * (u >> 5) + 1], bit);
+      }
+      exact_build = false;
+    } else {
+      // the crossing bin holds more codes than the list: digit rounds over
+      // every distinct code of the bin, then the exact class build
+      refine<false>([&](auto f) {
+        for (int u = threadIdx.x; u < ucnt; u += kSelBlock) {
+          const float sv = ulogit(uc[u]);
+          if (coarse_bin(sv - M) == cbin) f(sv, um[u]);
+        }
+      }, M, static_cast<uint64_t>(r), hm2, nullptr, &key_r, &above, &unused);
+    }
+  } else if (!have_key) {
     // the coarse count histogram of the base kernel (same logits, same M)
     for (int b = threadIdx.x; b < kCoarseBins; b += kSelBlock)
       hc[b] = coarse_hist[row * kCoarseBins + b];
@@ -528,17 +624,9 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) 
     refine_bin<RKIND, false, kCandFinal>(rsrc, M, x.bin, static_cast<uint64_t>(r), hc, nullptr,
                              cand, candw, &ncand, &key_r, &above, &unused);
   }
-  // with distinct codes the keys are classified through their code's class
-  // bits (one LDS read per key); otherwise each key's logit is recomputed
-  const int ucnt = RKIND == kFromUnique ? min(max(cb.ucount[h], 0), n) : 0;
-  const bool by_class = RKIND == kFromUnique && cb.uidx != nullptr && ucnt > 0 && ucnt <= kClassCodes;
-  const uint2 *cls = reinterpret_cast<const uint2 *>(pool);
-  const uint32_t *kidx = by_class ? cb.uidx + static_cast<size_t>(h) * cb.upitch : nullptr;
-  if (by_class) {
+  if (exact_build) {
     __syncthreads();  // the crossing search is done with the pool
-    const uint32_t *uc = cb.ucodes + static_cast<size_t>(h) * n;
     uint2 *clsw = reinterpret_cast<uint2 *>(pool);
-    const int lane = threadIdx.x & 63;
     // four groups of 64 codes per wave in flight (codes read from clamped
     // positions; those past the list are masked out of the ballots)
     constexpr int kG = 4;
@@ -549,8 +637,7 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) 
 #pragma unroll
       for (int g = 0; g < kG; ++g) {
         const int u = u0 + 64 * g + lane;
-        const uint32_t key =
-            desc_key(proxy_logit(src.P, cb.cp.col[1], cb.cp.col[2], cb.cp.col[3], code[g], sigma));
+        const uint32_t key = desc_key(ulogit(code[g]));
         const uint64_t ab = __ballot(u < ucnt && key < key_r);
         const uint64_t tb = __ballot(u < ucnt && key == key_r);
         if (lane < 2 && u0 + 64 * g < ucnt)
@@ -559,8 +646,8 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) 
                         : make_uint2(static_cast<uint32_t>(ab >> 32), static_cast<uint32_t>(tb >> 32));
       }
     }
-    __syncthreads();
   }
+  __syncthreads();
   const int cls_last = max((ucnt + 31) / 32 - 1, 0);
   // Ordered compaction: every key above key_r and the first `need` ties in
   // index order, in ascending key order.  Each pass takes kSelKeys
@@ -579,7 +666,6 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) 
   uint32_t out_run = 0, ties_run = 0;
   constexpr int KPT = kSelKeys;
   __shared__ uint32_t stage_all[kSelBlock * KPT];
-  const int lane = threadIdx.x & 63;
   uint32_t *stage = stage_all + (threadIdx.x >> 6) * 64 * KPT;
   // the pitch is a multiple of 4, so a group that starts before n lies in
   // the row; groups at or past n reread the row's last group
