@@ -474,9 +474,10 @@ constexpr int kMergedCand = 2048;
 constexpr int kMergedClassWords = kPoolWords - kCoarseBins - kMergedCand;  // 32-bit words
 constexpr int kMergedCodes = kMergedClassWords / 2 * 32;
 static_assert(kMergedClassWords % 2 == 0 && kMergedCodes >= 65536, "merged pool layout");
-// Keys per thread per compaction pass: with four, the 16 waves' output
-// slices take 16 KB of LDS and two blocks still fit on a CU.
-constexpr int kSelKeys = 4;
+// Keys per thread per compaction pass: with eight, the 16 waves' output
+// slices take 32 KB of LDS; with the table row sized at launch (1.5 KB for
+// three codebooks of 128) two blocks still fit on a CU.
+constexpr int kSelKeys = 8;
 static_assert(kSelKeys % 4 == 0 && kSelKeys * kSelBlock < 65536, "packed 16-bit counts");
 
 template <int KIND, int RKIND>
@@ -485,7 +486,7 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) 
     const float *__restrict__ tables, const int32_t *__restrict__ sel_counts, const float *__restrict__ row_max,
     const uint32_t *__restrict__ row_state,
     const uint32_t *__restrict__ coarse_hist, int32_t *sel_idx) {
-  __shared__ float lut[kMaxTable];
+  extern __shared__ float lut[];  // the table row: cs floats, sized at launch
   __shared__ __attribute__((aligned(16))) uint32_t pool[kPoolWords];
   __shared__ int ncand;
   uint32_t *hc = pool;
@@ -998,8 +999,9 @@ hipError_t select_run(int heads, int n, int c_q, const Subspaces &sub, int d,
   hipLaunchKernelGGL(select_base_kernel<K>, grid, block, 0, s, n, c_q, cb, sigma,  \
                      scores, tables, rho, k_fix, base, topp, row_max, row_state, \
                      coarse_hist)
+  const size_t lut_bytes = kind == kFromScores ? 16 : static_cast<size_t>(cb.cp.col[cb.cp.M]) * 4;
 #define SCOPE_SEL_FINAL(K, R)                                                      \
-  hipLaunchKernelGGL((select_final_kernel<K, R>), grid, block, 0, s, n, c_q, cb,   \
+  hipLaunchKernelGGL((select_final_kernel<K, R>), grid, block, lut_bytes, s, n, c_q, cb, \
                      sigma, scores, tables, sel_counts, row_max, row_state,       \
                      coarse_hist, sel_idx)
   if (kind == kFromScores) SCOPE_SEL_BASE(kFromScores);
