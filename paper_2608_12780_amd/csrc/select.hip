@@ -25,11 +25,13 @@
 // final kernel: the rank-r_c logit by the same radix selection on counts
 //   (reused from the base kernel when r_c == t_c; otherwise from the kept
 //   coarse histogram, one gathering pass and the digit rounds), then an
-//   ordered block compaction, four keys per thread, emits every key above
+//   ordered block compaction, eight keys per thread, emits every key above
 //   it plus the lowest-index ties, in ascending key order.  With distinct
 //   codes each key is classified by one LDS read: the row first writes two
-//   bits per distinct code (above / tied with the rank-r_c logit), and the
-//   code build stores each key's index among the distinct codes.
+//   bits per distinct code (above / tied with the rank-r_c logit; when the
+//   row searches the crossing itself, in the same pass that lists the
+//   crossing bin's codes), and the code build stores each key's index among
+//   the distinct codes.
 #include <math.h>
 
 #include "common.h"
@@ -42,8 +44,7 @@ namespace {
 constexpr int kSelBlock = 1024;
 constexpr int kCoarseBins = kSelCoarseBins;
 constexpr int kMaxTable = kSelMaxTable;
-constexpr int kCand = 8192;      // logits of the crossing coarse bin held in LDS
-constexpr int kCandFinal = 4096; // the same in the final kernel (two blocks per CU)
+constexpr int kCand = 4096;  // logits of the crossing coarse bin held in LDS (two blocks per CU)
 
 __device__ __forceinline__ int coarse_bin(float y) {
   // y = s - M <= 0; monotone non-increasing in s
@@ -344,8 +345,8 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) 
   __shared__ float lut[kMaxTable];
   __shared__ uint32_t hc[kCoarseBins];
   __shared__ uint64_t hm[kCoarseBins];
-  __shared__ float cand[kCandFinal];
-  __shared__ uint32_t candw[kCandFinal];
+  __shared__ float cand[kCand];
+  __shared__ uint32_t candw[kCand];
   __shared__ int ncand;
   const int c = blockIdx.x, h = blockIdx.y;
   const size_t row = static_cast<size_t>(h) * c_q + c;
@@ -419,7 +420,7 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) 
     const Crossing x = find_crossing<true>(hc, hm, kCoarseBins, 0, T);
     uint32_t cnt_above = x.cnt_before;
     uint64_t mass_above = x.mass_before;
-    refine_bin<KIND, true, kCandFinal>(src, M, x.bin, T, hc, hm, cand, candw, &ncand, &key_star,
+    refine_bin<KIND, true, kCand>(src, M, x.bin, T, hc, hm, cand, candw, &ncand, &key_star,
                             &cnt_above, &mass_above);
     const float s_star = desc_key_value(key_star);
     const uint64_t e_star = fixexp(s_star - M);
@@ -466,7 +467,7 @@ __global__ __launch_bounds__(kSelBlock) void select_head_kernel(
 // 32, one uint2 per group: bit u%32 of .x is set when the code's logit ranks
 // above the rank-r_c logit, of .y when it ties with it.  They replace the
 // coarse histogram and candidate list in LDS once the crossing is known.
-constexpr int kPoolWords = kCoarseBins + 2 * kCandFinal;
+constexpr int kPoolWords = kCoarseBins + 2 * kCand;
 constexpr int kClassCodes = kPoolWords / 2 * 32;  // distinct codes the words cover
 // the merged crossing pass keeps class words, the coarse histogram and a
 // list of the crossing bin's codes in the pool at once
@@ -491,7 +492,7 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) 
   __shared__ int ncand;
   uint32_t *hc = pool;
   float *cand = reinterpret_cast<float *>(pool + kCoarseBins);
-  uint32_t *candw = pool + kCoarseBins + kCandFinal;
+  uint32_t *candw = pool + kCoarseBins + kCand;
   const int c = blockIdx.x, h = blockIdx.y;
   const size_t row = static_cast<size_t>(h) * c_q + c;
   int32_t *out = sel_idx + row * n;
@@ -622,7 +623,7 @@ __global__ __launch_bounds__(kSelBlock) __attribute__((amdgpu_waves_per_eu(8))) 
       rsrc.mult = cb.umult + static_cast<size_t>(h) * n;
       rsrc.count = min(max(cb.ucount[h], 0), n);
     }
-    refine_bin<RKIND, false, kCandFinal>(rsrc, M, x.bin, static_cast<uint64_t>(r), hc, nullptr,
+    refine_bin<RKIND, false, kCand>(rsrc, M, x.bin, static_cast<uint64_t>(r), hc, nullptr,
                              cand, candw, &ncand, &key_r, &above, &unused);
   }
   if (exact_build) {
@@ -937,7 +938,7 @@ int code_parts(int n) {
 bool use_distinct_codes(int n) { return n <= kMaxDistinctKeys && code_parts(n) <= kMaxParts; }
 
 // Row pitch of the per-key index arrays: n rounded up to 4 entries, so the
-// final kernel reads four keys' indices as one 16-byte load.
+// final kernel reads four keys' indices per 16-byte load.
 static size_t key_pitch(int n) { return (static_cast<size_t>(n) + 3) & ~static_cast<size_t>(3); }
 
 size_t select_dedup_words(int heads, int n) {
