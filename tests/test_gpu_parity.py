@@ -375,6 +375,24 @@ def test_selection_beyond_the_distinct_code_limit():
     _select_from_codes(tables, codes, counts, d, c_m, 0.8, (n + 9) // 10)
 
 
+def test_selection_between_the_merged_and_the_class_bit_limits():
+    """130000 keys, every code distinct: the final kernel keeps the class
+    bits (up to 163840 codes) but has too many codes for the single pass that
+    also lists the rank crossing's candidates (up to 98304), so rows that
+    search their crossing gather it, run the digit rounds and classify in a
+    second pass.  Against the oracle."""
+    rng = np.random.default_rng(25)
+    H, C, n, d, c_m = 1, 6, 130000, 64, (64, 64, 64)
+    flat = rng.permutation(64 ** 3)[:n].astype(np.uint32)
+    codes = ((flat % 64) | (((flat // 64) % 64) << 10) | ((flat // 4096) << 20)).reshape(H, n)
+    assert 98304 < np.unique(codes).size == n <= 163840
+    tables = rng.standard_normal((H, C, sum(c_m))).astype(np.float32) * 2
+    counts = rng.multinomial(n, np.ones(C) / C, size=H).astype(np.int32)
+    gpu = _select_from_codes(tables, codes.astype(np.uint32), counts, d, c_m, 0.8, (n + 9) // 10)
+    # some rows search their own crossing (r_c differs from the Top-p count)
+    assert (gpu["sel_counts"] != gpu["topp"]).any()
+
+
 def test_selection_with_more_distinct_codes_than_the_class_bits_hold():
     """200000 keys, every code distinct: the distinct-code passes run (16
     parts), but the final compaction's LDS class bits cover 163840 codes, so
