@@ -4,25 +4,30 @@
 //
 // bf16 points x are exact in bf16.  Each centroid is split into two bf16
 // terms, u ~ hi + lo (hi = bf16(u), lo = bf16(u - hi)), so every product
-// x_c hi_c and x_c lo_c is exact and two bf16 MFMAs per k-step give
-//   s~_r = fl(nu_r - 2 <x, hi_r + lo_r>_mfma).
-// Its distance to the canonical score c_r is bounded per point by
-//   |s~_r - c_r| <= beta = 2|x| (E + 8 DXP 2^-24 Nmax) + 2^-23 (numax + 2.02 |x| Nmax)
+// x_c hi_c and x_c lo_c is exact.  The MFMA accumulator starts at -nu_r / 2
+// and two bf16 MFMAs per k-step add the products, which gives the halved,
+// negated score
+//   a_r = fl(-nu_r / 2 + <x, hi_r + lo_r>_mfma),   argmin_r c_r = argmax_r -c_r / 2.
+// Summed in any order with one fp32 rounding per addition, the 2 DXP
+// products and the start value err by at most 2 DXP 2^-24 (numax / 2 +
+// |x| Nmax); the canonical score adds its dot product's DXP 2^-24 |x| Nmax and
+// one rounding of the final fma.  So, in the canonical scale,
+//   |-2 a_r - c_r| <= beta = 2|x| (E + 8 DXP 2^-24 Nmax)
+//                            + 2^-23 ((2 DXP + 1) numax + 2.02 |x| Nmax)
 // (E >= |u_r - hi_r - lo_r|, Nmax >= |hi_r| + |lo_r| and |u_r|, numax >=
-// |nu_r|: the split residual, both fp32 accumulations, the two roundings of
-// the final subtraction), inflated by 1%.  So the canonical argmin r*
-// satisfies s~_{r*} <= min_r s~_r + 2 beta.
+// |nu_r|; about twice the terms derived, for slack), inflated by 1%, and the
+// canonical argmin r* satisfies a_{r*} >= max_r a_r - beta.
 //
-// One pass keeps, per point, the three smallest approximate scores with the
-// centroid index packed into the low mantissa bits (IB bits; this moves a
-// score by less than delta = 2^(IB-23) |s|, added to the margin).  If the
-// second-smallest is more than 2 beta + 2 delta above the smallest, the
-// smallest's index is the only candidate and thus r*.  If only the third
-// is, r* is one of the two smallest, and the point's two half-wave lanes
-// re-score one each with the canonical arithmetic.  For the very few points
-// with three or more candidates, the wave recomputes the scores, lists every
-// candidate within the margin and re-scores them canonically.  In both
-// cases the smallest (score, r) wins, so equal scores keep the lowest index.
+// One pass keeps, per point, the three largest a_r with the centroid index
+// packed into the low mantissa bits (IB bits; this moves a value by less
+// than delta = 2^(IB-23) |a|, added to the margin).  If the second-largest
+// is more than beta + 2 delta below the largest, the largest's index is the
+// only candidate and thus r*.  If only the third is, r* is one of the two
+// largest, and the point's two half-wave lanes re-score one each with the
+// canonical arithmetic.  For the very few points with three or more
+// candidates, the wave recomputes the values, lists every candidate within
+// the margin and re-scores them canonically.  In both cases the smallest
+// canonical (score, r) wins, so equal scores keep the lowest index.
 //
 // Blocks are persistent per head: the two-term codebook is staged in LDS
 // once, then each wave independently takes 32-point slices; chunk
@@ -204,11 +209,11 @@ __device__ __forceinline__ FilterBound reduce_bound(const float (*red)[NW]) {
 }
 
 // Stages head h's two-term codebook (16-byte pieces of each row; LDS row
-// stride 2 DXP + 8) and its norms into LDS and returns the head's bound
-// constants.  Ends with a block barrier; the caller makes sure no wave still
-// reads the previous contents.
+// stride 2 DXP + 8), its norms and the accumulator start values -nu / 2
+// into LDS and returns the head's bound constants.  Ends with a block
+// barrier; the caller makes sure no wave still reads the previous contents.
 template <int DXP, int NW = kWavesPerBlock>
-__device__ __forceinline__ FilterBound stage_codebook(uint16_t *Us, float *nus,
+__device__ __forceinline__ FilterBound stage_codebook(uint16_t *Us, float *nus, float *nhs,
                                                       float (*red)[NW],
                                                       const uint16_t *__restrict__ ubf,
                                                       const float *__restrict__ nu,
@@ -230,6 +235,10 @@ __device__ __forceinline__ FilterBound stage_codebook(uint16_t *Us, float *nus,
     const size_t row = static_cast<size_t>(h) * cpad + r;
     const float v = nu[row];
     nus[r] = v;
+    // exact for every norm at or above 2^-125 (smaller ones move by at most
+    // 2^-150, far inside the margin); padding rows (nu = FLT_MAX) start at
+    // -FLT_MAX / 2 and never win
+    nhs[r] = -0.5f * v;
     if (r < C) {
       e_max = fmaxf(e_max, bnd[2 * row + 0]);
       n_max = fmaxf(n_max, bnd[2 * row + 1]);
@@ -264,11 +273,12 @@ struct SliceArgs {
 };
 
 // The assignment of the 32 points of slice sl of head h by one wave, against
-// the codebook staged in Us/nus with bound constants B (candidate scratch of
-// this wave: cand, best, ncand).
+// the codebook staged in Us/nus/nhs with bound constants B (candidate
+// scratch of this wave: cand, best, ncand).
 template <int DXP>
 __device__ __forceinline__ void assign_slice(const SliceArgs &A, const uint16_t *Us,
-                                             const float *nus, FilterBound B, int h, int sl,
+                                             const float *nus, const float *nhs, FilterBound B,
+                                             int h, int sl,
                                              uint32_t *cand_w, unsigned long long *best_w,
                                              int *ncand_w) {
   constexpr int US = 2 * DXP + 8;  // LDS row stride of the two-term codebook
@@ -310,13 +320,21 @@ __device__ __forceinline__ void assign_slice(const SliceArgs &A, const uint16_t 
   ss += __shfl_xor(ss, 32);
   const float nx = sqrtf(ss) * 1.0001f + 1e-30f;
   const float beta = (2.0f * nx * (E + kappa * Nmax) +
-                      0x1p-23f * (numax + 2.02f * nx * Nmax)) * 1.01f + 1e-25f;
+                      0x1p-23f * ((2.0f * DXP + 1.0f) * numax + 2.02f * nx * Nmax)) * 1.01f + 1e-25f;
 
-  // approximate scores of the 32 centroids rb .. rb+31 for the 32 points
+  // a_r of the 32 centroids rb .. rb+31 for the 32 points: the accumulator
+  // starts at -nu_r / 2 (lane holds rows rb + 8(e/4) + 4hf + e%4)
   auto chain = [&](int rb) {
     f32x16 acc;
+    const float *nh = nhs + rb + 4 * hf;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+    for (int q = 0; q < 4; ++q) {
+      const float4 v = *reinterpret_cast<const float4 *>(nh + 8 * q);
+      acc[4 * q + 0] = v.x;
+      acc[4 * q + 1] = v.y;
+      acc[4 * q + 2] = v.z;
+      acc[4 * q + 3] = v.w;
+    }
     const uint16_t *urow = &Us[(rb + l32) * US + 8 * hf];
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
@@ -327,40 +345,48 @@ __device__ __forceinline__ void assign_slice(const SliceArgs &A, const uint16_t 
     }
     return acc;
   };
-  // one pass: the three smallest packed scores per point (each med3 keeps
-  // the smaller two of its inputs' upper pair; the start value lies above
-  // every score of valid inputs)
-  float m1 = 0x1.1p127f, m2 = 0x1.1p127f, m3 = 0x1.1p127f;
+  // one pass: the three largest packed values per point (each med3 keeps
+  // the larger two of its inputs' lower pair; the start value lies below
+  // every value of valid inputs).  The index packed here leaves out the
+  // lane's 4 hf, which is the same for all of the lane's values (so their
+  // order is that of the full index) and is added once after the pass.
+  // The mask stays in a vector register so that the index, uniform across
+  // the wave, can come from a scalar register.
+  uint32_t vmask;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(vmask) : "s"(~imask));
+  float m1 = -0x1.1p127f, m2 = -0x1.1p127f, m3 = -0x1.1p127f;
   auto fold = [&](const f32x16 &acc, int rb) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      const uint32_t r = static_cast<uint32_t>(rb + 8 * (e >> 2) + 4 * hf + (e & 3));
-      const float sc = fmaf(-2.0f, acc[e], nus[r]);
-      const float sp = __uint_as_float((__float_as_uint(sc) & ~imask) | r);
+      const uint32_t ru = static_cast<uint32_t>(rb + 8 * (e >> 2) + (e & 3));
+      const float sp = __uint_as_float((__float_as_uint(acc[e]) & vmask) | ru);
       m3 = __builtin_amdgcn_fmed3f(m2, m3, sp);
       m2 = __builtin_amdgcn_fmed3f(m1, m2, sp);
-      m1 = __builtin_amdgcn_fmed3f(m1, sp, -0x1.1p127f);
+      m1 = __builtin_amdgcn_fmed3f(m1, sp, 0x1.1p127f);  // max without NaN quieting
     }
   };
-  // software pipeline: the scores of block rb are folded while the
-  // MFMAs of block rb + 32 run
-  f32x16 prev = chain(0);
-  for (int rb = 32; rb < cpad; rb += 32) {
-    const f32x16 cur = chain(rb);
-    fold(prev, rb - 32);
-    prev = cur;
-    // each MFMA of this block is followed by an LDS read and a share
-    // of the previous block's fold
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-#pragma unroll
-    for (int k = 0; k < 2 * KS; ++k) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
-    }
+  // software pipeline: the values of one block are folded while the MFMAs
+  // of the next run; two accumulators alternate, so no copies
+  f32x16 acc0 = chain(0), acc1;
+  int rb = 32;
+  for (; rb + 32 < cpad; rb += 64) {
+    acc1 = chain(rb);
+    fold(acc0, rb - 32);
+    acc0 = chain(rb + 32);
+    fold(acc1, rb);
   }
-  fold(prev, cpad - 32);
+  if (rb < cpad) {
+    acc1 = chain(rb);
+    fold(acc0, rb - 32);
+    fold(acc1, rb);
+  } else {
+    fold(acc0, rb - 32);
+  }
   {
+    const uint32_t add = 4u * static_cast<uint32_t>(hf);
+    m1 = __uint_as_float(__float_as_uint(m1) + add);
+    m2 = __uint_as_float(__float_as_uint(m2) + add);
+    m3 = __uint_as_float(__float_as_uint(m3) + add);
     // the other half-wave's three into this one's (same multiset, same
     // result in both halves)
     const float o[3] = {__shfl_xor(m1, 32), __shfl_xor(m2, 32), __shfl_xor(m3, 32)};
@@ -368,19 +394,21 @@ __device__ __forceinline__ void assign_slice(const SliceArgs &A, const uint16_t 
     for (int q = 0; q < 3; ++q) {
       m3 = __builtin_amdgcn_fmed3f(m2, m3, o[q]);
       m2 = __builtin_amdgcn_fmed3f(m1, m2, o[q]);
-      m1 = fminf(m1, o[q]);
+      m1 = __builtin_amdgcn_fmed3f(m1, o[q], 0x1.1p127f);
     }
   }
-  const float slack = (2.0f * beta + 2.0f * dpack * fabsf(m1)) * 1.001f;
-  const float lim = m1 + slack;
-  const float thr = lim + fabsf(lim) * 2e-6f + 1e-30f;
-  const bool needy = valid && !(m2 > thr);
+  // candidates: a_r >= max a - beta (halved scale: 2 x beta / 2), less the
+  // two packing perturbations
+  const float slack = (beta + 2.0f * dpack * fabsf(m1)) * 1.001f;
+  const float lim = m1 - slack;
+  const float thr = lim - fabsf(lim) * 2e-6f - 1e-30f;
+  const bool needy = valid && !(m2 < thr);
   // three or more candidates (very rare)
-  const bool wide = needy && !(m3 > thr);
+  const bool wide = needy && !(m3 < thr);
   int arg = static_cast<int>(__float_as_uint(m1) & imask);
 
   if (__ballot(needy && !wide)) {
-    // exactly two candidates, the two smallest packed scores: the point's
+    // exactly two candidates, the two largest packed values: the point's
     // two half-wave lanes re-score one each canonically and exchange
     unsigned long long key = ~0ull;
     if (needy && !wide) {
@@ -408,9 +436,8 @@ __device__ __forceinline__ void assign_slice(const SliceArgs &A, const uint16_t 
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const uint32_t r = static_cast<uint32_t>(rb + 8 * (e >> 2) + 4 * hf + (e & 3));
-          const float sc = fmaf(-2.0f, acc[e], nus[r]);
-          const float sp = __uint_as_float((__float_as_uint(sc) & ~imask) | r);
-          if (static_cast<int>(r) < C && sp <= thr) {
+          const float sp = __uint_as_float((__float_as_uint(acc[e]) & ~imask) | r);
+          if (static_cast<int>(r) < C && sp >= thr) {
             const int slot = atomicAdd(ncand_w, 1);
             if (slot < kWaveCand)
               cand_w[slot] = (static_cast<uint32_t>(l32) << 16) | r;
@@ -467,7 +494,8 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
     const float *__restrict__ bnd, int C, int cpad, int32_t *assign,
     size_t a_hs, int32_t *chunk_hist, int nchunks) {
   __shared__ __attribute__((aligned(16))) uint16_t Us[kUbfLds];
-  __shared__ float nus[kMaxCpad];
+  __shared__ __attribute__((aligned(16))) float nus[kMaxCpad];
+  __shared__ __attribute__((aligned(16))) float nhs[kMaxCpad];
   __shared__ uint32_t cand[kWavesPerBlock][kWaveCand];
   __shared__ unsigned long long best[kWavesPerBlock][32];
   __shared__ int ncand[kWavesPerBlock];
@@ -486,9 +514,9 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
     const long long seg_end = end < static_cast<long long>(h + 1) * nslices
                                   ? end : static_cast<long long>(h + 1) * nslices;
     __syncthreads();
-    const FilterBound B = stage_codebook<DXP>(Us, nus, red, ubf, nu, bnd, h, C, cpad);
+    const FilterBound B = stage_codebook<DXP>(Us, nus, nhs, red, ubf, nu, bnd, h, C, cpad);
     for (long long g = beg + w; g < seg_end; g += kWavesPerBlock)
-      assign_slice<DXP>(A, Us, nus, B, h, static_cast<int>(g - static_cast<long long>(h) * nslices),
+      assign_slice<DXP>(A, Us, nus, nhs, B, h, static_cast<int>(g - static_cast<long long>(h) * nslices),
                         cand[w], best[w], &ncand[w]);
     beg = seg_end;
   }
@@ -515,7 +543,8 @@ template <int D0, int D1, int D2>
 __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma3_kernel(
     const Sub3 *__restrict__ Sp, int n, int heads) {
   __shared__ __attribute__((aligned(16))) uint16_t Us[kUbfLds];
-  __shared__ float nus[kMaxCpad];
+  __shared__ __attribute__((aligned(16))) float nus[kMaxCpad];
+  __shared__ __attribute__((aligned(16))) float nhs[kMaxCpad];
   __shared__ uint32_t cand[kWavesPerBlock][kWaveCand];
   __shared__ unsigned long long best[kWavesPerBlock][32];
   __shared__ int ncand[kWavesPerBlock];
@@ -531,11 +560,11 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma3_kernel(
     const long long seg_end = end < static_cast<long long>(h + 1) * nslices
                                   ? end : static_cast<long long>(h + 1) * nslices;
     __syncthreads();
-    stage_codebook<D0>(Us + Sp->uoff[0], nus + Sp->noff[0], red[0], Sp->ubf[0], Sp->nu[0],
+    stage_codebook<D0>(Us + Sp->uoff[0], nus + Sp->noff[0], nhs + Sp->noff[0], red[0], Sp->ubf[0], Sp->nu[0],
                        Sp->bnd[0], h, Sp->a[0].C, Sp->a[0].cpad);
-    stage_codebook<D1>(Us + Sp->uoff[1], nus + Sp->noff[1], red[1], Sp->ubf[1], Sp->nu[1],
+    stage_codebook<D1>(Us + Sp->uoff[1], nus + Sp->noff[1], nhs + Sp->noff[1], red[1], Sp->ubf[1], Sp->nu[1],
                        Sp->bnd[1], h, Sp->a[1].C, Sp->a[1].cpad);
-    stage_codebook<D2>(Us + Sp->uoff[2], nus + Sp->noff[2], red[2], Sp->ubf[2], Sp->nu[2],
+    stage_codebook<D2>(Us + Sp->uoff[2], nus + Sp->noff[2], nhs + Sp->noff[2], red[2], Sp->ubf[2], Sp->nu[2],
                        Sp->bnd[2], h, Sp->a[2].C, Sp->a[2].cpad);
     const long long first = static_cast<long long>(h) * nslices;
     const int m = w < Sp->wave0[1] ? 0 : w < Sp->wave0[2] ? 1 : 2;
@@ -544,19 +573,19 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma3_kernel(
       const SliceArgs A = Sp->a[0];
       const FilterBound B = reduce_bound<kWavesPerBlock>(red[0]);
       for (long long g = beg + wi; g < seg_end; g += nw)
-        assign_slice<D0>(A, Us + Sp->uoff[0], nus + Sp->noff[0], B, h, static_cast<int>(g - first),
+        assign_slice<D0>(A, Us + Sp->uoff[0], nus + Sp->noff[0], nhs + Sp->noff[0], B, h, static_cast<int>(g - first),
                          cand[w], best[w], &ncand[w]);
     } else if (m == 1) {
       const SliceArgs A = Sp->a[1];
       const FilterBound B = reduce_bound<kWavesPerBlock>(red[1]);
       for (long long g = beg + wi; g < seg_end; g += nw)
-        assign_slice<D1>(A, Us + Sp->uoff[1], nus + Sp->noff[1], B, h, static_cast<int>(g - first),
+        assign_slice<D1>(A, Us + Sp->uoff[1], nus + Sp->noff[1], nhs + Sp->noff[1], B, h, static_cast<int>(g - first),
                          cand[w], best[w], &ncand[w]);
     } else {
       const SliceArgs A = Sp->a[2];
       const FilterBound B = reduce_bound<kWavesPerBlock>(red[2]);
       for (long long g = beg + wi; g < seg_end; g += nw)
-        assign_slice<D2>(A, Us + Sp->uoff[2], nus + Sp->noff[2], B, h, static_cast<int>(g - first),
+        assign_slice<D2>(A, Us + Sp->uoff[2], nus + Sp->noff[2], nhs + Sp->noff[2], B, h, static_cast<int>(g - first),
                          cand[w], best[w], &ncand[w]);
     }
     beg = seg_end;
