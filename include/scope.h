@@ -313,8 +313,8 @@ int32_t scope_sparse_attention(const scope_shape *shape, const void *q,
  * cannot allocate device memory (code under HIP graph capture, serving loops
  * and harnesses that forbid it).  Arguments, outputs, layout and errors as
  * call 5 without `workspace`/`ws_bytes`: the call's work list (heads *
- * (ceil(n / 256) + c_q) entries of 16 bytes) lives in a fixed device array
- * of SCOPE_NOALLOC_MAX_WORK_ITEMS entries (1 MiB), one per GPU, held until
+ * (ceil(n / 256) + c_q) slots of two 16-byte entries) lives in a fixed
+ * device array of SCOPE_NOALLOC_MAX_WORK_ITEMS entries (1 MiB), one per GPU, held until
  * the process ends; larger problems return SCOPE_ERR_SCRATCH_LIMIT before
  * anything is enqueued.  The array's device address is looked up on the
  * first call on each device (the current device).  No call allocates or

@@ -194,7 +194,7 @@ size_t select_ws(const scope_shape *s, int c_q, void *base, SelectWs *w) {
 
 size_t attn_ws(const scope_shape *s, int c_q, void *base, int4 **items) {
   Carver cv(base);
-  int4 *it = cv.take<int4>(static_cast<size_t>(s->heads) * scope::attn_items_per_head(s->n, c_q));
+  int4 *it = cv.take<int4>(2 * static_cast<size_t>(s->heads) * scope::attn_items_per_head(s->n, c_q));
   if (items) *items = it;
   return cv.used;
 }
@@ -819,9 +819,10 @@ int32_t scope_sparse_attention_noalloc(const scope_shape *shape, const void *q,
   int32_t st = check_attention(shape, q, k, v, c_q, offsets, perm, sel_counts,
                                sel_idx, scale, o);
   if (st) return st;
-  const size_t items = static_cast<size_t>(shape->heads) *
-                       scope::attn_items_per_head(shape->n, c_q);
-  if (items > scope::kAttnScratchItems) return SCOPE_ERR_SCRATCH_LIMIT;
+  // two 16-byte entries per work slot
+  const size_t entries = 2 * static_cast<size_t>(shape->heads) *
+                         scope::attn_items_per_head(shape->n, c_q);
+  if (entries > scope::kAttnScratchItems) return SCOPE_ERR_SCRATCH_LIMIT;
   int4 *list = nullptr;
   SCOPE_TRY(scope::attention_scratch(&list));
   SCOPE_TRY(scope::attention_run(shape->heads, shape->n, shape->d,

@@ -113,7 +113,7 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel(
   const int item = xcd_item(static_cast<int>(blockIdx.x), total_items);
   if (item >= total_items) return;
   const int h = item / items_per_head;
-  const int4 it = items[item];
+  const int4 it = items[2 * item];  // work slots of this kernel hold one chunk
   const int c = it.x, row0 = it.y, rows = it.z, r = it.w;
   if (rows <= 0) return;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
@@ -374,33 +374,34 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel(
 // straight into LDS by the buffer unit (one 1 KB load per 4 rows, no
 // staging registers).  Rows land unpadded, so 16-byte slots are
 // XOR-swizzled: slot = chunk ^ (row mod 16) in K tiles (16-row b128 reads)
-// and chunk ^ 4 (row mod 4) in V tiles (4-row transposing reads).  The four
-// tile buffers are distinct LDS objects, so the compiler's waits for the
-// loads into one never hold up reads of another.
-__global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
-    int n, int c_q, int items_per_head, int total_items,
-    const void *__restrict__ qv, const void *__restrict__ kv,
-    const void *__restrict__ vv, void *ov, const int32_t *__restrict__ offsets,
-    const int32_t *__restrict__ perm, const int32_t *__restrict__ sel_idx,
-    const int4 *__restrict__ items, float scale_log2) {
-  constexpr int D = 128;
-  __shared__ __attribute__((aligned(16))) uint16_t K0[kBN * D];
-  __shared__ __attribute__((aligned(16))) uint16_t K1[kBN * D];
-  __shared__ __attribute__((aligned(16))) uint16_t V0[kBN * D];
-  __shared__ __attribute__((aligned(16))) uint16_t V1[kBN * D];
+// and chunk ^ 4 (row mod 4) in V tiles (4-row transposing reads).  A work
+// slot may hold two chunks (A, B) of different clusters: A's waves come
+// first, each chunk has its own tiles, and every wave gathers its share of
+// both.  The four tile buffers (K and V, two steps) are distinct LDS
+// objects, each holding the tiles of both chunks, so the compiler's waits
+// for the loads into one never hold up the reads of another.
+using DmaTile = uint16_t[2][kBN * 128];
 
-  const int item = xcd_item(static_cast<int>(blockIdx.x), total_items);
-  if (item >= total_items) return;
-  const int h = item / items_per_head;
-  const int4 it = items[item];
-  const int c = it.x, row0 = it.y, rows = it.z, r = it.w;
-  if (rows <= 0) return;
+template <bool PAIRED>
+__device__ __forceinline__ void attn_dma_body(
+    int n, int c_q, int h, int4 ia, int4 ib, const void *__restrict__ qv,
+    const void *__restrict__ kv, const void *__restrict__ vv, void *ov,
+    const int32_t *__restrict__ offsets, const int32_t *__restrict__ perm,
+    const int32_t *__restrict__ sel_idx, float scale_log2, DmaTile &K0, DmaTile &K1,
+    DmaTile &V0, DmaTile &V1) {
+  constexpr int D = 128;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int l32 = lane & 31, hf = lane >> 5;
   const size_t hoff = static_cast<size_t>(h) * n * D;
+  // this wave's chunk: A's ceil(rows / 32) waves first, then B's
+  const int wa = (ia.z + 31) >> 5;
+  const int g = PAIRED && w >= wa ? 1 : 0;
+  const int4 it = g ? ib : ia;
+  const int c = it.x, row0 = it.y, rows = it.z, r = it.w;
+  const int wl = w - (g ? wa : 0);
 
-  // queries: wave w owns rows 32w + l32 of the chunk
-  const int ql = w * 32 + l32;
+  // queries: wave wl of the chunk owns its rows 32 wl + l32
+  const int ql = wl * 32 + l32;
   const bool qvalid = ql < rows;
   int qi = 0;
   if (qvalid) {
@@ -412,7 +413,7 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
   for (int s = 0; s < D / 16; ++s)
     qf[s] = as_bf16x8(qvalid ? load8<true>(qv, hoff + static_cast<size_t>(qi) * D + 16 * s + 8 * hf)
                              : make_uint4(0, 0, 0, 0));
-  const bool wave_active = w * 32 < rows;
+  const bool wave_active = wl * 32 < rows;
 
   f32x16 oacc[D / 32];
 #pragma unroll
@@ -421,36 +422,57 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
     for (int e = 0; e < 16; ++e) oacc[db][e] = 0.0f;
   float m_run = -INFINITY, l_run = 0.0f;
 
-  const int32_t *sel = sel_idx + (static_cast<size_t>(h) * c_q + c) * n;
-  const int ntiles = (r + kBN - 1) / kBN;
-  const __amdgpu_buffer_rsrc_t rsel = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<int32_t *>(sel), static_cast<short>(0), r * 4, 0x00020000);
+  // key tiles of each chunk; the block steps through the longer list
+  const int ntA = (ia.w + kBN - 1) / kBN, ntB = PAIRED ? (ib.w + kBN - 1) / kBN : 0;
+  const int ntiles = ntA > ntB ? ntA : ntB;
+  const int nt_own = (r + kBN - 1) / kBN;
+  auto sel_rsrc = [&](const int4 &e) {
+    return __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t *>(sel_idx + (static_cast<size_t>(h) * c_q + e.x) * n),
+        static_cast<short>(0), e.w * 4, 0x00020000);
+  };
+  const __amdgpu_buffer_rsrc_t rselA = sel_rsrc(ia);
+  const __amdgpu_buffer_rsrc_t rselB = sel_rsrc(PAIRED ? ib : ia);
   const int nbytes = static_cast<int>(static_cast<uint32_t>(n) * (D * 2));
   const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t *>(static_cast<const uint16_t *>(kv) + hoff), static_cast<short>(0), nbytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t *>(static_cast<const uint16_t *>(vv) + hoff), static_cast<short>(0), nbytes, 0x00020000);
 
-  // gathers: wave w brings rows 8w .. 8w+7 of each tile, four rows (1 KB)
-  // per load; lane L covers row 8w + 4i + L/16, slot L%16, and fetches the
-  // chunk that the swizzle puts there
-  auto load_idx = [&](int tile, int (&ix)[2]) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-      ix[i] = __builtin_amdgcn_raw_buffer_load_b32(rsel, (tile * kBN + 8 * w + 4 * i + (lane >> 4)) * 4, 0, 0);
+  // gathers: wave w brings rows 8w .. 8w+7 of each chunk's tile, four rows
+  // (1 KB) per load; lane L covers row 8w + 4i + L/16, slot L%16, and
+  // fetches the chunk that the swizzle puts there.  Past the end of a
+  // chunk's key list its index loads read zeros, so its gathers fetch row 0
+  // (the pairing matches key counts, so few such tiles).
+  struct Idx {
+    int a[2], b[2];
   };
-  auto gather_k = [&](uint16_t *kbuf, const int (&ix)[2]) {
+  auto load_idx = [&](int tile, Idx &ix) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int row = 8 * w + 4 * i + (lane >> 4), s = lane & 15;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, kbuf + (8 * w + 4 * i) * D, 16, ix[i] * (D * 2) + 16 * (s ^ (row & 15)), 0, 0, 0);
+      const int at = (tile * kBN + 8 * w + 4 * i + (lane >> 4)) * 4;
+      ix.a[i] = __builtin_amdgcn_raw_buffer_load_b32(rselA, at, 0, 0);
+      ix.b[i] = PAIRED ? __builtin_amdgcn_raw_buffer_load_b32(rselB, at, 0, 0) : 0;
     }
   };
-  auto gather_v = [&](uint16_t *vbuf, const int (&ix)[2]) {
+  auto gather_k = [&](uint16_t (*kbuf)[kBN * D], const Idx &ix) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int row = 8 * w + 4 * i + (lane >> 4), s = lane & 15;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, vbuf + (8 * w + 4 * i) * D, 16, ix[i] * (D * 2) + 16 * (s ^ (4 * (row & 3))), 0, 0, 0);
+      const int col = 16 * (s ^ (row & 15));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, kbuf[0] + (8 * w + 4 * i) * D, 16, ix.a[i] * (D * 2) + col, 0, 0, 0);
+      if constexpr (PAIRED)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, kbuf[1] + (8 * w + 4 * i) * D, 16, ix.b[i] * (D * 2) + col, 0, 0, 0);
+    }
+  };
+  auto gather_v = [&](uint16_t (*vbuf)[kBN * D], const Idx &ix) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int row = 8 * w + 4 * i + (lane >> 4), s = lane & 15;
+      const int col = 16 * (s ^ (4 * (row & 3)));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, vbuf[0] + (8 * w + 4 * i) * D, 16, ix.a[i] * (D * 2) + col, 0, 0, 0);
+      if constexpr (PAIRED)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, vbuf[1] + (8 * w + 4 * i) * D, 16, ix.b[i] * (D * 2) + col, 0, 0, 0);
     }
   };
 
@@ -461,11 +483,12 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
   const int vsw = 4 * (rl & 3);
   const int vhalf = 4 * (lane & 1);   // elements
 
-  // tile T from kt/vt0; the gathers of the next tile into kn/vn are issued
-  // between the phases: K rows after the S MFMAs, V rows before the PV MFMAs
-  auto compute = [&](int tile, const uint16_t *kt, const uint16_t *vt0, uint16_t *kn,
-                     uint16_t *vn, const int (&ix)[2]) {
-    if (!wave_active) {
+  // tile T of this wave's chunk from kt/vt0; the gathers of tile T+1 into
+  // kn/vn are issued between the phases: K rows after the S MFMAs, V rows
+  // before the PV MFMAs
+  auto compute = [&](int tile, const uint16_t *kt, const uint16_t *vt0,
+                     uint16_t (*kn)[kBN * D], uint16_t (*vn)[kBN * D], const Idx &ix) {
+    if (!wave_active || tile >= nt_own) {
       gather_k(kn, ix);
       gather_v(vn, ix);
       return;
@@ -575,18 +598,18 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
   // one step: indices of tile T+2 requested, tile T computed while tile T+1
   // is gathered into the free buffers; every wave's gathers land before the
   // barrier
-  int cidx[2], nidx[2];
-  auto step = [&](int tile, const uint16_t *kc, const uint16_t *vc, uint16_t *kn, uint16_t *vn) {
+  Idx cidx, nidx;
+  auto step = [&](int tile, uint16_t (*kc)[kBN * D], uint16_t (*vc)[kBN * D],
+                  uint16_t (*kn)[kBN * D], uint16_t (*vn)[kBN * D]) {
     load_idx(tile + 2, nidx);
-    compute(tile, kc, vc, kn, vn, cidx);
+    compute(tile, kc[g], vc[g], kn, vn, cidx);
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's gathers are in LDS
     __syncthreads();
-    cidx[0] = nidx[0];
-    cidx[1] = nidx[1];
+    cidx = nidx;
   };
 
   if (ntiles > 0) {
-    int ix0[2];
+    Idx ix0;
     load_idx(0, ix0);
     load_idx(1, cidx);
     gather_k(K0, ix0);
@@ -616,24 +639,76 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
     }
 }
 
-// Work list of one head: every cluster's queries cut into chunks of kBM rows,
-// clusters in order; unused slots get rows = 0.
+__global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
+    int n, int c_q, int items_per_head, int total_items,
+    const void *__restrict__ qv, const void *__restrict__ kv,
+    const void *__restrict__ vv, void *ov, const int32_t *__restrict__ offsets,
+    const int32_t *__restrict__ perm, const int32_t *__restrict__ sel_idx,
+    const int4 *__restrict__ items, float scale_log2) {
+  __shared__ __attribute__((aligned(16))) DmaTile K0;
+  __shared__ __attribute__((aligned(16))) DmaTile K1;
+  __shared__ __attribute__((aligned(16))) DmaTile V0;
+  __shared__ __attribute__((aligned(16))) DmaTile V1;
+  const int item = xcd_item(static_cast<int>(blockIdx.x), total_items);
+  if (item >= total_items) return;
+  const int h = item / items_per_head;
+  const int4 ia = items[2 * item], ib = items[2 * item + 1];
+  if (ia.z <= 0) return;
+  // one block-uniform branch: a lone chunk gathers one set of tiles
+  if (ib.z > 0)
+    attn_dma_body<true>(n, c_q, h, ia, ib, qv, kv, vv, ov, offsets, perm, sel_idx, scale_log2,
+                        K0, K1, V0, V1);
+  else
+    attn_dma_body<false>(n, c_q, h, ia, ib, qv, kv, vv, ov, offsets, perm, sel_idx, scale_log2,
+                         K0, K1, V0, V1);
+}
+
+// Work list of one head.  Every cluster's queries are cut into chunks of kBM
+// rows; a block runs one work slot of two entries (A, B), each (cluster,
+// first row, rows, selected keys), B empty (rows = 0) or a second chunk that
+// shares the block: A's chunk takes waves 0 .. ceil(rows_A / 32) - 1 and
+// B's the next ones.  Slots: the clusters' full chunks in cluster order,
+// then their remainder chunks (fewer than kBM rows), then empty slots.  With
+// `pair`, remainders are paired so that the two chunks need at most kNW
+// waves together: bucketed by their wave count w and ordered by key count
+// within a bucket, bucket w (largest first) takes partners from bucket
+// min(8 - w, w) down to 1 in key-count order, so paired chunks run similar
+// numbers of key tiles.  Remainders left without a partner run alone.
+constexpr int kPairMaxClusters = 2048;  // pairing up to this many clusters
 __global__ __launch_bounds__(1024) void attn_items_kernel(
-    int n, int c_q, int items_per_head, const int32_t *__restrict__ offsets,
+    int n, int c_q, int items_per_head, int pair, const int32_t *__restrict__ offsets,
     const int32_t *__restrict__ sel_counts, int4 *items) {
   __shared__ int wtot[16];
+  __shared__ int rem_w[kPairMaxClusters], rem_r[kPairMaxClusters], ord[kPairMaxClusters];
+  __shared__ int bucket_n[kNW + 1], bucket_at[kNW + 1];
+  __shared__ int4 seg[64];   // (A's first ordinal, B's first ordinal or -1, count, same bucket)
+  __shared__ int seg_at[65], nseg, full_tot, rem_tot;
   const int h = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int32_t *off = offsets + static_cast<size_t>(h) * (c_q + 1);
-  int4 *out = items + static_cast<size_t>(h) * items_per_head;
+  const int32_t *scnt = sel_counts + static_cast<size_t>(h) * c_q;
+  int4 *out = items + static_cast<size_t>(h) * items_per_head * 2;
+  const bool do_pair = pair && c_q <= kPairMaxClusters;
+  auto count_of = [&](int c) { return min(max(off[c + 1] - off[c], 0), n); };
+  auto keys_of = [&](int c) { return min(max(scnt[c], 0), n); };
+  auto put = [&](int slot, int4 a, int4 b) {
+    if (slot < items_per_head) {
+      out[2 * slot] = a;
+      out[2 * slot + 1] = b;
+    }
+  };
+  const int4 none = make_int4(0, 0, 0, 0);
+  if (t <= kNW) bucket_n[t] = 0;
+  __syncthreads();
+  // full chunks, in cluster order
   int run = 0;
   for (int c0 = 0; c0 < c_q; c0 += 1024) {
     const int c = c0 + t;
     int cnt = 0, rsel = 0;
     if (c < c_q) {
-      cnt = min(max(off[c + 1] - off[c], 0), n);
-      rsel = min(max(sel_counts[static_cast<size_t>(h) * c_q + c], 0), n);
+      cnt = count_of(c);
+      rsel = keys_of(c);
     }
-    const int k = (cnt + kBM - 1) / kBM;
+    const int k = cnt / kBM, rem = cnt - k * kBM;
     const int incl = wave_incl_scan(k);
     if (lane == 63) wtot[w] = incl;
     __syncthreads();
@@ -644,15 +719,120 @@ __global__ __launch_bounds__(1024) void attn_items_kernel(
     }
     __syncthreads();
     const int first = run + base + incl - k;
-    for (int q = 0; q < k; ++q) {
-      const int slot = first + q;
-      if (slot < items_per_head)
-        out[slot] = make_int4(c, q * kBM, min(kBM, cnt - q * kBM), rsel);
-    }
+    for (int q = 0; q < k; ++q) put(first + q, make_int4(c, q * kBM, kBM, rsel), none);
     run += tot;
+    // remainders, bucketed by wave count for pairing
+    if (do_pair && c < c_q) {
+      rem_w[c] = rem > 0 ? (rem + 31) / 32 : 0;
+      rem_r[c] = rsel;
+      if (rem > 0) atomicAdd(&bucket_n[rem_w[c]], 1);
+    }
   }
-  for (int slot = run + t; slot < items_per_head; slot += 1024)
-    out[slot] = make_int4(0, 0, 0, 0);
+  if (t == 0) full_tot = run;
+  __syncthreads();
+  if (!do_pair) {
+    // remainders alone, in cluster order, after the full chunks
+    int at = 0;
+    for (int c0 = 0; c0 < c_q; c0 += 1024) {
+      const int c = c0 + t;
+      int cnt = 0, rsel = 0;
+      if (c < c_q) {
+        cnt = count_of(c);
+        rsel = keys_of(c);
+      }
+      const int rem = cnt % kBM, has = rem > 0 ? 1 : 0;
+      const int incl = wave_incl_scan(has);
+      if (lane == 63) wtot[w] = incl;
+      __syncthreads();
+      int base = 0, tot = 0;
+      for (int i = 0; i < 16; ++i) {
+        if (i < w) base += wtot[i];
+        tot += wtot[i];
+      }
+      __syncthreads();
+      if (has) put(full_tot + at + base + incl - 1, make_int4(c, cnt - rem, rem, rsel), none);
+      at += tot;
+    }
+    for (int slot = full_tot + at + t; slot < items_per_head; slot += 1024) put(slot, none, none);
+    return;
+  }
+  // ordinal of each remainder within (bucket ascending, keys ascending,
+  // cluster ascending)
+  if (t == 0) {
+    int a = 0;
+    for (int b = 0; b <= kNW; ++b) {
+      bucket_at[b] = a;
+      a += b == 0 ? 0 : bucket_n[b];
+    }
+    rem_tot = a;
+  }
+  __syncthreads();
+  for (int c = t; c < c_q; c += 1024) {
+    const int wc = rem_w[c];
+    if (wc == 0) continue;
+    const int rc = rem_r[c];
+    int pos = bucket_at[wc];
+    for (int o = 0; o < c_q; ++o)
+      if (rem_w[o] == wc && (rem_r[o] < rc || (rem_r[o] == rc && o < c))) ++pos;
+    ord[pos] = c;
+  }
+  // the pairing plan (at most kNW * kNW segments), one thread
+  if (t == 0) {
+    int nxt[kNW + 1], left[kNW + 1];
+    for (int b = 0; b <= kNW; ++b) {
+      nxt[b] = bucket_at[b];
+      left[b] = b == 0 ? 0 : bucket_n[b];
+    }
+    int ns = 0;
+    for (int wa = kNW; wa >= 1; --wa) {
+      for (int wb = min(kNW - wa, wa); wb >= 1 && left[wa] > 0; --wb) {
+        const int m = wb == wa ? left[wa] / 2 : min(left[wa], left[wb]);
+        if (m <= 0) continue;
+        seg[ns++] = make_int4(nxt[wa], nxt[wb], m, wb == wa ? 1 : 0);
+        if (wb == wa) {
+          nxt[wa] += 2 * m;
+          left[wa] -= 2 * m;
+        } else {
+          nxt[wa] += m;
+          left[wa] -= m;
+          nxt[wb] += m;
+          left[wb] -= m;
+        }
+      }
+      if (left[wa] > 0) {  // no partner left: alone
+        seg[ns++] = make_int4(nxt[wa], -1, left[wa], 0);
+        nxt[wa] += left[wa];
+        left[wa] = 0;
+      }
+    }
+    int a = 0;
+    for (int i = 0; i < ns; ++i) {
+      seg_at[i] = a;
+      a += seg[i].z;
+    }
+    seg_at[ns] = a;
+    nseg = ns;
+  }
+  __syncthreads();
+  const int total = seg_at[nseg];
+  auto entry = [&](int c) {
+    const int cnt = count_of(c), rem = cnt % kBM;
+    return make_int4(c, cnt - rem, rem, rem_r[c]);
+  };
+  for (int i = t; i < total; i += 1024) {
+    int s = 0;
+    while (seg_at[s + 1] <= i) ++s;
+    const int4 g = seg[s];
+    const int j = i - seg_at[s];
+    if (g.y < 0) {
+      put(full_tot + i, entry(ord[g.x + j]), none);
+    } else if (g.w) {
+      put(full_tot + i, entry(ord[g.x + 2 * j]), entry(ord[g.x + 2 * j + 1]));
+    } else {
+      put(full_tot + i, entry(ord[g.x + j]), entry(ord[g.y + j]));
+    }
+  }
+  for (int slot = full_tot + total + t; slot < items_per_head; slot += 1024) put(slot, none, none);
 }
 
 template <int D>
@@ -708,7 +888,8 @@ hipError_t attention_scratch(int4 **items) {
   return hipSuccess;
 }
 
-// Slots of one head: sum_c ceil(n_c / kBM) <= ceil(n / kBM) + c_q.
+// Work slots of one head: sum_c ceil(n_c / kBM) <= ceil(n / kBM) + c_q; each
+// slot is two int4 entries.
 int attn_items_per_head(int n, int c_q) { return (n + kBM - 1) / kBM + c_q; }
 
 hipError_t attention_run(int heads, int n, int d, bool bf16, const void *q,
@@ -717,8 +898,10 @@ hipError_t attention_run(int heads, int n, int d, bool bf16, const void *q,
                          const int32_t *sel_counts, const int32_t *sel_idx,
                          float scale, int4 *items, hipStream_t s) {
   const int iph = attn_items_per_head(n, c_q);
+  // remainder chunks share blocks only in the LDS-DMA kernel
+  const int pair = bf16 && d == 128 ? 1 : 0;
   hipLaunchKernelGGL(attn_items_kernel, dim3(heads), dim3(1024), 0, s, n, c_q,
-                     iph, offsets, sel_counts, items);
+                     iph, pair, offsets, sel_counts, items);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const float sl2 = scale * 1.4426950408889634f;

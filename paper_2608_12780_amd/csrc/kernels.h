@@ -152,7 +152,8 @@ hipError_t debug_fixexp(const float *y, uint64_t *out, int64_t count,
                         hipStream_t s);
 
 int attn_items_per_head(int n, int c_q);
-// Work-list entries of the no-allocation attention entry point (1 MiB).
+// 16-byte work-list entries of the no-allocation attention entry point
+// (1 MiB; two per work slot).
 constexpr size_t kAttnScratchItems = SCOPE_NOALLOC_MAX_WORK_ITEMS;
 // Device address of that work list on the current device (looked up once
 // per device).

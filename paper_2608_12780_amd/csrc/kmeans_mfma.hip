@@ -309,11 +309,12 @@ __device__ __forceinline__ void assign_slice(const SliceArgs &A, const uint16_t 
   for (int s = 0; s < KS; ++s) {
     const uint4 v4 = load_group8(xrow, 16 * s + 8 * hf, dx, valid, vec);
     const uint32_t wv[4] = {v4.x, v4.y, v4.z, v4.w};
+    // |x|^2 only sizes the margin: two squares per dot2 (each rounding
+    // within 2^-23 relative, far inside the 1e-4 slack below)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const float a = __uint_as_float(wv[q] << 16), b = __uint_as_float(wv[q] & 0xFFFF0000u);
-      ss = fmaf(a, a, ss);
-      ss = fmaf(b, b, ss);
+      const bf16x2 p2 = __builtin_bit_cast(bf16x2, wv[q]);
+      ss = __builtin_amdgcn_fdot2_f32_bf16(p2, p2, ss, false);
     }
     xf[s] = __builtin_bit_cast(bf16x8, v4);
   }

@@ -155,8 +155,9 @@ def test_noalloc_attention_validation():
     assert call(hy_shape(), scale=float("nan")) == INVALID
     assert call(hy_shape(), q=None) == INVALID
     assert call(hy_shape(), c_q=0) == INVALID
-    # heads * (ceil(n / 256) + c_q) work items against the fixed list
-    items = lambda sh, c_q: sh.heads * (-(-sh.n // 256) + c_q)
+    # heads * (ceil(n / 256) + c_q) work slots of two entries against the
+    # fixed list
+    items = lambda sh, c_q: 2 * sh.heads * (-(-sh.n // 256) + c_q)
     big = hy_shape(heads=96)
     assert items(big, 256) > 65536
     assert call(big) == 5
