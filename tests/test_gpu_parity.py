@@ -497,3 +497,48 @@ def test_extreme_small_shapes(grid, d, split, c_q, c_m, k_fix, dtype):
     gpu, ref = check_layer(cfg)
     if k_fix == n:
         assert (gpu["sel_counts"] == n).all()
+
+
+def _attention_case(sizes, keys, heads=2, d=128, seed=0):
+    """Sparse attention on a given clustering (cluster sizes, per cluster a
+    key count) with random permutation and random ascending key sets."""
+    rng = np.random.default_rng(seed)
+    n = int(sum(sizes))
+    c_q = len(sizes)
+    qkv = [G.bf16_round(rng.standard_normal((heads, n, d)).astype(np.float32) * s)
+           for s in (1.5, 1.5, 1.0)]
+    offsets = np.zeros((heads, c_q + 1), np.int32)
+    offsets[:, 1:] = np.cumsum(sizes)
+    perm = np.stack([rng.permutation(n) for _ in range(heads)]).astype(np.int32)
+    sel_counts = np.zeros((heads, c_q), np.int32)
+    sel_idx = np.zeros((heads, c_q, n), np.int32)
+    for h in range(heads):
+        for c, r in enumerate(keys):
+            r = int(min(r, n))
+            sel_counts[h, c] = r
+            sel_idx[h, c, :r] = np.sort(rng.choice(n, r, replace=False))
+    shape = B.make_shape(heads, n, d, B.BF16, ((0, 16, 72), (16, 56, 56)))
+    dev = [torch.from_numpy(a).cuda().to(torch.bfloat16) for a in qkv]
+    o = torch.empty_like(dev[0])
+    ws = B.alloc_workspace(shape, c_q, (8, 8, 8))
+    t = lambda a: torch.from_numpy(a).cuda()
+    B.scope_sparse_attention(shape, *dev, c_q, t(offsets), t(perm), t(sel_counts),
+                             t(sel_idx), 0.0, o, ws)
+    torch.cuda.synchronize()
+    ref = oracle.attention(*qkv, offsets, perm, sel_counts, sel_idx)
+    return G.assert_attention_close(o.float().cpu().numpy(), ref)
+
+
+def test_attention_pairs_remainder_chunks_of_every_width():
+    # clusters with 0-2 full 256-query chunks and remainders of every wave
+    # count 1..8 (1 .. 255 rows), several per count, with equal, close and
+    # very different key counts, so that the work list pairs remainders of
+    # complementary widths, leaves some alone and runs pairs whose key
+    # lists end at different tiles
+    rems = [1, 17, 32, 33, 60, 64, 65, 96, 97, 100, 128, 129, 150, 160, 161, 192,
+            193, 200, 224, 225, 240, 255, 5, 31, 70, 130, 190, 230, 40, 250, 3, 120]
+    sizes = [256 * (i % 3) + rm for i, rm in enumerate(rems)]
+    pool = [1, 63, 64, 65, 640, 640, 640, 641, 700, 1000, 2049, 5000]
+    keys = [pool[(7 * i) % len(pool)] for i in range(len(sizes))]
+    mx, mr = _attention_case(sizes, keys)
+    G.say(f"[parity] paired work slots: max-abs {mx:.3e} mean-rel {mr:.3e}")
