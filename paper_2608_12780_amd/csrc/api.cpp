@@ -484,8 +484,13 @@ int32_t cluster_key_subspaces(const scope_shape *shape, const void *k, const int
   // the three assignments in one pass over K when the codebooks fit the LDS
   // together, else one pass per subspace
   const bool fused = scope::km_assign3_ok(p);
+  bool args_stored = false;
   auto assign_all = [&]() -> hipError_t {
-    if (fused) return scope::km_assign3(p, w.args3, s);
+    if (fused) {
+      const hipError_t e = scope::km_assign3(p, w.args3, !args_stored, s);
+      args_stored = true;
+      return e;
+    }
     for (int m = 0; m < 3; ++m) {
       const hipError_t e = scope::km_assign(p[m], false, s);
       if (e != hipSuccess) return e;

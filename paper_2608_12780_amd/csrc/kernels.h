@@ -61,7 +61,10 @@ hipError_t km_group(const KmProblem &p, hipStream_t s);
 bool km_assign3_ok(const KmProblem (&p)[3]);
 // scratch: km_assign3_scratch_bytes() of device memory (its arguments)
 size_t km_assign3_scratch_bytes();
-hipError_t km_assign3(const KmProblem (&p)[3], void *scratch, hipStream_t s);
+// store_args: write the launch arguments to the scratch (once per call; the
+// later passes of the call reuse them)
+hipError_t km_assign3(const KmProblem (&p)[3], void *scratch, bool store_args,
+                      hipStream_t s);
 
 // Centroid update by one streaming pass over the rows.  Up to kMaxSub
 // subspaces of the same rows (channels col0[m] .. col0[m]+dx[m], C[m]

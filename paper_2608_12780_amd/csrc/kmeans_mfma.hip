@@ -126,9 +126,9 @@ __device__ __forceinline__ uint32_t asc_key(float f) {
 // wave per row: lanes split the channels, lane 0 keeps the norm's fma chain
 // in channel order.
 template <int DXP>
-__global__ __launch_bounds__(256) void km_prep_kernel(
-    const float *__restrict__ U, size_t u_hs, int C, int cpad, int dx,
-    uint16_t *ubf, float *nu, float *bnd) {
+__device__ __forceinline__ void km_prep_row(const float *__restrict__ U, size_t u_hs, int C,
+                                            int cpad, int dx, uint16_t *ubf, float *nu,
+                                            float *bnd) {
   const int h = blockIdx.y, lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= cpad) return;
@@ -176,6 +176,33 @@ __global__ __launch_bounds__(256) void km_prep_kernel(
     bnd[2 * row + 0] = static_cast<float>(sqrt(e2));
     bnd[2 * row + 1] = static_cast<float>(fmax(sqrt(n2), sqrt(h2) + sqrt(l2)));
   }
+}
+
+template <int DXP>
+__global__ __launch_bounds__(256) void km_prep_kernel(
+    const float *__restrict__ U, size_t u_hs, int C, int cpad, int dx,
+    uint16_t *ubf, float *nu, float *bnd) {
+  km_prep_row<DXP>(U, u_hs, C, cpad, dx, ubf, nu, bnd);
+}
+
+// The three subspaces' codebooks in one launch (blockIdx.z = subspace).
+struct Prep3 {
+  const float *U[3];
+  size_t u_hs[3];
+  int C[3], cpad[3], dx[3];
+  uint16_t *ubf[3];
+  float *nu[3], *bnd[3];
+};
+
+template <int D0, int D1, int D2>
+__global__ __launch_bounds__(256) void km_prep3_kernel(Prep3 P) {
+  const int m = blockIdx.z;
+  if (m == 0)
+    km_prep_row<D0>(P.U[0], P.u_hs[0], P.C[0], P.cpad[0], P.dx[0], P.ubf[0], P.nu[0], P.bnd[0]);
+  else if (m == 1)
+    km_prep_row<D1>(P.U[1], P.u_hs[1], P.C[1], P.cpad[1], P.dx[1], P.ubf[1], P.nu[1], P.bnd[1]);
+  else
+    km_prep_row<D2>(P.U[2], P.u_hs[2], P.C[2], P.cpad[2], P.dx[2], P.ubf[2], P.nu[2], P.bnd[2]);
 }
 
 // Keeps the compiler from moving this wave's LDS accesses across the call
@@ -862,7 +889,26 @@ hipError_t launch_mfma(const KmProblem &p, bool with_hist, hipStream_t s) {
 __global__ void store_sub3_kernel(Sub3 S, Sub3 *dst) { *dst = S; }
 
 template <int D0, int D1, int D2>
-hipError_t launch_mfma3(const KmProblem (&p)[3], Sub3 *dev_args, hipStream_t s) {
+hipError_t launch_mfma3(const KmProblem (&p)[3], Sub3 *dev_args, bool store_args,
+                        hipStream_t s) {
+  // the three codebooks' two-term splits, norms and bound parts
+  Prep3 P{};
+  int cmax = 0;
+  for (int m = 0; m < 3; ++m) {
+    P.U[m] = p[m].u;
+    P.u_hs[m] = p[m].u_head_stride;
+    P.C[m] = p[m].C;
+    P.cpad[m] = p[m].cpad;
+    P.dx[m] = p[m].dx;
+    P.ubf[m] = p[m].ubf;
+    P.nu[m] = p[m].nu;
+    P.bnd[m] = p[m].bnd;
+    cmax = p[m].cpad > cmax ? p[m].cpad : cmax;
+  }
+  hipLaunchKernelGGL((km_prep3_kernel<D0, D1, D2>), dim3((cmax + 3) / 4, p[0].heads, 3),
+                     dim3(256), 0, s, P);
+  hipError_t e0 = hipGetLastError();
+  if (e0 != hipSuccess) return e0;
   Sub3 S{};
   int uoff = 0, noff = 0;
   const int dxp[3] = {D0, D1, D2};
@@ -903,30 +949,16 @@ hipError_t launch_mfma3(const KmProblem (&p)[3], Sub3 *dev_args, hipStream_t s) 
     cus = 256;
   const int blocks = static_cast<int>(slices < static_cast<long long>(cus) * kWavesPerBlock
                                           ? (slices + kWavesPerBlock - 1) / kWavesPerBlock : cus);
-  // the arguments go to device memory, so each wave group loads only its own
-  hipLaunchKernelGGL(store_sub3_kernel, dim3(1), dim3(1), 0, s, S, dev_args);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  // the arguments go to device memory, so each wave group loads only its
+  // own; they hold only pointers and sizes, so one store per call suffices
+  if (store_args) {
+    hipLaunchKernelGGL(store_sub3_kernel, dim3(1), dim3(1), 0, s, S, dev_args);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   hipLaunchKernelGGL((km_assign_mfma3_kernel<D0, D1, D2>), dim3(blocks), dim3(64 * kWavesPerBlock),
                      0, s, dev_args, p[0].n, p[0].heads);
   return hipGetLastError();
-}
-
-template <int DXP>
-hipError_t prep(const KmProblem &p, hipStream_t s) {
-  hipLaunchKernelGGL(km_prep_kernel<DXP>, dim3((p.cpad + 3) / 4, p.heads), dim3(256), 0, s, p.u,
-                     p.u_head_stride, p.C, p.cpad, p.dx, p.ubf, p.nu, p.bnd);
-  return hipGetLastError();
-}
-
-hipError_t prep_any(const KmProblem &p, hipStream_t s) {
-  switch (p.dxp) {
-    case 16: return prep<16>(p, s);
-    case 32: return prep<32>(p, s);
-    case 48: return prep<48>(p, s);
-    case 64: return prep<64>(p, s);
-    default: return prep<128>(p, s);
-  }
 }
 
 }  // namespace
@@ -949,16 +981,13 @@ bool km_assign3_ok(const KmProblem (&p)[3]) {
 
 size_t km_assign3_scratch_bytes() { return sizeof(Sub3); }
 
-hipError_t km_assign3(const KmProblem (&p)[3], void *scratch, hipStream_t s) {
-  for (int m = 0; m < 3; ++m) {
-    const hipError_t e = prep_any(p[m], s);
-    if (e != hipSuccess) return e;
-  }
+hipError_t km_assign3(const KmProblem (&p)[3], void *scratch, bool store_args,
+                      hipStream_t s) {
   Sub3 *args = static_cast<Sub3 *>(scratch);
   const int a = p[0].dxp, b = p[1].dxp;
-  if (a == 16 && b == 64) return launch_mfma3<16, 64, 64>(p, args, s);
-  if (a == 48) return launch_mfma3<48, 48, 48>(p, args, s);
-  return launch_mfma3<16, 32, 32>(p, args, s);
+  if (a == 16 && b == 64) return launch_mfma3<16, 64, 64>(p, args, store_args, s);
+  if (a == 48) return launch_mfma3<48, 48, 48>(p, args, store_args, s);
+  return launch_mfma3<16, 32, 32>(p, args, store_args, s);
 }
 
 int km_cpad(int C) { return (C + 31) / 32 * 32; }
