@@ -386,7 +386,8 @@ __device__ __forceinline__ void assign_slice(const SliceArgs &A, const uint16_t 
   auto fold = [&](const f32x16 &acc, int rb) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
-      const uint32_t ru = static_cast<uint32_t>(rb + 8 * (e >> 2) + (e & 3));
+      const uint32_t ru = static_cast<uint32_t>(
+          __builtin_amdgcn_readfirstlane(rb + 8 * (e >> 2) + (e & 3)));
       const float sp = __uint_as_float((__float_as_uint(acc[e]) & vmask) | ru);
       m3 = __builtin_amdgcn_fmed3f(m2, m3, sp);
       m2 = __builtin_amdgcn_fmed3f(m1, m2, sp);

@@ -520,7 +520,11 @@ def _attention_case(sizes, keys, heads=2, d=128, seed=0):
     shape = B.make_shape(heads, n, d, B.BF16, ((0, 16, 72), (16, 56, 56)))
     dev = [torch.from_numpy(a).cuda().to(torch.bfloat16) for a in qkv]
     o = torch.empty_like(dev[0])
-    ws = B.alloc_workspace(shape, c_q, (8, 8, 8))
+    # the attention call needs only its work list: two 16-byte entries per
+    # slot, heads * (ceil(n / 256) + c_q) slots (clustering with this many
+    # clusters is beyond the workspace-size call)
+    ws = torch.empty(2 * heads * (-(-n // 256) + c_q) * 16 + 256, dtype=torch.uint8,
+                     device="cuda")
     t = lambda a: torch.from_numpy(a).cuda()
     B.scope_sparse_attention(shape, *dev, c_q, t(offsets), t(perm), t(sel_counts),
                              t(sel_idx), 0.0, o, ws)
@@ -542,3 +546,14 @@ def test_attention_pairs_remainder_chunks_of_every_width():
     keys = [pool[(7 * i) % len(pool)] for i in range(len(sizes))]
     mx, mr = _attention_case(sizes, keys)
     G.say(f"[parity] paired work slots: max-abs {mx:.3e} mean-rel {mr:.3e}")
+
+
+def test_attention_remainders_alone_above_the_pairing_limit():
+    # more clusters than the work list pairs (2,048): every remainder chunk
+    # runs alone, after the full chunks
+    rng = np.random.default_rng(11)
+    sizes = [int(x) for x in rng.integers(0, 9, 2100)]
+    sizes[5], sizes[700] = 300, 600
+    keys = [int(x) for x in rng.integers(1, 200, 2100)]
+    mx, mr = _attention_case(sizes, keys, heads=1, seed=2)
+    G.say(f"[parity] {len(sizes)} clusters, unpaired remainders: max-abs {mx:.3e} mean-rel {mr:.3e}")
