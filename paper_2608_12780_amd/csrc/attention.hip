@@ -673,7 +673,8 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
 // waves together: bucketed by their wave count w and ordered by key count
 // within a bucket, bucket w (largest first) takes partners from bucket
 // min(8 - w, w) down to 1 in key-count order, so paired chunks run similar
-// numbers of key tiles.  Remainders left without a partner run alone.
+// numbers of key tiles.  Remainders left without a partner (among them every
+// remainder of 8 waves) run alone.
 constexpr int kPairMaxClusters = 2048;  // pairing up to this many clusters
 __global__ __launch_bounds__(1024) void attn_items_kernel(
     int n, int c_q, int items_per_head, int pair, const int32_t *__restrict__ offsets,
@@ -682,7 +683,7 @@ __global__ __launch_bounds__(1024) void attn_items_kernel(
   __shared__ int rem_w[kPairMaxClusters], rem_r[kPairMaxClusters], ord[kPairMaxClusters];
   __shared__ int bucket_n[kNW + 1], bucket_at[kNW + 1];
   __shared__ int4 seg[64];   // (A's first ordinal, B's first ordinal or -1, count, same bucket)
-  __shared__ int seg_at[65], nseg, full_tot, rem_tot;
+  __shared__ int seg_at[65], nseg, full_tot;
   const int h = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int32_t *off = offsets + static_cast<size_t>(h) * (c_q + 1);
   const int32_t *scnt = sel_counts + static_cast<size_t>(h) * c_q;
@@ -764,7 +765,6 @@ __global__ __launch_bounds__(1024) void attn_items_kernel(
       bucket_at[b] = a;
       a += b == 0 ? 0 : bucket_n[b];
     }
-    rem_tot = a;
   }
   __syncthreads();
   for (int c = t; c < c_q; c += 1024) {
