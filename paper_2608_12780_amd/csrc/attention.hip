@@ -68,9 +68,10 @@ __device__ __forceinline__ uint4 load8(const void *base, size_t elem) {
 }
 
 // Work items run in list order: heads one after the other and, within a
-// head, clusters in order with their row chunks adjacent.  All XCDs work on
-// the same head at a time, so one head's K/V (60 MB at 118800 x 128 bf16) is
-// what the 256 MB memory-side cache has to hold.
+// head, by estimated cost, largest first, with a cluster's row chunks
+// adjacent.  All XCDs work on the same head at a time, so one head's K/V
+// (60 MB at 118800 x 128 bf16) is what the 256 MB memory-side cache has to
+// hold.
 //
 // Block b runs on XCD b mod 8.  Runs of kRun consecutive work items (the
 // chunks of one cluster, which gather the same K/V rows) go to one XCD so
@@ -674,8 +675,13 @@ __global__ __launch_bounds__(kNW * 64) void attn_kernel_dma(
 // within a bucket, bucket w (largest first) takes partners from bucket
 // min(8 - w, w) down to 1 in key-count order, so paired chunks run similar
 // numbers of key tiles.  Remainders left without a partner (among them every
-// remainder of 8 waves) run alone.
+// remainder of 8 waves) run alone.  Up to kSortMaxSlots slots per head, the
+// head's slots are then reordered by estimated cost, largest first (ties
+// keep their order, so a cluster's full chunks stay adjacent): the
+// expensive blocks of each head start early and the cheap ones fill in
+// behind them, which shortens the launch's tail.
 constexpr int kPairMaxClusters = 2048;  // pairing up to this many clusters
+constexpr int kSortMaxSlots = 2048;     // cost-ordered work lists up to this many slots
 __global__ __launch_bounds__(1024) void attn_items_kernel(
     int n, int c_q, int items_per_head, int pair, const int32_t *__restrict__ offsets,
     const int32_t *__restrict__ sel_counts, int4 *items) {
@@ -684,17 +690,54 @@ __global__ __launch_bounds__(1024) void attn_items_kernel(
   __shared__ int bucket_n[kNW + 1], bucket_at[kNW + 1];
   __shared__ int4 seg[64];   // (A's first ordinal, B's first ordinal or -1, count, same bucket)
   __shared__ int seg_at[65], nseg, full_tot;
+  __shared__ int4 staged[2 * kSortMaxSlots];
+  __shared__ unsigned long long cost[kSortMaxSlots];
   const int h = blockIdx.x, t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int32_t *off = offsets + static_cast<size_t>(h) * (c_q + 1);
   const int32_t *scnt = sel_counts + static_cast<size_t>(h) * c_q;
   int4 *out = items + static_cast<size_t>(h) * items_per_head * 2;
   const bool do_pair = pair && c_q <= kPairMaxClusters;
+  const bool sorted = items_per_head <= kSortMaxSlots;
   auto count_of = [&](int c) { return min(max(off[c + 1] - off[c], 0), n); };
   auto keys_of = [&](int c) { return min(max(scnt[c], 0), n); };
   auto put = [&](int slot, int4 a, int4 b) {
     if (slot < items_per_head) {
-      out[2 * slot] = a;
-      out[2 * slot + 1] = b;
+      if (sorted) {
+        staged[2 * slot] = a;
+        staged[2 * slot + 1] = b;
+      } else {
+        out[2 * slot] = a;
+        out[2 * slot + 1] = b;
+      }
+    }
+  };
+  // the staged slots, largest estimated cost first: a slot costs its key
+  // tiles times the per-tile time of its wave count (about 1.45x for 5-8
+  // waves against 1-4) and of a second chunk's gathers (about 1.15x).  The
+  // first `used` slots hold chunks; the empty ones after them stay in place.
+  auto emit_sorted = [&](int used) {
+    if (!sorted) return;
+    __syncthreads();
+    for (int i = t; i < used; i += 1024) {
+      const int4 a = staged[2 * i], b = staged[2 * i + 1];
+      const int ta = (a.w + kBN - 1) / kBN, tb = b.z > 0 ? (b.w + kBN - 1) / kBN : 0;
+      const int waves = (a.z + 31) / 32 + (b.z > 0 ? (b.z + 31) / 32 : 0);
+      const uint32_t per = waves > 4 ? (b.z > 0 ? 196u : 171u) : (b.z > 0 ? 135u : 118u);
+      const uint32_t k = static_cast<uint32_t>(ta > tb ? ta : tb) * per;
+      // descending cost, then ascending slot: one unsigned comparison
+      cost[i] = (static_cast<unsigned long long>(k) << 32) | static_cast<uint32_t>(~i);
+    }
+    __syncthreads();
+    for (int i = t; i < items_per_head; i += 1024) {
+      int rank = i;
+      if (i < used) {
+        const unsigned long long ci = cost[i];
+        rank = 0;
+#pragma unroll 8
+        for (int j = 0; j < used; ++j) rank += cost[j] > ci ? 1 : 0;
+      }
+      out[2 * rank] = staged[2 * i];
+      out[2 * rank + 1] = staged[2 * i + 1];
     }
   };
   const int4 none = make_int4(0, 0, 0, 0);
@@ -755,6 +798,7 @@ __global__ __launch_bounds__(1024) void attn_items_kernel(
       at += tot;
     }
     for (int slot = full_tot + at + t; slot < items_per_head; slot += 1024) put(slot, none, none);
+    emit_sorted(min(full_tot + at, items_per_head));
     return;
   }
   // ordinal of each remainder within (bucket ascending, keys ascending,
@@ -833,6 +877,7 @@ __global__ __launch_bounds__(1024) void attn_items_kernel(
     }
   }
   for (int slot = full_tot + total + t; slot < items_per_head; slot += 1024) put(slot, none, none);
+  emit_sorted(min(full_tot + total, items_per_head));
 }
 
 template <int D>
