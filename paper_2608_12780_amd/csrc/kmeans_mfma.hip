@@ -30,8 +30,10 @@
 // canonical (score, r) wins, so equal scores keep the lowest index.
 //
 // Blocks are persistent per head: the two-term codebook is staged in LDS
-// once, then each wave independently takes 32-point slices; chunk
-// histograms for the grouping are accumulated with global atomics.
+// once, then each wave independently takes the block's next 32-point slice
+// from a counter in LDS (so a wave slowed by a re-score does not hold up the
+// others); chunk histograms for the grouping are accumulated with global
+// atomics.
 #include <math.h>
 
 #include "common.h"
@@ -529,6 +531,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
   __shared__ unsigned long long best[kWavesPerBlock][32];
   __shared__ int ncand[kWavesPerBlock];
   __shared__ float red[3][kWavesPerBlock];
+  __shared__ int next_slice;
   const int w = threadIdx.x >> 6;
   const SliceArgs A{X, x_hs, ld, col0, dx, n, C, cpad, U, u_hs, assign, a_hs, chunk_hist, nchunks};
   const int nslices = (n + 31) / 32;
@@ -543,29 +546,36 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma_kernel(
     const long long seg_end = end < static_cast<long long>(h + 1) * nslices
                                   ? end : static_cast<long long>(h + 1) * nslices;
     __syncthreads();
+    if (threadIdx.x == 0) next_slice = 0;  // visible after the staging barrier
     const FilterBound B = stage_codebook<DXP>(Us, nus, nhs, red, ubf, nu, bnd, h, C, cpad);
-    for (long long g = beg + w; g < seg_end; g += kWavesPerBlock)
+    // a wave that is done takes the block's next slice
+    const long long count = seg_end - beg;
+    for (;;) {
+      int u = 0;
+      if ((threadIdx.x & 63) == 0) u = atomicAdd(&next_slice, 1);
+      u = __builtin_amdgcn_readfirstlane(__shfl(u, 0));
+      if (u >= count) break;
+      const long long g = beg + u;
       assign_slice<DXP>(A, Us, nus, nhs, B, h, static_cast<int>(g - static_cast<long long>(h) * nslices),
                         cand[w], best[w], &ncand[w]);
+    }
     beg = seg_end;
   }
 }
 
 // The three key subspaces in one pass over the rows: their codebooks are
 // staged in LDS side by side (subspace m at element offset uoff[m] and norm
-// offset noff[m]), and the block's waves are split into three groups, group
-// m assigning subspace m over the block's slices.  The groups walk the same
-// slices in the same order, so a row fetched from HBM by one group is found
-// in cache by the others, and each wave keeps the registers of a single
-// codebook width.  Group sizes follow the subspaces' work (wave0[m] is the
-// first wave of group m, wave0[3] = the block's wave count).
+// offset noff[m]), and the block's waves take work units (slice, subspace)
+// from a counter in LDS, in slice order.  A wave that is done takes the next
+// unit whatever its subspace, so the subspaces' different costs balance
+// out, and the three units of a slice start at about the same time, so a
+// row fetched from HBM for one is found in cache by the others.
 struct Sub3 {
   SliceArgs a[3];
   const uint16_t *ubf[3];
   const float *nu[3];
   const float *bnd[3];
   int uoff[3], noff[3];
-  int wave0[4];
 };
 
 template <int D0, int D1, int D2>
@@ -578,6 +588,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma3_kernel(
   __shared__ unsigned long long best[kWavesPerBlock][32];
   __shared__ int ncand[kWavesPerBlock];
   __shared__ float red[3][3][kWavesPerBlock];
+  __shared__ int next_unit;
   const int w = threadIdx.x >> 6;
   const int nslices = (n + 31) / 32;
   const long long total = static_cast<long long>(heads) * nslices;
@@ -589,6 +600,7 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma3_kernel(
     const long long seg_end = end < static_cast<long long>(h + 1) * nslices
                                   ? end : static_cast<long long>(h + 1) * nslices;
     __syncthreads();
+    if (threadIdx.x == 0) next_unit = 0;  // visible after the staging barriers
     stage_codebook<D0>(Us + Sp->uoff[0], nus + Sp->noff[0], nhs + Sp->noff[0], red[0], Sp->ubf[0], Sp->nu[0],
                        Sp->bnd[0], h, Sp->a[0].C, Sp->a[0].cpad);
     stage_codebook<D1>(Us + Sp->uoff[1], nus + Sp->noff[1], nhs + Sp->noff[1], red[1], Sp->ubf[1], Sp->nu[1],
@@ -596,26 +608,26 @@ __global__ __launch_bounds__(64 * kWavesPerBlock) void km_assign_mfma3_kernel(
     stage_codebook<D2>(Us + Sp->uoff[2], nus + Sp->noff[2], nhs + Sp->noff[2], red[2], Sp->ubf[2], Sp->nu[2],
                        Sp->bnd[2], h, Sp->a[2].C, Sp->a[2].cpad);
     const long long first = static_cast<long long>(h) * nslices;
-    const int m = w < Sp->wave0[1] ? 0 : w < Sp->wave0[2] ? 1 : 2;
-    const int wi = w - Sp->wave0[m], nw = Sp->wave0[m + 1] - Sp->wave0[m];
-    if (m == 0) {
-      const SliceArgs A = Sp->a[0];
-      const FilterBound B = reduce_bound<kWavesPerBlock>(red[0]);
-      for (long long g = beg + wi; g < seg_end; g += nw)
-        assign_slice<D0>(A, Us + Sp->uoff[0], nus + Sp->noff[0], nhs + Sp->noff[0], B, h, static_cast<int>(g - first),
-                         cand[w], best[w], &ncand[w]);
-    } else if (m == 1) {
-      const SliceArgs A = Sp->a[1];
-      const FilterBound B = reduce_bound<kWavesPerBlock>(red[1]);
-      for (long long g = beg + wi; g < seg_end; g += nw)
-        assign_slice<D1>(A, Us + Sp->uoff[1], nus + Sp->noff[1], nhs + Sp->noff[1], B, h, static_cast<int>(g - first),
-                         cand[w], best[w], &ncand[w]);
-    } else {
-      const SliceArgs A = Sp->a[2];
-      const FilterBound B = reduce_bound<kWavesPerBlock>(red[2]);
-      for (long long g = beg + wi; g < seg_end; g += nw)
-        assign_slice<D2>(A, Us + Sp->uoff[2], nus + Sp->noff[2], nhs + Sp->noff[2], B, h, static_cast<int>(g - first),
-                         cand[w], best[w], &ncand[w]);
+    const FilterBound B0 = reduce_bound<kWavesPerBlock>(red[0]);
+    const FilterBound B1 = reduce_bound<kWavesPerBlock>(red[1]);
+    const FilterBound B2 = reduce_bound<kWavesPerBlock>(red[2]);
+    const long long units = 3 * (seg_end - beg);
+    for (;;) {
+      int u = 0;
+      if ((threadIdx.x & 63) == 0) u = atomicAdd(&next_unit, 1);
+      u = __builtin_amdgcn_readfirstlane(__shfl(u, 0));
+      if (u >= units) break;
+      const long long g = beg + u / 3;
+      const int m = u - 3 * (u / 3);
+      if (m == 0)
+        assign_slice<D0>(Sp->a[0], Us + Sp->uoff[0], nus + Sp->noff[0], nhs + Sp->noff[0], B0, h,
+                         static_cast<int>(g - first), cand[w], best[w], &ncand[w]);
+      else if (m == 1)
+        assign_slice<D1>(Sp->a[1], Us + Sp->uoff[1], nus + Sp->noff[1], nhs + Sp->noff[1], B1, h,
+                         static_cast<int>(g - first), cand[w], best[w], &ncand[w]);
+      else
+        assign_slice<D2>(Sp->a[2], Us + Sp->uoff[2], nus + Sp->noff[2], nhs + Sp->noff[2], B2, h,
+                         static_cast<int>(g - first), cand[w], best[w], &ncand[w]);
     }
     beg = seg_end;
   }
@@ -926,26 +938,6 @@ hipError_t launch_mfma3(const KmProblem (&p)[3], Sub3 *dev_args, bool store_args
     uoff += q.cpad * (2 * dxp[m] + 8);
     noff += q.cpad;
   }
-  // waves per group in proportion to each subspace's work per slice: the
-  // fold (per centroid) plus the matrix products (per centroid and 16
-  // channels, two terms), at least two waves each.  A k-step's two MFMAs
-  // take a quarter of a fold's issue cycles, but weighting them at one half
-  // (3, 6 and 7 waves for channel ranges of 16, 56 and 56 at 128 centroids,
-  // against 4, 6 and 6) measured 3.5% faster over the key stage.
-  double work[3], tot = 0.0;
-  for (int m = 0; m < 3; ++m) {
-    work[m] = p[m].cpad * (1.0 + 0.5 * dxp[m] / 16.0);
-    tot += work[m];
-  }
-  S.wave0[0] = 0;
-  for (int m = 0; m < 2; ++m) {
-    int wm = static_cast<int>(work[m] / tot * kWavesPerBlock + 0.5);
-    wm = wm < 2 ? 2 : wm;
-    S.wave0[m + 1] = S.wave0[m] + wm;
-  }
-  if (S.wave0[2] > kWavesPerBlock - 2) S.wave0[2] = kWavesPerBlock - 2;
-  if (S.wave0[1] > S.wave0[2] - 2) S.wave0[1] = S.wave0[2] - 2;
-  S.wave0[3] = kWavesPerBlock;
   const long long slices = static_cast<long long>(p[0].heads) * ((p[0].n + 31) / 32);
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
