@@ -348,6 +348,23 @@ int32_t scope_debug_mfma_loop(float *out, int32_t blocks, int32_t iters,
 int32_t scope_debug_fixexp(const float *y, uint64_t *out, int64_t count,
                            void *stream);
 
+/* Diagnostic: the work list of call 5 for `heads` heads, as the sparse
+ * attention builds it.  offsets [heads][c_q + 1] and sel_counts
+ * [heads][c_q] (device) are as for scope_sparse_attention.  *items_per_head
+ * (host) receives S, the slots per head; items (device, 16-byte aligned,
+ * `capacity` int32 values, at least heads * S * 8) receives
+ * [heads][S][2][4] int32: each slot holds two entries (cluster, first row,
+ * rows, selected keys) run by one block, the second with rows = 0 when the
+ * block runs one chunk, and slots with both entries empty after the used
+ * ones.  pair != 0 lets two remainder chunks share a slot, as the bf16,
+ * d = 128 kernel does.  Returns SCOPE_ERR_INVALID_ARGUMENT on bad sizes or
+ * pointers, before any launch.                                              */
+int32_t scope_debug_attention_items(int32_t heads, int32_t n, int32_t c_q,
+                                    int32_t pair, const int32_t *offsets,
+                                    const int32_t *sel_counts, int32_t *items,
+                                    int64_t capacity, int32_t *items_per_head,
+                                    void *stream);
+
 #ifdef __cplusplus
 }
 #endif

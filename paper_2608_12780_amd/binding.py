@@ -28,6 +28,7 @@ ENTRY_POINTS = (
     "scope_proxy_scores_partition", "scope_select_partition",
     "scope_sparse_attention_noalloc", "scope_debug_copy", "scope_debug_mfma_loop",
     "scope_cluster_queries_warm", "scope_cluster_key_subspaces_warm",
+    "scope_debug_attention_items",
 )
 MAX_SUBSPACES, MAX_D = 8, 128
 POLICIES = {"online": 0, "fixed": 1, "topp": 2}
@@ -112,6 +113,8 @@ def lib() -> ctypes.CDLL:
         L.scope_debug_fixexp.argtypes = [P, P, ctypes.c_int64, P]
         L.scope_debug_copy.argtypes = [P, P, Z, P]
         L.scope_debug_mfma_loop.argtypes = [P, I, I, P]
+        L.scope_debug_attention_items.argtypes = [I, I, I, I, P, P, P, ctypes.c_int64,
+                                                  ctypes.POINTER(I), P]
         PP = ctypes.POINTER(Partition)
         L.scope_partition_workspace_size.argtypes = [SP, I, PP, ctypes.POINTER(Z)]
         L.scope_cluster_key_partition.argtypes = [SP, P, PP, I, P, I, P, P, P, Z, P, P]
@@ -332,6 +335,21 @@ def scope_debug_mfma_loop(out, blocks, iters, stream=None):
     _check("scope_debug_mfma_loop", lib().scope_debug_mfma_loop(
         _ptr(out, torch.float32, int(blocks) * 256, "out"), int(blocks), int(iters),
         _stream(stream)))
+
+
+def scope_debug_attention_items(heads, n, c_q, offsets, sel_counts, pair=True, stream=None):
+    """The sparse attention's work list: an int32 device tensor
+    [heads][slots][2][4] of (cluster, first row, rows, selected keys)."""
+    s = ctypes.c_int32(0)
+    slots = -(-int(n) // 256) + int(c_q)
+    items = torch.empty(int(heads) * slots * 8, dtype=torch.int32, device=offsets.device)
+    _check("scope_debug_attention_items", lib().scope_debug_attention_items(
+        int(heads), int(n), int(c_q), 1 if pair else 0,
+        _ptr(offsets, torch.int32, int(heads) * (int(c_q) + 1), "offsets"),
+        _ptr(sel_counts, torch.int32, int(heads) * int(c_q), "sel_counts"),
+        _ptr(items, torch.int32, None, "items"), items.numel(), ctypes.byref(s),
+        _stream(stream)))
+    return items.view(int(heads), s.value, 2, 4)
 
 
 def scope_debug_fixexp(y, out, stream=None):

@@ -878,6 +878,25 @@ int32_t scope_debug_mfma_loop(float *out, int32_t blocks, int32_t iters, void *s
   return SCOPE_OK;
 }
 
+int32_t scope_debug_attention_items(int32_t heads, int32_t n, int32_t c_q, int32_t pair,
+                                    const int32_t *offsets, const int32_t *sel_counts,
+                                    int32_t *items, int64_t capacity,
+                                    int32_t *items_per_head, void *stream) {
+  if (heads < 1 || heads > 65535 || n < 1 || n > kMaxN || c_q < 1 || c_q > n)
+    return SCOPE_ERR_INVALID_ARGUMENT;
+  if (!offsets || !sel_counts || !items || !items_per_head ||
+      reinterpret_cast<uintptr_t>(items) % 16)
+    return SCOPE_ERR_INVALID_ARGUMENT;
+  const int iph = scope::attn_items_per_head(n, c_q);
+  if (capacity < 0 || static_cast<uint64_t>(capacity) < 8ull * heads * iph)
+    return SCOPE_ERR_INVALID_ARGUMENT;
+  *items_per_head = iph;
+  SCOPE_TRY(scope::attention_items(heads, n, c_q, pair != 0, offsets, sel_counts,
+                                   reinterpret_cast<int4 *>(items),
+                                   static_cast<hipStream_t>(stream)));
+  return SCOPE_OK;
+}
+
 int32_t scope_debug_fixexp(const float *y, uint64_t *out, int64_t count,
                            void *stream) {
   if (count < 0 || (count > 0 && (!y || !out))) return SCOPE_ERR_INVALID_ARGUMENT;

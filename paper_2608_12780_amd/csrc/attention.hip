@@ -937,6 +937,13 @@ hipError_t attention_scratch(int4 **items) {
 // slot is two int4 entries.
 int attn_items_per_head(int n, int c_q) { return (n + kBM - 1) / kBM + c_q; }
 
+hipError_t attention_items(int heads, int n, int c_q, bool pair, const int32_t *offsets,
+                           const int32_t *sel_counts, int4 *items, hipStream_t s) {
+  hipLaunchKernelGGL(attn_items_kernel, dim3(heads), dim3(1024), 0, s, n, c_q,
+                     attn_items_per_head(n, c_q), pair ? 1 : 0, offsets, sel_counts, items);
+  return hipGetLastError();
+}
+
 hipError_t attention_run(int heads, int n, int d, bool bf16, const void *q,
                          const void *k, const void *v, void *o, int c_q,
                          const int32_t *offsets, const int32_t *perm,

@@ -161,6 +161,9 @@ constexpr size_t kAttnScratchItems = SCOPE_NOALLOC_MAX_WORK_ITEMS;
 // Device address of that work list on the current device (looked up once
 // per device).
 hipError_t attention_scratch(int4 **items);
+// The work list alone (as attention_run builds it), for diagnostics.
+hipError_t attention_items(int heads, int n, int c_q, bool pair, const int32_t *offsets,
+                           const int32_t *sel_counts, int4 *items, hipStream_t s);
 hipError_t attention_run(int heads, int n, int d, bool bf16, const void *q,
                          const void *k, const void *v, void *o, int c_q,
                          const int32_t *offsets, const int32_t *perm,

@@ -178,6 +178,27 @@ def test_proxy_scores_and_fixexp_validation():
     assert L.scope_debug_fixexp(None, None, 0, None) == OK   # empty: no launch
 
 
+def test_work_list_diagnostic_validation():
+    L = B.lib()
+    S = ctypes.c_int32(-1)
+    slots = -(-118800 // 256) + 256
+    need = 24 * slots * 8
+    call = lambda heads=24, n=118800, c_q=256, off=FAKE, sel=FAKE, items=FAKE, cap=need, s=S: \
+        L.scope_debug_attention_items(heads, n, c_q, 1, off, sel, items, cap,
+                                      None if s is None else ctypes.byref(s), None)
+    assert call(heads=0) == INVALID
+    assert call(n=0) == INVALID
+    assert call(c_q=0) == INVALID
+    assert call(c_q=118801) == INVALID          # more clusters than rows
+    assert call(off=None) == INVALID
+    assert call(sel=None) == INVALID
+    assert call(items=None) == INVALID
+    assert call(items=ctypes.c_void_p((1 << 20) + 4)) == INVALID   # not 16-byte aligned
+    assert call(cap=need - 1) == INVALID
+    assert call(s=None) == INVALID
+    assert S.value == -1                        # nothing written before a rejection
+
+
 def test_binding_rejects_host_tensors():
     torch = pytest.importorskip("torch")
     sh = hy_shape(heads=1, n=64, d=64, ranges=((0, 16, 40), (16, 24, 24)))
