@@ -147,10 +147,19 @@ __device__ __forceinline__ void km_prep_row(const float *__restrict__ U, size_t 
   }
   const float *u = U + h * u_hs + static_cast<size_t>(r) * dx;
   double e2 = 0.0, n2 = 0.0, h2 = 0.0, l2 = 0.0;
-  for (int c = lane; c < DXP; c += 64) {
+  float xs[(DXP + 63) / 64];  // channel lane + 64 j of the row, 0 past dx
+#pragma unroll
+  for (int j = 0; j < (DXP + 63) / 64; ++j) {
+    const int c = lane + 64 * j;
+    xs[j] = c < dx ? u[c] : 0.0f;
+  }
+#pragma unroll
+  for (int j = 0; j < (DXP + 63) / 64; ++j) {
+    const int c = lane + 64 * j;
+    if (c >= DXP) break;
     uint16_t bh = 0, bl = 0;
     if (c < dx) {
-      const float x = u[c];
+      const float x = xs[j];
       bh = to_bf16(x);
       const float rest = x - bf16_to_f32(bh);  // exact
       bl = to_bf16(rest);
@@ -171,9 +180,18 @@ __device__ __forceinline__ void km_prep_row(const float *__restrict__ U, size_t 
     h2 += __shfl_xor(h2, o);
     l2 += __shfl_xor(l2, o);
   }
+  // the canonical norm: one fma per channel in channel order, each channel
+  // taken from the lane that loaded it
+  float nr = 0.0f;
+#pragma unroll
+  for (int j = 0; j < (DXP + 63) / 64; ++j) {
+    const int cend = dx - 64 * j < 64 ? dx - 64 * j : 64;
+    for (int c = 0; c < cend; ++c) {
+      const float v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(xs[j]), c));
+      nr = fmaf(v, v, nr);
+    }
+  }
   if (lane == 0) {
-    float nr = 0.0f;
-    for (int c = 0; c < dx; ++c) nr = fmaf(u[c], u[c], nr);
     nu[row] = nr;
     bnd[2 * row + 0] = static_cast<float>(sqrt(e2));
     bnd[2 * row + 1] = static_cast<float>(fmax(sqrt(n2), sqrt(h2) + sqrt(l2)));
